@@ -1,0 +1,279 @@
+"""Plain CPU Kernel K-means oracle — TEST INFRASTRUCTURE, not part of the engine.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import or run anything in this directory.  The GPU engine
+(``paper_2601_17136_amd``) shares no code with it and never calls it.
+
+Everything is evaluated from the definitions of Section II-B of the paper
+(Eqs. 1-8), in double precision, from the same single-precision points, cluster
+ids and kernel parameters the engine receives.  Kernel entries come from the
+small C evaluator ``kkm_ref.c`` (direct definition of each kernel function,
+fp64); every clustering step below is NumPy on those fp64 values.
+
+Naming.  The paper's point matrix P is ``X`` here.  Its assignment matrix V
+(Eq. 3) holds 1/|L_j| in one entry per column; this oracle keeps the one-hot
+(unnormalised) form, so
+  * ``E[i, j] = sum_{m in L_j} K[i, m]``   (the paper's E of Eq. 4 times |L_j|),
+  * ``z[j]    = ||mu_j||^2``               (the paper's c of Eqs. 6-7),
+  * ``D[i, j] = K[i, i] - 2 E[i, j]/|L_j| + z[j]``  (Eq. 8 plus diag K, which
+    Eq. 8 leaves out; adding a per-row constant does not move the argmin, and
+    with it D is the true squared feature-space distance),
+  * ``J(cl)   = sum_i D[i, cl(i)] = tr K - sum_j |L_j| z[j]``.
+
+Readings where the paper is silent (each is listed in the design doc):
+  * an empty cluster j has D[:, j] = +inf (never chosen) and z[j] = 0;
+  * the argmin takes the lowest index among equal minima, and is decided on D
+    rounded to single precision, the precision the paper computes in
+    (Section V); the engine decides in the same precision;
+  * stop rule: tol < 0 runs exactly max_iter updates; tol = 0 stops after an
+    update that changed no assignment; tol > 0 also stops once
+    J(cl_{t-1}) - J(cl_t) <= tol * |J(cl_{t-1})|.
+
+Functions with no independent pin: none (see tests/test_oracle_pins.py).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+KIND_LINEAR, KIND_POLY, KIND_GAUSS = 0, 1, 2
+_KIND_NAMES = {"linear": KIND_LINEAR, "poly": KIND_POLY, "gauss": KIND_GAUSS}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kkm_ref.c")
+_LIB_PATH = os.path.join(_HERE, "libkkm_ref.so")
+_lib = None
+
+
+def build_ref(force: bool = False) -> str:
+    """Compile kkm_ref.c into libkkm_ref.so with gcc (plain C, OpenMP)."""
+    stale = (not os.path.exists(_LIB_PATH)
+             or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC))
+    if force or stale:
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O3", "-march=x86-64-v3", "-fopenmp", "-fPIC",
+                               "-shared", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _ref():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build_ref())
+        i64, i32, f64, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_double, ctypes.c_void_p
+        lib.kkm_ref_kernel_block.argtypes = [vp, i64, i32, i32, f64, f64, i32, vp, i64, vp, i64, vp]
+        lib.kkm_ref_kernel_pairs.argtypes = [vp, i64, i32, i32, f64, f64, i32, vp, vp, i64, vp]
+        lib.kkm_ref_own_cluster_sums.argtypes = [vp, i64, i32, i32, f64, f64, i32,
+                                                 vp, vp, vp, vp, i64, vp]
+        for f in (lib.kkm_ref_kernel_block, lib.kkm_ref_kernel_pairs, lib.kkm_ref_own_cluster_sums):
+            f.restype = None
+        _lib = lib
+    return _lib
+
+
+class Kernel:
+    """A kernel function kappa with its parameters (Eq. 2 and Section IV).
+
+    ``gamma`` and ``coef0`` are the single-precision values the engine gets;
+    the oracle widens exactly those values to double.
+    """
+
+    def __init__(self, kind, gamma=1.0, coef0=1.0, degree=2):
+        self.kind = _KIND_NAMES[kind] if isinstance(kind, str) else int(kind)
+        self.gamma = float(np.float32(gamma))
+        self.coef0 = float(np.float32(coef0))
+        self.degree = int(degree)
+
+    def _args(self):
+        return (self.kind, self.gamma, self.coef0, self.degree)
+
+    def block(self, X: np.ndarray, rows=None, cols=None) -> np.ndarray:
+        """K[rows][:, cols] in fp64, each entry kappa(x_i, x_j) from its definition."""
+        X = np.ascontiguousarray(X, dtype=np.float32)
+        n, d = X.shape
+        rows = np.arange(n, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.arange(n, dtype=np.int64) if cols is None else np.ascontiguousarray(cols, dtype=np.int64)
+        out = np.empty((rows.size, cols.size), dtype=np.float64)
+        if out.size:
+            _ref().kkm_ref_kernel_block(X.ctypes.data, n, d, *self._args(), rows.ctypes.data,
+                                        rows.size, cols.ctypes.data, cols.size, out.ctypes.data)
+        return out
+
+    def pairs(self, X: np.ndarray, rows, cols) -> np.ndarray:
+        """kappa(x_rows[p], x_cols[p]) for each p, fp64."""
+        X = np.ascontiguousarray(X, dtype=np.float32)
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        cols = np.ascontiguousarray(cols, dtype=np.int64)
+        assert rows.shape == cols.shape
+        out = np.empty(rows.size, dtype=np.float64)
+        if out.size:
+            _ref().kkm_ref_kernel_pairs(X.ctypes.data, X.shape[0], X.shape[1], *self._args(),
+                                        rows.ctypes.data, cols.ctypes.data, rows.size, out.ctypes.data)
+        return out
+
+    def diag(self, X: np.ndarray) -> np.ndarray:
+        i = np.arange(X.shape[0], dtype=np.int64)
+        return self.pairs(X, i, i)
+
+    def matrix(self, X: np.ndarray) -> np.ndarray:
+        """The full n x n kernel matrix (Eqs. 1-2): small n only."""
+        return self.block(X)
+
+
+# ---------------------------------------------------------------- clustering steps
+
+def cluster_sizes(cl: np.ndarray, k: int) -> np.ndarray:
+    """|L_j| = number of points assigned to cluster j (the L_j of Eq. 3)."""
+    return np.bincount(np.asarray(cl, dtype=np.int64), minlength=k)[:k].astype(np.int64)
+
+
+def one_hot(cl: np.ndarray, k: int) -> np.ndarray:
+    """The transposed assignment matrix in one-hot form: n x k, entry 1 where cl(i) = j."""
+    cl = np.asarray(cl, dtype=np.int64)
+    V = np.zeros((cl.size, k), dtype=np.float64)
+    V[np.arange(cl.size), cl] = 1.0
+    return V
+
+
+def one_hot_product(K_rows: np.ndarray, cl: np.ndarray, k: int) -> np.ndarray:
+    """E = K V^T (Eq. 4) with one-hot V: E[i, j] = sum_{m: cl(m)=j} K[i, m]."""
+    return K_rows @ one_hot(cl, k)
+
+
+def mask(E_rows: np.ndarray, cl_rows: np.ndarray) -> np.ndarray:
+    """Eq. 5: each point's entry of E in its own cluster, E[i, cl(i)]."""
+    cl_rows = np.asarray(cl_rows, dtype=np.int64)
+    return E_rows[np.arange(cl_rows.size), cl_rows]
+
+
+def self_terms(own: np.ndarray, cl: np.ndarray, counts: np.ndarray) -> np.ndarray:
+    """Eqs. 6-7: z[j] = (1/|L_j|^2) sum_{i in L_j} E[i, j] = ||mu_j||^2 in feature space.
+
+    ``own`` is the mask of Eq. 5 over all points.  Multiplying by V (whose
+    entries are 1/|L_j|) applies one 1/|L_j|; the second comes from E being
+    one-hot here rather than normalised.  Empty clusters get z = 0.
+    """
+    k = counts.size
+    sums = np.bincount(np.asarray(cl, dtype=np.int64), weights=own, minlength=k)[:k]
+    z = np.zeros(k, dtype=np.float64)
+    nz = counts > 0
+    z[nz] = sums[nz] / counts[nz].astype(np.float64) ** 2
+    return z
+
+
+def distances(diagK_rows: np.ndarray, E_rows: np.ndarray, z: np.ndarray, counts: np.ndarray) -> np.ndarray:
+    """Eq. 8 plus diag K: D[i, j] = K[i, i] - 2 E[i, j]/|L_j| + z[j]; +inf for empty j."""
+    D = np.full(E_rows.shape, np.inf, dtype=np.float64)
+    nz = counts > 0
+    D[:, nz] = (diagK_rows[:, None] - 2.0 * E_rows[:, nz] / counts[nz].astype(np.float64)
+                + z[None, nz])
+    return D
+
+
+def assign(D: np.ndarray, decide_in=np.float32) -> np.ndarray:
+    """Row-wise argmin (end of Section II-B), lowest index among equal minima.
+
+    The comparison is made on D rounded to ``decide_in`` (default: single
+    precision, the paper's working precision); np.argmin returns the first
+    occurrence of the minimum.
+    """
+    Dd = D.astype(decide_in) if decide_in is not None else D
+    return np.argmin(Dd, axis=1).astype(np.int32)
+
+
+def objective(trace_K: float, z: np.ndarray, counts: np.ndarray) -> float:
+    """J(cl) = sum_i D[i, cl(i)] = tr K - sum_j |L_j| z[j] (sum of squared distances)."""
+    return float(trace_K - np.sum(counts.astype(np.float64) * z))
+
+
+# ------------------------------------------------------------ whole step / loop
+
+def step_full(K: np.ndarray, cl: np.ndarray, k: int) -> dict:
+    """One clustering iteration on a formed kernel matrix (small n).
+
+    Returns E, z, D, the new assignment, the cluster sizes of the input
+    assignment and of the new one, the number of changed assignments and
+    J(cl) of the input assignment (= sum_i D[i, cl(i)]).
+    """
+    cl = np.asarray(cl, dtype=np.int64)
+    counts = cluster_sizes(cl, k)
+    E = one_hot_product(K, cl, k)
+    z = self_terms(mask(E, cl), cl, counts)
+    D = distances(np.diag(K).copy(), E, z, counts)
+    new = assign(D)
+    J = float(np.sum(D[np.arange(cl.size), cl]))
+    return dict(E=E, z=z, D=D, cl=new, counts=counts, counts_new=cluster_sizes(new, k),
+                changed=int(np.count_nonzero(new != cl)), J=J)
+
+
+def stop_now(tol: float, changed: int, J_prev, J_cur) -> bool:
+    """Stop rule after an update (see the module docstring)."""
+    if tol < 0:
+        return False
+    if changed == 0:
+        return True
+    if tol > 0 and J_prev is not None and (J_prev - J_cur) <= tol * abs(J_prev):
+        return True
+    return False
+
+
+def iterate_full(K: np.ndarray, cl0: np.ndarray, k: int, max_iter: int, tol: float = -1.0):
+    """The clustering loop of Alg. 1 at P = 1 (every collective is the identity).
+
+    Returns (final cl, iters_done, obj_hist, trajectory) where obj_hist[t] =
+    J(cl_t) and trajectory[t] = cl_{t+1}.
+    """
+    cl = np.asarray(cl0, dtype=np.int32).copy()
+    hist, traj = [], []
+    iters = 0
+    for t in range(max_iter):
+        out = step_full(K, cl, k)
+        hist.append(out["J"])
+        traj.append(out["cl"])
+        cl = out["cl"]
+        iters = t + 1
+        if stop_now(tol, out["changed"], hist[t - 1] if t > 0 else None, hist[t]):
+            break
+    return cl, iters, np.array(hist), traj
+
+
+def own_cluster_sums(kern: Kernel, X: np.ndarray, cl: np.ndarray, k: int, rows=None) -> np.ndarray:
+    """E[i, cl(i)] for the given rows (default: all), without forming K (Eq. 5)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    cl = np.ascontiguousarray(cl, dtype=np.int32)
+    n = X.shape[0]
+    rows = np.arange(n, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    order = np.argsort(cl, kind="stable").astype(np.int64)
+    offsets = np.zeros(k + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(cluster_sizes(cl, k))
+    own = np.empty(rows.size, dtype=np.float64)
+    if rows.size:
+        _ref().kkm_ref_own_cluster_sums(X.ctypes.data, n, X.shape[1], *kern._args(), cl.ctypes.data,
+                                        order.ctypes.data, offsets.ctypes.data, rows.ctypes.data,
+                                        rows.size, own.ctypes.data)
+    return own
+
+
+def step_rows(kern: Kernel, X: np.ndarray, cl: np.ndarray, k: int, rows, z=None) -> dict:
+    """One iteration evaluated only on sampled rows, for n too large to form K.
+
+    z (all clusters) needs every point's own-cluster sum; pass a precomputed z
+    to skip that O(sum_j |L_j|^2 d) pass.  Returns E, D, new assignment on the
+    rows, plus z, counts and J(cl).
+    """
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    cl = np.asarray(cl, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    counts = cluster_sizes(cl, k)
+    diag_all = kern.diag(X)
+    if z is None:
+        z = self_terms(own_cluster_sums(kern, X, cl, k), cl, counts)
+    K_rows = kern.block(X, rows, None)
+    E = one_hot_product(K_rows, cl, k)
+    D = distances(diag_all[rows], E, z, counts)
+    return dict(E=E, z=z, D=D, cl=assign(D), counts=counts,
+                J=objective(float(diag_all.sum()), z, counts), K_rows=K_rows)
