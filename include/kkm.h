@@ -1,0 +1,203 @@
+/*
+ * kkm.h — C ABI of the MI355X (gfx950) exact Kernel K-means engine.
+ *
+ * The engine computes the linear-algebraic formulation of Kernel K-means of
+ * "Communication-Avoiding Linear Algebraic Kernel K-Means on GPUs"
+ * (arXiv 2601.17136), Section II-B, on one GPU:
+ *
+ *   B = X X^T                                   (Eq. 1)
+ *   K = kappa(B) elementwise                    (Eq. 2; plus linear and Gaussian)
+ *   E = K V^T,  V one-hot in cluster ids        (Eq. 4, unnormalised here)
+ *   z_j = (1/|L_j|^2) sum_{i in L_j} E(i,j)      (Eqs. 5-7: the paper's c_j)
+ *   D(i,j) = K(i,i) - 2 E(i,j)/|L_j| + z_j       (Eq. 8 plus diag K)
+ *   cl'(i) = argmin_j D(i,j)                     (end of Section II-B)
+ *
+ * repeated as the clustering loop of Alg. 1 with one process (every
+ * collective is the identity).  V is carried as int32 cluster ids, which is
+ * all the paper communicates of V (Section V).
+ *
+ * Conventions for every entry point:
+ *  - Return value: KKM_OK (0) or a negative kkm_status.  After a failure,
+ *    kkm_last_error(ctx) holds a message.  Argument checks run on the host
+ *    before any HIP call; a call that fails them has enqueued nothing.
+ *  - Device pointers are plain HIP device addresses (e.g. a torch tensor's
+ *    data_ptr()); they stay owned by the caller.  Host pointers are marked.
+ *  - Points X are n x d, fp32, row-major, contiguous (row i at X + i*d).
+ *  - Cluster ids are int32 in [0, k).  An id outside that range is detected
+ *    on the device and reported as KKM_ERR_DEVICE_DATA; kernels clamp ids so
+ *    that no access goes out of bounds before the report.
+ *  - All work runs on the stream given to kkm_create.  kkm_build_kernel is
+ *    asynchronous; kkm_iterate, kkm_objective, kkm_step, kkm_copy_* return
+ *    after their work has completed.
+ *  - A context is not thread-safe; calls on one context must not overlap.
+ */
+#ifndef KKM_H
+#define KKM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KKM_ABI_VERSION 1
+#define KKM_MAX_K 4096 /* largest supported cluster count */
+
+typedef enum kkm_status {
+  KKM_OK = 0,
+  KKM_ERR_ARG = -1,         /* invalid argument; nothing enqueued */
+  KKM_ERR_OOM = -2,         /* needs more device memory than the budget allows */
+  KKM_ERR_HIP = -3,         /* a HIP runtime call failed (message has the HIP error) */
+  KKM_ERR_STATE = -4,       /* call out of order, e.g. kkm_iterate before a build */
+  KKM_ERR_DEVICE_DATA = -5  /* device input invalid: a cluster id outside [0, k) */
+} kkm_status;
+
+/* Kernel functions kappa.  LINEAR is the paper's "B = K" (Section IV);
+ * POLY is Eq. 2, (gamma x.y + coef0)^degree; GAUSS is exp(-gamma |x-y|^2),
+ * which the paper does not use but which the same formulation admits. */
+typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
+
+/* Where K lives.  RESIDENT stores K (n*n fp32) in device memory once and
+ * streams it every iteration.  ONTHEFLY never stores K: every iteration
+ * recomputes its tiles and folds them straight into E, which is the paper's
+ * single-GPU sliding-window baseline (Section VI-D) done tile by tile.
+ * AUTO picks RESIDENT when K fits the memory budget, else ONTHEFLY. */
+typedef enum kkm_mode { KKM_MODE_AUTO = 0, KKM_MODE_RESIDENT = 1, KKM_MODE_ONTHEFLY = 2 } kkm_mode;
+
+typedef struct kkm_params {
+  float gamma;    /* POLY: scale of x.y; GAUSS: > 0.  Ignored for LINEAR. */
+  float coef0;    /* POLY: additive constant c.  Ignored otherwise. */
+  int32_t degree; /* POLY: integer exponent, 1..16.  Ignored otherwise. */
+  int32_t mode;   /* kkm_mode */
+} kkm_params;
+
+typedef struct kkm_ctx kkm_ctx; /* opaque; owns K, the staged points and all scratch */
+
+/* Per-kernel timing, collected with HIP events on the context's stream when
+ * enabled by kkm_set_timing.  Index with the KKM_PHASE_* constants. */
+enum {
+  KKM_PHASE_STAGE = 0,   /* copy/pad X, row norms */
+  KKM_PHASE_GEMM = 1,    /* K = kappa(X X^T) tiles (resident build) */
+  KKM_PHASE_FIXUP = 2,   /* Gaussian entries recomputed from differences */
+  KKM_PHASE_LABELS = 3,  /* validate ids, cluster sizes, per-block counts */
+  KKM_PHASE_SCATTER = 4, /* stable counting sort of points by cluster */
+  KKM_PHASE_SPMM = 5,    /* E = K V^T over stored K */
+  KKM_PHASE_ASSIGN = 6,  /* z, distances, argmin, new sizes */
+  KKM_PHASE_ONTHEFLY = 7,/* recomputed K tiles folded into E */
+  KKM_PHASE_OTHER = 8,   /* gathers, copies, trace */
+  KKM_NPHASE = 9
+};
+typedef struct kkm_timing {
+  double ms[KKM_NPHASE];       /* summed kernel time per phase, milliseconds */
+  int64_t launches[KKM_NPHASE];/* kernel launches per phase */
+} kkm_timing;
+
+/* Facts about the built problem. */
+typedef struct kkm_info {
+  int64_t n;
+  int32_t d, d_pad;       /* feature count and its zero-padded width */
+  int32_t kind, mode;     /* kkm_kind, resolved kkm_mode (never AUTO) */
+  int64_t ld;             /* row stride of K in floats (resident mode) */
+  size_t bytes_K;         /* device bytes held by K (0 on the fly) */
+  size_t bytes_total;     /* device bytes held by the context */
+  int64_t fixups;         /* Gaussian entries recomputed from differences at build */
+} kkm_info;
+
+/* Create a context on the current HIP device.
+ * out:        receives the context (host pointer).
+ * hip_stream: hipStream_t to run on; NULL = the default (null) stream.
+ * mem_budget: device bytes the context may hold; 0 = 95% of the free memory
+ *             reported by hipMemGetInfo at creation.
+ * Errors: KKM_ERR_ARG (out NULL), KKM_ERR_HIP. */
+int kkm_create(kkm_ctx **out, void *hip_stream, size_t mem_budget);
+
+/* Free every device buffer the context holds, then the context.  NULL is a no-op. */
+int kkm_destroy(kkm_ctx *ctx);
+
+/* Message describing the last failure on ctx ("" if none).  With ctx NULL,
+ * the last failure of a call that had no context (kkm_create, kkm_plan). */
+const char *kkm_last_error(const kkm_ctx *ctx);
+
+/* Pure host planning, no HIP call.  Picks the mode for a problem and the
+ * device bytes it needs (K, staged points, per-iteration scratch for k
+ * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget.
+ * Errors: KKM_ERR_ARG (bad sizes), KKM_ERR_OOM (even the on-the-fly mode
+ * does not fit, or RESIDENT was requested and K does not fit). */
+int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode,
+             int32_t *mode_out, size_t *bytes_out);
+
+/* Host-only argument checks that the entry points apply first; exported so
+ * they can be exercised without a GPU.  Return KKM_OK or KKM_ERR_ARG. */
+int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params *params);
+int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
+
+/* Build the kernel matrix K = kappa(X X^T) (Eqs. 1-2) for the clustering loop.
+ * X:      device, n x d fp32 row-major.  The engine copies it (zero-padded to
+ *         d_pad columns); the caller may free X once this call has returned.
+ * n:      points, 1 .. 2^31-1.   d: features, 1 .. 65536.
+ * kind:   kkm_kind.   params: host pointer (gamma, coef0, degree, mode).
+ * RESIDENT: stores K (n rows, stride ld) in device memory; diag K is exact
+ *   (Gaussian: exactly 1).  Gaussian entries whose expansion
+ *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are
+ *   recomputed from the coordinate differences.
+ * ONTHEFLY: stages X and row norms only.
+ * Replaces any earlier build on ctx.  Asynchronous.
+ * Errors: KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_build_kernel(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t kind,
+                     const kkm_params *params);
+
+/* Run the clustering loop (Alg. 1 with one process).
+ * V:          device int32[n]: the initial cluster ids on entry, the final
+ *             ids on return.
+ * k:          clusters, 1 .. min(n, KKM_MAX_K).
+ * max_iter:   >= 0 assignment updates at most.
+ * tol:        < 0: run exactly max_iter updates (no host round trip per
+ *             update).  = 0: stop after an update that changed no id.
+ *             > 0: also stop once J(prev) - J(cur) <= tol * |J(prev)|.
+ * iters_done: host, may be NULL: updates applied.
+ * obj_hist:   host, may be NULL, max_iter entries: obj_hist[t] = J(cl_t),
+ *             the objective sum_i D(i, cl_t(i)) of the ids before update t.
+ * Empty clusters get D = +inf (never chosen) and stay empty; ties go to the
+ * lowest cluster index.
+ * Errors: KKM_ERR_ARG, KKM_ERR_STATE (no build), KKM_ERR_DEVICE_DATA, KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_iterate(kkm_ctx *ctx, int32_t *V, int32_t k, int32_t max_iter, double tol,
+                int32_t *iters_done, double *obj_hist);
+
+/* J(cl) = sum_i D(i, cl(i)) = tr K - sum_j |L_j| z_j for the ids V (device
+ * int32[n]); written to *J (host).  Errors as kkm_iterate. */
+int kkm_objective(kkm_ctx *ctx, const int32_t *V, int32_t k, double *J);
+
+/* One clustering step from ids cl_in, exposing every intermediate (for
+ * parity checks; not tuned).  All pointers are device memory except J.
+ * E: n x k fp32 row-major, E(i,j) = sum_{m: cl(m)=j} K(i,m)  (may be NULL)
+ * z: k fp32, the cluster self-terms                          (may be NULL)
+ * D: n x k fp32 row-major distances, +inf for empty clusters (may be NULL)
+ * cl_out: n int32 new ids; counts_out: k int32 sizes of cl_in (may be NULL each)
+ * J: host double, J(cl_in)                                   (may be NULL)
+ * Errors as kkm_iterate. */
+int kkm_step(kkm_ctx *ctx, const int32_t *cl_in, int32_t k, float *E, float *z, float *D,
+             int32_t *cl_out, int32_t *counts_out, double *J);
+
+/* Rows r0 .. r1-1 of K into out (device, (r1-r0) x n fp32 row-major).  In
+ * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses.
+ * Errors: KKM_ERR_ARG (range), KKM_ERR_STATE, KKM_ERR_HIP. */
+int kkm_copy_kernel_rows(kkm_ctx *ctx, int64_t r0, int64_t r1, float *out);
+
+/* diag K into out (device, n fp32). */
+int kkm_copy_diag(kkm_ctx *ctx, float *out);
+
+/* Timing: enable (1) or disable (0) per-kernel HIP-event timing; enabling
+ * also clears the accumulated figures.  kkm_get_timing synchronises the
+ * stream and returns the sums so far. */
+int kkm_set_timing(kkm_ctx *ctx, int32_t enable);
+int kkm_get_timing(kkm_ctx *ctx, kkm_timing *out);
+
+int kkm_get_info(kkm_ctx *ctx, kkm_info *out);
+
+int kkm_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KKM_H */

@@ -1,0 +1,344 @@
+// The clustering iteration over a stored K (Section II-B, Eqs. 3-8; the loop
+// body of Alg. 1 with a single process).
+//
+// E = K V^T is computed in its transposed form E^T = V K, the form the paper
+// uses for its SpMM (Section IV): row j of E^T is the sum of the rows of K
+// that belong to cluster j.  Points are first sorted by cluster (a stable
+// counting sort), so every workgroup of the SpMM sums a run of rows of one
+// cluster over a stripe of columns with a single accumulator: one add per
+// element of K, each row segment read as 4 KB of contiguous memory.  K is
+// symmetric, so the columns of E^T are the rows of E.
+//
+// Per iteration:  scatter (sorted order)  ->  spmm_onehot (E^T, partial self
+// terms)  ->  assign (z, distances, argmin, new sizes, next sort offsets).
+// All reductions of floating-point values run in a fixed order, so results
+// are bitwise reproducible; only integer counters use atomics.
+#include "kkm_internal.h"
+
+namespace kkm {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ inline int clamp_id(int c, int k) { return c < 0 ? 0 : (c >= k ? k - 1 : c); }
+
+// ----------------------------------------------------------------- assign
+//
+// mode 0 (labels): check ids, count cluster sizes and per-block histograms.
+// mode 1 (full):   z_j = (1/|L_j|^2) sum_s zpart[j][s]            (Eqs. 5-7)
+//                  D(i,j) = K(i,i) - 2 E(i,j)/|L_j| + z_j         (Eq. 8 + diag K)
+//                  cl'(i) = lowest j attaining min_j D(i,j); sizes of cl'.
+// Both modes end with the last-arriving workgroup turning the per-block
+// histograms into the sorted-order offsets and the SpMM chunk table.
+
+__device__ void sort_tables(const IterBufs& b, const int* __restrict__ counts, int* offs, int* qf,
+                            int* segsum) {
+  const int k = b.k, nb = b.nblk, tid = threadIdx.x;
+  if (tid == 0) {
+    int o = 0, q = 0;
+    for (int j = 0; j < k; ++j) {
+      const int c = counts[j];
+      offs[j] = o;
+      qf[j] = q;
+      o += c;
+      q += (c + kChunk - 1) / kChunk;
+    }
+    offs[k] = o;
+    qf[k] = q;
+    *b.nchunks = q;
+  }
+  __syncthreads();
+  for (int j = tid; j <= k; j += 256) {
+    b.off[j] = offs[j];
+    b.qfirst[j] = qf[j];
+  }
+  // base[j][blk] = offs[j] + number of members of j in blocks before blk
+  if (k <= 256) {
+    const int G = 256 / k, j = tid / G, g = tid % G;
+    const int seg = (nb + G - 1) / G, lo = g * seg, hi = (lo + seg < nb) ? lo + seg : nb;
+    int s = 0;
+    if (j < k)
+      for (int bb = lo; bb < hi; ++bb) s += b.hist[(int64_t)j * nb + bb];
+    segsum[tid] = s;
+    __syncthreads();
+    if (j < k) {
+      int run = offs[j];
+      for (int gg = 0; gg < g; ++gg) run += segsum[j * G + gg];
+      for (int bb = lo; bb < hi; ++bb) {
+        b.base[(int64_t)j * nb + bb] = run;
+        run += b.hist[(int64_t)j * nb + bb];
+      }
+    }
+  } else {
+    for (int j = tid; j < k; j += 256) {
+      int run = offs[j];
+      for (int bb = 0; bb < nb; ++bb) {
+        b.base[(int64_t)j * nb + bb] = run;
+        run += b.hist[(int64_t)j * nb + bb];
+      }
+    }
+  }
+  // chunk q of cluster j covers sorted positions [p0, p1), at most kChunk long
+  const int nq = qf[k];
+  for (int q = tid; q < nq; q += 256) {
+    int lo = 0, hi = k - 1;  // last j with qf[j] <= q
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (qf[mid] <= q) lo = mid;
+      else hi = mid - 1;
+    }
+    const int j = lo;
+    const int p0 = offs[j] + (q - qf[j]) * kChunk;
+    const int end = offs[j + 1];
+    b.chunk_j[q] = j;
+    b.chunk_p0[q] = p0;
+    b.chunk_p1[q] = (p0 + kChunk < end) ? p0 + kChunk : end;
+  }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __restrict__ counts_in,
+                                                     const int* __restrict__ cl_in,
+                                                     int* __restrict__ cl_out,
+                                                     int* __restrict__ counts_out,
+                                                     int* __restrict__ changed,
+                                                     double* __restrict__ obj,
+                                                     float* __restrict__ z_out,
+                                                     float* __restrict__ D_out) {
+  extern __shared__ double smem_d[];
+  const int k = b.k, tid = threadIdx.x;
+  double* zd = smem_d;                 // k
+  float* zf = (float*)(zd + k);        // k
+  float* sc = zf + k;                  // k
+  int* hist = (int*)(sc + k);          // k
+  int* offs = hist + k;                // k + 1
+  int* qf = offs + k + 1;              // k + 1
+  int* segsum = qf + k + 1;            // 256
+  __shared__ int is_last;
+
+  for (int j = tid; j < k; j += 256) hist[j] = 0;
+  if (MODE == 1) {
+    for (int j = tid; j < k; j += 256) {
+      const int c = counts_in[j];
+      double zs = 0.0;
+      if (c > 0)
+        for (int s = 0; s < b.nstripes; ++s) zs += b.zpart[(int64_t)j * b.nstripes + s];
+      const double z = c > 0 ? zs / ((double)c * (double)c) : 0.0;
+      zd[j] = c > 0 ? zs / (double)c : 0.0;  // |L_j| z_j
+      zf[j] = (float)z;
+      sc[j] = c > 0 ? -2.0f / (float)c : 0.f;
+      if (blockIdx.x == 0 && z_out) z_out[j] = (float)z;
+    }
+  }
+  __syncthreads();
+  if (MODE == 1 && blockIdx.x == 0 && tid == 0 && obj) {
+    double s = 0.0;
+    for (int j = 0; j < k; ++j) s += zd[j];
+    *obj = *b.trK - s;  // J(cl_in) = tr K - sum_j |L_j| z_j
+  }
+
+  const int64_t i = (int64_t)blockIdx.x * kBlk + tid;
+  const bool valid = i < b.n;
+  int lab = 0, chg = 0;
+  if (valid) {
+    if (MODE == 0) {
+      lab = cl_in[i];
+      if (lab < 0 || lab >= k) {
+        atomicOr(b.status, 1);
+        lab = clamp_id(lab, k);
+      }
+    } else {
+      const float dg = b.diagK[i];
+      float best = INFINITY;
+      int arg = -1;
+      for (int j = 0; j < k; ++j) {
+        const float s = sc[j];
+        float Dv = INFINITY;
+        if (s != 0.f) {
+          Dv = fmaf(s, b.Et[(int64_t)j * b.ld + i], dg + zf[j]);
+          if (arg < 0 || Dv < best) {
+            best = Dv;
+            arg = j;
+          }
+        }
+        if (D_out) D_out[i * k + j] = Dv;
+      }
+      lab = arg < 0 ? 0 : arg;
+      chg = (lab != clamp_id(cl_in[i], k));
+      cl_out[i] = lab;
+    }
+    atomicAdd(&hist[lab], 1);
+  }
+  const int nchg = __syncthreads_count(chg);
+  for (int j = tid; j < k; j += 256) {
+    const int c = hist[j];
+    b.hist[(int64_t)j * b.nblk + blockIdx.x] = c;
+    if (c) atomicAdd(&counts_out[j], c);
+  }
+  if (MODE == 1 && tid == 0 && nchg && changed) atomicAdd(changed, nchg);
+
+  // the last workgroup to finish builds the tables for the next scatter/SpMM
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) is_last = (atomicAdd(b.done_ctr, 1u) == (unsigned)(gridDim.x - 1));
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  if (tid == 0) *b.done_ctr = 0u;
+  sort_tables(b, counts_out, offs, qf, segsum);
+}
+
+static size_t assign_smem(int k) { return (size_t)k * 28 + 8 + 1024 + 64; }
+
+hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
+                         int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
+                         float* D_out, hipStream_t s) {
+  dim3 grid((unsigned)b.nblk), block(256);
+  const size_t sm = assign_smem(b.k);
+  if (mode == 0)
+    hipLaunchKernelGGL(assign_kernel<0>, grid, block, sm, s, b, counts_in, cl_in, cl_out,
+                       counts_out, changed, obj, z_out, D_out);
+  else
+    hipLaunchKernelGGL(assign_kernel<1>, grid, block, sm, s, b, counts_in, cl_in, cl_out,
+                       counts_out, changed, obj, z_out, D_out);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------- scatter
+//
+// Stable counting sort: point i of block blk goes to
+//   base[cl(i)][blk] + (members of cl(i) in earlier wavefronts of blk)
+//                    + (members of cl(i) in earlier lanes of its wavefront).
+// Workgroup 0 also clears this iteration's size and change counters.
+__global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __restrict__ cl,
+                                                      int* __restrict__ zero_counts,
+                                                      int* __restrict__ zero_changed) {
+  extern __shared__ int wc[];  // 4 wavefronts x k
+  const int k = b.k, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (blockIdx.x == 0) {
+    if (zero_counts)
+      for (int j = tid; j < k; j += 256) zero_counts[j] = 0;
+    if (zero_changed && tid == 0) *zero_changed = 0;
+  }
+  for (int q = tid; q < 4 * k; q += 256) wc[q] = 0;
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * kBlk + tid;
+  const bool valid = i < b.n;
+  const int lab = valid ? clamp_id(cl[i], k) : -1;
+  int rank = 0;
+  unsigned long long todo = __ballot(valid);
+  while (todo) {
+    const int leader = __ffsll((long long)todo) - 1;
+    const int L = __shfl(lab, leader, 64);
+    const unsigned long long m = __ballot(lab == L);
+    if (lab == L) rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == leader) wc[w * k + L] = __popcll(m);
+    todo &= ~m;
+  }
+  __syncthreads();
+  if (valid) {
+    int r = b.base[(int64_t)lab * b.nblk + blockIdx.x] + rank;
+    for (int ww = 0; ww < w; ++ww) r += wc[ww * k + lab];
+    b.perm[r] = (int)i;
+    b.pos[i] = r;
+  }
+}
+
+hipError_t launch_scatter(const IterBufs& b, const int* cl, int* zero_counts, int* zero_changed,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)b.nblk), dim3(256), (size_t)4 * b.k * sizeof(int),
+                     s, b, cl, zero_counts, zero_changed);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------- SpMM
+//
+// Workgroup (stripe, q): columns [stripe*1024, +1024) of the rows listed in
+// chunk q (one cluster j, at most 256 rows in sorted order).  Each lane keeps
+// one float4 accumulator; rows are summed in sorted order.  The chunk's sum
+// goes to P[q]; the last chunk of cluster j to arrive for this stripe adds
+// the chunks of j in chunk order, writes E^T(j, stripe), and the stripe's
+// share of sum_{i in L_j} E(i, j) for the self-term z_j.
+__global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restrict__ K, IterBufs b,
+                                                          const int* __restrict__ cl) {
+  const int ns = b.nstripes;
+  const int stripe = (int)(blockIdx.x % (unsigned)ns);
+  const int q = (int)(blockIdx.x / (unsigned)ns);
+  if (q >= *b.nchunks) return;
+  const int j = b.chunk_j[q], p0 = b.chunk_p0[q], p1 = b.chunk_p1[q];
+  const int tid = threadIdx.x;
+  __shared__ int rows[kChunk];
+  __shared__ int last;
+  __shared__ double red[4];
+  for (int p = p0 + tid; p < p1; p += 256) rows[p - p0] = b.perm[p];
+  __syncthreads();
+
+  const int64_t ld = b.ld;
+  const int64_t col = (int64_t)stripe * kStripe + tid * 4;
+  const bool active = col < ld;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  const int nr = p1 - p0;
+  if (active) {
+    const float* base = K + col;
+    int r = 0;
+    for (; r + 8 <= nr; r += 8) {
+      f4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[u] = __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r + u] * ld));
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; r < nr; ++r) acc += __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r] * ld));
+  }
+
+  const int qa = b.qfirst[j], qb = b.qfirst[j + 1];
+  f4 e = acc;
+  if (qb - qa > 1) {
+    if (active) *(f4*)(b.P + (int64_t)q * ld + col) = acc;
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) last = (atomicAdd(&b.spmm_cnt[stripe * b.k + j], 1u) == (unsigned)(qb - qa - 1));
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    if (tid == 0) b.spmm_cnt[stripe * b.k + j] = 0u;
+    e = (f4){0.f, 0.f, 0.f, 0.f};
+    if (active)
+      for (int qq = qa; qq < qb; ++qq) e += (qq == q) ? acc : *(const f4*)(b.P + (int64_t)qq * ld + col);
+  }
+  double zs = 0.0;
+  if (active) {
+    *(f4*)(b.Et + (int64_t)j * ld + col) = e;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (col + c < b.n && cl[col + c] == j) zs += (double)e[c];
+  }
+  for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = zs;
+  __syncthreads();
+  if (tid == 0) b.zpart[(int64_t)j * ns + stripe] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, const int* cl, hipStream_t s) {
+  const long long grid = (long long)b.nstripes * b.qmax;
+  hipLaunchKernelGGL(spmm_onehot_kernel, dim3((unsigned)grid), dim3(256), 0, s, K, b, cl);
+  return hipGetLastError();
+}
+
+// E (n x k, row-major) from E^T; empty clusters read as 0.
+__global__ void et_to_e_kernel(IterBufs b, const int* __restrict__ counts, float* __restrict__ E) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= b.n * b.k) return;
+  const int64_t i = t / b.k;
+  const int j = (int)(t % b.k);
+  E[t] = counts[j] > 0 ? b.Et[(int64_t)j * b.ld + i] : 0.f;
+}
+
+hipError_t launch_et_to_e(const IterBufs& b, const int* counts, float* E, hipStream_t s) {
+  const int64_t tot = b.n * b.k;
+  hipLaunchKernelGGL(et_to_e_kernel, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, b,
+                     counts, E);
+  return hipGetLastError();
+}
+
+}  // namespace kkm

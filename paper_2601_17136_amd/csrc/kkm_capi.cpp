@@ -1,0 +1,641 @@
+// Host side of the engine: the C ABI declared in include/kkm.h.
+//
+// A context owns every device buffer.  kkm_build_kernel stages the points and
+// (resident mode) builds K; kkm_iterate runs the loop body of Alg. 1 with one
+// process: scatter -> spmm_onehot -> assign per update, enqueued back to back
+// on the context's stream with no host round trip unless a stop test needs
+// one.  Argument checks run before any HIP call.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kkm.h"
+#include "kkm_internal.h"
+
+using namespace kkm;
+
+namespace {
+
+struct TimedLaunch {
+  int phase;
+  hipEvent_t start, stop;
+};
+
+struct Alloc {
+  void* p;
+  size_t bytes;
+};
+
+thread_local std::string g_noctx_err;
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Error estimate for the Gaussian expansion s = |x|^2 + |y|^2 - 2 x.y in fp32:
+// |err(s)| ~ kFixAcc * 2^-24 * (|x|^2 + |y|^2), and the entry moves by
+// gamma * err(s) * K.  Entries where that exceeds kFixTol are recomputed.
+constexpr float kFixAcc = 8.0f;
+constexpr float kFixTol = 2.0e-6f;
+
+struct Sizes {
+  int64_t n, n_pad, ld, nblk;
+  int d_pad, nstripes;
+};
+
+Sizes sizes_for(int64_t n, int32_t d) {
+  Sizes s;
+  s.n = n;
+  s.n_pad = round_up(n, kTile);
+  s.ld = round_up(n, 64);
+  s.d_pad = (int)round_up(d, kBK);
+  s.nblk = (n + kBlk - 1) / kBlk;
+  s.nstripes = (int)((s.ld + kStripe - 1) / kStripe);
+  return s;
+}
+
+size_t staged_bytes(const Sizes& s) {
+  return (size_t)s.n_pad * s.d_pad * 4 + (size_t)s.n_pad * 4 + (size_t)s.n * 4 + 64;
+}
+size_t k_bytes(const Sizes& s) { return (size_t)s.n * (size_t)s.ld * 4; }
+int64_t qmax_for(const Sizes& s, int k) { return (s.n + kChunk - 1) / kChunk + k; }
+
+size_t ws_bytes(const Sizes& s, int k) {
+  const int64_t qmax = qmax_for(s, k);
+  size_t b = 0;
+  b += (size_t)k * s.ld * 4;              // Et
+  b += (size_t)qmax * s.ld * 4;           // P
+  b += (size_t)s.nstripes * k * 4;        // spmm counters
+  b += (size_t)k * s.nstripes * 8;        // zpart
+  b += (size_t)2 * k * s.nblk * 4;        // hist, base
+  b += (size_t)2 * (k + 1) * 4;           // off, qfirst
+  b += (size_t)3 * qmax * 4 + 4;          // chunk table
+  b += (size_t)4 * s.n * 4;               // perm, pos, two id buffers
+  b += (size_t)2 * k * 4 + 64;            // counts, status, done counter
+  return b + 32 * 256;                    // alignment slack
+}
+
+}  // namespace
+
+struct kkm_ctx {
+  hipStream_t stream = nullptr;
+  int device = 0;
+  size_t budget = 0, held = 0;
+  std::string err;
+
+  bool built = false;
+  Sizes sz{};
+  int d = 0, kind = 0, mode = 0;
+  kkm_params params{};
+  KappaParams kp{};
+  float *Xp = nullptr, *nrm = nullptr, *diagK = nullptr, *K = nullptr;
+  double* trK = nullptr;
+  int2* fix_list = nullptr;
+  unsigned long long* fix_count = nullptr;
+  long long fix_cap = 0;
+  int64_t fixups = 0;
+  std::vector<Alloc> build_allocs;
+
+  int k_ws = 0, iter_ws = 0;
+  IterBufs ib{};
+  int* counts[2] = {nullptr, nullptr};
+  int* clbuf[2] = {nullptr, nullptr};
+  std::vector<Alloc> ws_allocs;
+  int* changed = nullptr;
+  double* obj = nullptr;
+  std::vector<Alloc> hist_allocs;
+
+  bool timing = false;
+  std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> pool;
+  kkm_timing tacc{};
+};
+
+namespace {
+
+int fail(kkm_ctx* c, int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->err = buf;
+  else g_noctx_err = buf;
+  return code;
+}
+
+int hip_fail(kkm_ctx* c, hipError_t e, const char* what) {
+  return fail(c, KKM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(c, expr, what)                    \
+  do {                                            \
+    hipError_t e_ = (expr);                       \
+    if (e_ != hipSuccess) return hip_fail(c, e_, what); \
+  } while (0)
+
+int dalloc(kkm_ctx* c, void** p, size_t bytes, std::vector<Alloc>& owner, const char* what) {
+  bytes = std::max<size_t>(bytes, 256);
+  if (c->held + bytes > c->budget)
+    return fail(c, KKM_ERR_OOM, "%s needs %zu bytes; %zu of the %zu-byte budget already held", what,
+                bytes, c->held, c->budget);
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(c, KKM_ERR_OOM, "hipMalloc(%zu) for %s: %s", bytes, what, hipGetErrorString(e));
+  }
+  owner.push_back({*p, bytes});
+  c->held += bytes;
+  return KKM_OK;
+}
+
+void release(kkm_ctx* c, std::vector<Alloc>& owner) {
+  for (const Alloc& a : owner) {
+    (void)hipFree(a.p);
+    c->held -= std::min(c->held, a.bytes);
+  }
+  owner.clear();
+}
+
+hipEvent_t take_event(kkm_ctx* c) {
+  if (!c->pool.empty()) {
+    hipEvent_t e = c->pool.back();
+    c->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+int run(kkm_ctx* c, int phase, const char* what, F&& f) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (c->timing) {
+    a = take_event(c);
+    b = take_event(c);
+    if (a) (void)hipEventRecord(a, c->stream);
+  }
+  hipError_t e = f();
+  if (c->timing && a && b) {
+    (void)hipEventRecord(b, c->stream);
+    c->pending.push_back({phase, a, b});
+  }
+  if (e != hipSuccess) return hip_fail(c, e, what);
+  return KKM_OK;
+}
+
+void collect_timing(kkm_ctx* c) {
+  for (auto& t : c->pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(t.stop) == hipSuccess && hipEventElapsedTime(&ms, t.start, t.stop) == hipSuccess) {
+      c->tacc.ms[t.phase] += ms;
+      c->tacc.launches[t.phase] += 1;
+    }
+    c->pool.push_back(t.start);
+    c->pool.push_back(t.stop);
+  }
+  c->pending.clear();
+}
+
+void free_ws(kkm_ctx* c) {
+  release(c, c->ws_allocs);
+  c->k_ws = 0;
+  c->ib = IterBufs{};
+}
+
+void free_hist(kkm_ctx* c) {
+  release(c, c->hist_allocs);
+  c->iter_ws = 0;
+  c->changed = nullptr;
+  c->obj = nullptr;
+}
+
+void free_build(kkm_ctx* c) {
+  free_ws(c);
+  free_hist(c);
+  release(c, c->build_allocs);
+  c->Xp = c->nrm = c->diagK = c->K = nullptr;
+  c->trK = nullptr;
+  c->fix_list = nullptr;
+  c->fix_count = nullptr;
+  c->fix_cap = 0;
+  c->built = false;
+}
+
+// Allocate one block and carve it (keeps the accounting to one number).
+int carve_ws(kkm_ctx* c, int k) {
+  const Sizes& s = c->sz;
+  void* base = nullptr;
+  int rc = dalloc(c, &base, ws_bytes(s, k), c->ws_allocs, "iteration scratch");
+  if (rc) return rc;
+  char* p = (char*)base;
+  auto take = [&](size_t bytes) {
+    char* r = p;
+    p += (bytes + 255) / 256 * 256;
+    return (void*)r;
+  };
+  IterBufs& b = c->ib;
+  b = IterBufs{};
+  b.n = s.n;
+  b.ld = s.ld;
+  b.k = k;
+  b.nblk = (int)s.nblk;
+  b.nstripes = s.nstripes;
+  const int64_t qmax = qmax_for(s, k);
+  b.qmax = (int)qmax;
+  b.diagK = c->diagK;
+  b.trK = c->trK;
+  b.Et = (float*)take((size_t)k * s.ld * 4);
+  b.P = (float*)take((size_t)qmax * s.ld * 4);
+  b.spmm_cnt = (unsigned*)take((size_t)s.nstripes * k * 4);
+  b.zpart = (double*)take((size_t)k * s.nstripes * 8);
+  b.hist = (int*)take((size_t)k * s.nblk * 4);
+  b.base = (int*)take((size_t)k * s.nblk * 4);
+  b.off = (int*)take((size_t)(k + 1) * 4);
+  b.qfirst = (int*)take((size_t)(k + 1) * 4);
+  b.chunk_j = (int*)take((size_t)qmax * 4);
+  b.chunk_p0 = (int*)take((size_t)qmax * 4);
+  b.chunk_p1 = (int*)take((size_t)qmax * 4);
+  b.nchunks = (int*)take(4);
+  b.perm = (int*)take((size_t)s.n * 4);
+  b.pos = (int*)take((size_t)s.n * 4);
+  c->clbuf[0] = (int*)take((size_t)s.n * 4);
+  c->clbuf[1] = (int*)take((size_t)s.n * 4);
+  c->counts[0] = (int*)take((size_t)k * 4);
+  c->counts[1] = (int*)take((size_t)k * 4);
+  b.status = (int*)take(4);
+  b.done_ctr = (unsigned*)take(4);
+  c->k_ws = k;
+  // counters that kernels expect at zero between uses
+  HIP_TRY(c, launch_zero_ints((int*)b.spmm_cnt, (int64_t)s.nstripes * k, c->stream), "zero counters");
+  HIP_TRY(c, launch_zero_ints((int*)b.done_ctr, 1, c->stream), "zero counters");
+  return KKM_OK;
+}
+
+int ensure_ws(kkm_ctx* c, int k, int iters) {
+  if (c->k_ws != k) {
+    free_ws(c);
+    int rc = carve_ws(c, k);
+    if (rc) return rc;
+  }
+  if (c->iter_ws < iters || !c->obj) {
+    free_hist(c);
+    int cap = std::max(iters, 64);
+    void* p = nullptr;
+    int rc = dalloc(c, &p, (size_t)cap * 12 + 512, c->hist_allocs, "objective history");
+    if (rc) return rc;
+    c->obj = (double*)p;
+    c->changed = (int*)((char*)p + (size_t)cap * 8);
+    c->iter_ws = cap;
+  }
+  return KKM_OK;
+}
+
+int check_ids_on_device(kkm_ctx* c, const int32_t* V) {
+  IterBufs& b = c->ib;
+  int rc;
+  if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(c->counts[0], b.k, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(b.status, 1, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_LABELS, "assign(labels)", [&] {
+         return launch_assign(0, b, nullptr, V, nullptr, c->counts[0], nullptr, nullptr, nullptr,
+                              nullptr, c->stream);
+       })))
+    return rc;
+  int status = 0;
+  HIP_TRY(c, hipMemcpyAsync(&status, b.status, sizeof(int), hipMemcpyDeviceToHost, c->stream), "read status");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if (status & 1) return fail(c, KKM_ERR_DEVICE_DATA, "a cluster id is outside [0, %d)", b.k);
+  return KKM_OK;
+}
+
+// One update: ids cur (sizes in counts[t&1]) -> ids nxt (sizes in counts[(t+1)&1]).
+int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float* D_out) {
+  IterBufs& b = c->ib;
+  int* cin = c->counts[t & 1];
+  int* cout = c->counts[(t + 1) & 1];
+  int rc;
+  if ((rc = run(c, KKM_PHASE_SCATTER, "scatter", [&] {
+         return launch_scatter(b, cur, cout, c->changed + t, c->stream);
+       })))
+    return rc;
+  if (c->mode == KKM_MODE_RESIDENT) {
+    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, cur, c->stream); })))
+      return rc;
+  } else {
+    return fail(c, KKM_ERR_STATE, "on-the-fly mode is not available in this build");
+  }
+  return run(c, KKM_PHASE_ASSIGN, "assign", [&] {
+    return launch_assign(1, b, cin, cur, nxt, cout, c->changed + t, c->obj + t, z_out, D_out, c->stream);
+  });
+}
+
+int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  if (kkm_check_iterate_args(c->sz.n, k, max_iter) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  return KKM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kkm_abi_version(void) { return KKM_ABI_VERSION; }
+
+const char* kkm_last_error(const kkm_ctx* ctx) { return ctx ? ctx->err.c_str() : g_noctx_err.c_str(); }
+
+int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params* p) {
+  if (n < 1 || n > 2147483647LL) return fail(nullptr, KKM_ERR_ARG, "n=%lld must be in [1, 2^31-1]", (long long)n);
+  if (d < 1 || d > 65536) return fail(nullptr, KKM_ERR_ARG, "d=%d must be in [1, 65536]", d);
+  if (kind != KKM_LINEAR && kind != KKM_POLY && kind != KKM_GAUSS)
+    return fail(nullptr, KKM_ERR_ARG, "kind=%d is not LINEAR(0), POLY(1) or GAUSS(2)", kind);
+  if (!p) return fail(nullptr, KKM_ERR_ARG, "params is NULL");
+  if (p->mode < KKM_MODE_AUTO || p->mode > KKM_MODE_ONTHEFLY)
+    return fail(nullptr, KKM_ERR_ARG, "mode=%d is not AUTO(0), RESIDENT(1) or ONTHEFLY(2)", p->mode);
+  if (kind == KKM_POLY) {
+    if (!(std::isfinite(p->gamma) && std::isfinite(p->coef0)))
+      return fail(nullptr, KKM_ERR_ARG, "polynomial gamma and coef0 must be finite");
+    if (p->degree < 1 || p->degree > 16)
+      return fail(nullptr, KKM_ERR_ARG, "polynomial degree=%d must be in [1, 16]", p->degree);
+  }
+  if (kind == KKM_GAUSS && !(p->gamma > 0.f && std::isfinite(p->gamma)))
+    return fail(nullptr, KKM_ERR_ARG, "Gaussian gamma=%g must be finite and > 0", (double)p->gamma);
+  return KKM_OK;
+}
+
+int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter) {
+  if (k < 1 || k > KKM_MAX_K) return fail(nullptr, KKM_ERR_ARG, "k=%d must be in [1, %d]", k, KKM_MAX_K);
+  if ((int64_t)k > n) return fail(nullptr, KKM_ERR_ARG, "k=%d exceeds n=%lld", k, (long long)n);
+  if (max_iter < 0) return fail(nullptr, KKM_ERR_ARG, "max_iter=%d must be >= 0", max_iter);
+  return KKM_OK;
+}
+
+int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode,
+             int32_t* mode_out, size_t* bytes_out) {
+  if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
+    return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
+  if (k < 1 || k > KKM_MAX_K || (int64_t)k > n) return fail(nullptr, KKM_ERR_ARG, "bad k=%d", k);
+  if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_ONTHEFLY)
+    return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
+  const Sizes s = sizes_for(n, d);
+  const size_t base = staged_bytes(s) + ws_bytes(s, k) + 4096;
+  const size_t resident = base + k_bytes(s);
+  const size_t onthefly = base + staged_bytes(s);  // sorted copy of the points
+  int mode = requested_mode;
+  if (mode == KKM_MODE_AUTO) mode = resident <= mem_budget ? KKM_MODE_RESIDENT : KKM_MODE_ONTHEFLY;
+  const size_t need = mode == KKM_MODE_RESIDENT ? resident : onthefly;
+  if (mode_out) *mode_out = mode;
+  if (bytes_out) *bytes_out = need;
+  if (need > mem_budget)
+    return fail(nullptr, KKM_ERR_OOM, "%s mode needs %zu bytes, budget %zu",
+                mode == KKM_MODE_RESIDENT ? "resident" : "on-the-fly", need, mem_budget);
+  return KKM_OK;
+}
+
+int kkm_create(kkm_ctx** out, void* hip_stream, size_t mem_budget) {
+  if (!out) return fail(nullptr, KKM_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(nullptr, KKM_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (mem_budget == 0) {
+    size_t freeb = 0, totalb = 0;
+    e = hipMemGetInfo(&freeb, &totalb);
+    if (e != hipSuccess) return fail(nullptr, KKM_ERR_HIP, "hipMemGetInfo: %s", hipGetErrorString(e));
+    mem_budget = (size_t)((double)freeb * 0.95);
+  }
+  kkm_ctx* c = new kkm_ctx();
+  c->stream = (hipStream_t)hip_stream;
+  c->device = dev;
+  c->budget = mem_budget;
+  *out = c;
+  return KKM_OK;
+}
+
+int kkm_destroy(kkm_ctx* c) {
+  if (!c) return KKM_OK;
+  (void)hipStreamSynchronize(c->stream);
+  collect_timing(c);
+  free_build(c);
+  for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
+  delete c;
+  return KKM_OK;
+}
+
+int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (kkm_check_build_args(n, d, kind, params) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  if (!X) return fail(c, KKM_ERR_ARG, "X is NULL");
+  int32_t mode = 0;
+  size_t need = 0;
+  // plan with k = 1: the k-dependent scratch is sized when kkm_iterate is called
+  size_t held_by_build = 0;
+  for (const Alloc& a : c->build_allocs) held_by_build += a.bytes;
+  for (const Alloc& a : c->ws_allocs) held_by_build += a.bytes;
+  for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
+  const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
+  if (kkm_plan(n, d, 1, budget_left, params->mode, &mode, &need) != KKM_OK)
+    return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
+  if (mode == KKM_MODE_ONTHEFLY)
+    return fail(c, KKM_ERR_ARG, "on-the-fly mode is not available in this build");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  collect_timing(c);
+  free_build(c);
+
+  c->sz = sizes_for(n, d);
+  c->d = d;
+  c->kind = kind;
+  c->mode = mode;
+  c->params = *params;
+  KappaParams& kp = c->kp;
+  kp.kind = kind;
+  kp.gamma = params->gamma;
+  kp.coef0 = params->coef0;
+  kp.degree = params->degree;
+  kp.neg_g_log2e = (float)(-(double)params->gamma * 1.4426950408889634);
+  kp.fix_scale = (float)((double)params->gamma * kFixAcc * std::ldexp(1.0, -24));
+  kp.fix_tol = kFixTol;
+
+  const Sizes& s = c->sz;
+  int rc;
+  void* p = nullptr;
+  if ((rc = dalloc(c, &p, staged_bytes(s), c->build_allocs, "staged points"))) return rc;
+  c->Xp = (float*)p;
+  c->nrm = c->Xp + (size_t)s.n_pad * s.d_pad;
+  c->diagK = c->nrm + s.n_pad;
+  if ((rc = dalloc(c, &p, 64, c->build_allocs, "trace"))) return rc;
+  c->trK = (double*)p;
+  if (mode == KKM_MODE_RESIDENT) {
+    if ((rc = dalloc(c, &p, k_bytes(s), c->build_allocs, "kernel matrix K"))) return rc;
+    c->K = (float*)p;
+  }
+  if ((rc = run(c, KKM_PHASE_STAGE, "stage", [&] {
+         return launch_stage(X, n, d, s.d_pad, s.n_pad, c->Xp, c->nrm, c->stream);
+       })))
+    return rc;
+
+  c->fixups = 0;
+  if (kind == KKM_GAUSS) {
+    const long long upper = (long long)(n * (n - 1) / 2);
+    long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
+    const size_t room = c->budget > c->held ? c->budget - c->held : 0;
+    cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
+    cap = std::max<long long>(cap, 1);
+    if ((rc = dalloc(c, &p, (size_t)cap * sizeof(int2) + 256, c->build_allocs, "fix-up list"))) return rc;
+    c->fix_list = (int2*)p;
+    c->fix_count = (unsigned long long*)((char*)p + (size_t)cap * sizeof(int2));
+    c->fix_cap = cap;
+    HIP_TRY(c, hipMemsetAsync(c->fix_count, 0, sizeof(unsigned long long), c->stream), "clear fix-up count");
+  }
+  c->built = true;  // buffers exist from here on; free_build releases them
+
+  if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
+         return launch_gemm_kappa(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->K, c->diagK, c->fix_list,
+                                  c->fix_count, c->fix_cap, c->stream);
+       })))
+    return rc;
+  if (kind == KKM_GAUSS) {
+    unsigned long long cnt = 0;
+    HIP_TRY(c, hipMemcpyAsync(&cnt, c->fix_count, sizeof cnt, hipMemcpyDeviceToHost, c->stream), "read fix-up count");
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    c->fixups = (int64_t)cnt;
+    const long long listed = std::min<long long>((long long)cnt, c->fix_cap);
+    if ((rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
+           return launch_gauss_fixup_list(c->Xp, s.d_pad, s.ld, kp, c->fix_list, listed, c->K, c->stream);
+         })))
+      return rc;
+    if ((long long)cnt > c->fix_cap) {
+      if ((rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup_scan", [&] {
+             return launch_gauss_fixup_scan(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->K, c->stream);
+           })))
+        return rc;
+    }
+  }
+  return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
+}
+
+int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
+                double* obj_hist) {
+  int rc;
+  if ((rc = check_ready(c, k, max_iter))) return rc;
+  if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
+  if (iters_done) *iters_done = 0;
+  if ((rc = ensure_ws(c, k, max_iter))) return rc;
+  if ((rc = check_ids_on_device(c, V))) return rc;
+  const int* cur = V;
+  int t = 0;
+  double Jprev = 0.0;
+  for (; t < max_iter; ++t) {
+    int* nxt = c->clbuf[t & 1];
+    if ((rc = one_update(c, t, cur, nxt, nullptr, nullptr))) return rc;
+    cur = nxt;
+    if (tol >= 0.0) {
+      int chg = 0;
+      double J = 0.0;
+      HIP_TRY(c, hipMemcpyAsync(&chg, c->changed + t, sizeof chg, hipMemcpyDeviceToHost, c->stream), "read changes");
+      HIP_TRY(c, hipMemcpyAsync(&J, c->obj + t, sizeof J, hipMemcpyDeviceToHost, c->stream), "read objective");
+      HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+      bool stop = chg == 0;
+      if (!stop && tol > 0.0 && t > 0 && (Jprev - J) <= tol * std::fabs(Jprev)) stop = true;
+      Jprev = J;
+      if (stop) {
+        ++t;
+        break;
+      }
+    }
+  }
+  if (t > 0)
+    HIP_TRY(c, hipMemcpyAsync(V, cur, (size_t)c->sz.n * 4, hipMemcpyDeviceToDevice, c->stream), "copy ids");
+  if (obj_hist && t > 0)
+    HIP_TRY(c, hipMemcpyAsync(obj_hist, c->obj, (size_t)t * sizeof(double), hipMemcpyDeviceToHost, c->stream),
+            "read objective history");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if (iters_done) *iters_done = t;
+  return KKM_OK;
+}
+
+int kkm_step(kkm_ctx* c, const int32_t* cl_in, int32_t k, float* E, float* z, float* D, int32_t* cl_out,
+             int32_t* counts_out, double* J) {
+  int rc;
+  if ((rc = check_ready(c, k, 1))) return rc;
+  if (!cl_in) return fail(c, KKM_ERR_ARG, "cl_in is NULL");
+  if ((rc = ensure_ws(c, k, 1))) return rc;
+  if ((rc = check_ids_on_device(c, cl_in))) return rc;
+  int* nxt = cl_out ? cl_out : c->clbuf[0];
+  if ((rc = one_update(c, 0, cl_in, nxt, z, D))) return rc;
+  if (E && (rc = run(c, KKM_PHASE_OTHER, "et_to_e", [&] { return launch_et_to_e(c->ib, c->counts[0], E, c->stream); })))
+    return rc;
+  if (counts_out)
+    HIP_TRY(c, hipMemcpyAsync(counts_out, c->counts[0], (size_t)k * 4, hipMemcpyDeviceToDevice, c->stream), "copy counts");
+  if (J) HIP_TRY(c, hipMemcpyAsync(J, c->obj, sizeof(double), hipMemcpyDeviceToHost, c->stream), "read objective");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
+}
+
+int kkm_objective(kkm_ctx* c, const int32_t* V, int32_t k, double* J) {
+  if (!J) return fail(c, KKM_ERR_ARG, "J is NULL");
+  return kkm_step(c, V, k, nullptr, nullptr, nullptr, nullptr, nullptr, J);
+}
+
+int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  if (!out || r0 < 0 || r1 > c->sz.n || r0 > r1) return fail(c, KKM_ERR_ARG, "bad row range [%lld, %lld)", (long long)r0, (long long)r1);
+  if (r1 == r0) return KKM_OK;
+  if (c->mode != KKM_MODE_RESIDENT) return fail(c, KKM_ERR_STATE, "on-the-fly mode is not available in this build");
+  const size_t row = (size_t)c->sz.n * 4;
+  HIP_TRY(c, hipMemcpy2DAsync(out, row, c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, row, (size_t)(r1 - r0),
+                              hipMemcpyDeviceToDevice, c->stream), "copy rows");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
+}
+
+int kkm_copy_diag(kkm_ctx* c, float* out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  if (!out) return fail(c, KKM_ERR_ARG, "out is NULL");
+  HIP_TRY(c, hipMemcpyAsync(out, c->diagK, (size_t)c->sz.n * 4, hipMemcpyDeviceToDevice, c->stream), "copy diag");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
+}
+
+int kkm_set_timing(kkm_ctx* c, int32_t enable) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  (void)hipStreamSynchronize(c->stream);
+  collect_timing(c);
+  c->timing = enable != 0;
+  if (c->timing) c->tacc = kkm_timing{};
+  return KKM_OK;
+}
+
+int kkm_get_timing(kkm_ctx* c, kkm_timing* out) {
+  if (!c || !out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  collect_timing(c);
+  *out = c->tacc;
+  return KKM_OK;
+}
+
+int kkm_get_info(kkm_ctx* c, kkm_info* out) {
+  if (!c || !out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  out->n = c->sz.n;
+  out->d = c->d;
+  out->d_pad = c->sz.d_pad;
+  out->kind = c->kind;
+  out->mode = c->mode;
+  out->ld = c->sz.ld;
+  out->bytes_K = c->mode == KKM_MODE_RESIDENT ? k_bytes(c->sz) : 0;
+  out->bytes_total = c->held;
+  out->fixups = c->fixups;
+  return KKM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Internal declarations shared by the engine's HIP translation units.
+// Every kernel here is written for gfx950 (CDNA4: 64-lane wavefronts, fp32
+// MFMA, 160 KB LDS per CU, 8 XCDs with private L2s).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace kkm {
+
+// K-build tiling: 128 x 128 output tile per 256-thread workgroup (2 x 2
+// wavefronts, each 64 x 64 = 2 x 2 MFMA 32x32 blocks), 16-wide k chunks.
+constexpr int kTile = 128;
+constexpr int kBK = 16;
+
+// One-hot SpMM: a workgroup streams a stripe of kStripe columns of K over a
+// chunk of at most kChunk rows that all belong to one cluster.
+constexpr int kStripe = 1024;
+constexpr int kChunk = 256;
+
+// Points per workgroup in the label/assign/scatter kernels.
+constexpr int kBlk = 256;
+
+enum Kind { LINEAR = 0, POLY = 1, GAUSS = 2 };
+
+struct KappaParams {
+  int kind;
+  float gamma;
+  float coef0;
+  int degree;
+  float neg_g_log2e;  // -gamma * log2(e): exp(-gamma s) = exp2(neg_g_log2e * s)
+  float fix_scale;    // Gaussian: error estimate of s is fix_scale * (|x|^2 + |y|^2)
+  float fix_tol;      // recompute an entry when gamma * err(s) * K exceeds this
+};
+
+// Everything a clustering iteration reads and writes on the device.
+struct IterBufs {
+  int64_t n, ld;
+  int k, nblk, nstripes, qmax;
+  const float* diagK;   // n
+  const double* trK;    // 1
+  float* Et;            // k x ld: E transposed, E(i,j) at Et[j*ld + i]
+  float* P;             // qmax x ld: per-chunk partial row sums
+  unsigned* spmm_cnt;   // nstripes x k arrival counters
+  double* zpart;        // k x nstripes partial self-term sums
+  int* hist;            // k x nblk per-block cluster counts (cluster-major)
+  int* base;            // k x nblk sorted position of each block's first member
+  int* off;             // k + 1 cluster offsets in the sorted order
+  int* qfirst;          // k + 1 first chunk of each cluster
+  int* chunk_j;         // qmax
+  int* chunk_p0;        // qmax
+  int* chunk_p1;        // qmax
+  int* nchunks;         // 1
+  int* perm;            // n: sorted position -> point
+  int* pos;             // n: point -> sorted position
+  int* status;          // 1: bit 0 = id out of range
+  unsigned* done_ctr;   // 1: arrival counter of the assign kernel
+};
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
+                        float* nrm, hipStream_t s);
+hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
+                             const KappaParams& kp, float* K, float* diagK, int2* fix_list,
+                             unsigned long long* fix_count, long long fix_cap, hipStream_t s);
+hipError_t launch_gauss_fixup_list(const float* Xp, int d_pad, int64_t ld, const KappaParams& kp,
+                                   const int2* fix_list, long long count, float* K, hipStream_t s);
+hipError_t launch_gauss_fixup_scan(const float* Xp, const float* nrm, int64_t n, int d_pad,
+                                   int64_t ld, const KappaParams& kp, float* K, hipStream_t s);
+hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
+hipError_t launch_fill_diag(float* diagK, int64_t n, float v, hipStream_t s);
+
+hipError_t launch_zero_ints(int* p, int64_t count, hipStream_t s);
+// mode 0: validate cl_in, count, per-block histogram (no distances).
+// mode 1: distances from Et/zpart/counts_in, argmin -> cl_out, new counts.
+hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
+                         int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
+                         float* D_out, hipStream_t s);
+hipError_t launch_scatter(const IterBufs& b, const int* cl, int* zero_counts, int* zero_changed,
+                          hipStream_t s);
+hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, const int* cl, hipStream_t s);
+hipError_t launch_et_to_e(const IterBufs& b, const int* counts, float* E, hipStream_t s);
+
+}  // namespace kkm

@@ -1,0 +1,213 @@
+"""Thin ctypes binding to libkkm.so: the C ABI of include/kkm.h under the same names.
+
+Only argument marshalling happens here: device tensors become raw pointers
+(after dtype/device/contiguity checks), host results come back as Python
+values, and a non-zero status raises KKMError with the library's message.
+Every step of the computation runs in the library's HIP kernels.  If the
+library has not been built, loading it fails loudly; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkkm.so")
+
+KKM_OK, KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP, KKM_ERR_STATE, KKM_ERR_DEVICE_DATA = 0, -1, -2, -3, -4, -5
+KKM_LINEAR, KKM_POLY, KKM_GAUSS = 0, 1, 2
+KKM_MODE_AUTO, KKM_MODE_RESIDENT, KKM_MODE_ONTHEFLY = 0, 1, 2
+KKM_MAX_K = 4096
+PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "other")
+KINDS = {"linear": KKM_LINEAR, "poly": KKM_POLY, "gauss": KKM_GAUSS}
+MODES = {"auto": KKM_MODE_AUTO, "resident": KKM_MODE_RESIDENT, "onthefly": KKM_MODE_ONTHEFLY}
+
+
+class KKMError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"kkm error {code}: {msg}")
+        self.code = code
+
+
+class kkm_params(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_float), ("coef0", ctypes.c_float),
+                ("degree", ctypes.c_int32), ("mode", ctypes.c_int32)]
+
+
+class kkm_timing(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * len(PHASES)), ("launches", ctypes.c_int64 * len(PHASES))]
+
+
+class kkm_info(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int32), ("d_pad", ctypes.c_int32),
+                ("kind", ctypes.c_int32), ("mode", ctypes.c_int32), ("ld", ctypes.c_int64),
+                ("bytes_K", ctypes.c_size_t), ("bytes_total", ctypes.c_size_t),
+                ("fixups", ctypes.c_int64)]
+
+
+_lib = None
+_vp, _i32, _i64, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_size_t
+_SIGS = {
+    "kkm_abi_version": ([], _i32),
+    "kkm_last_error": ([_vp], ctypes.c_char_p),
+    "kkm_create": ([ctypes.POINTER(_vp), _vp, _sz], _i32),
+    "kkm_destroy": ([_vp], _i32),
+    "kkm_plan": ([_i64, _i32, _i32, _sz, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
+    "kkm_check_build_args": ([_i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
+    "kkm_check_iterate_args": ([_i64, _i32, _i32], _i32),
+    "kkm_build_kernel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
+    "kkm_iterate": ([_vp, _vp, _i32, _i32, _f64, ctypes.POINTER(_i32), _vp], _i32),
+    "kkm_objective": ([_vp, _vp, _i32, ctypes.POINTER(_f64)], _i32),
+    "kkm_step": ([_vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(_f64)], _i32),
+    "kkm_copy_kernel_rows": ([_vp, _i64, _i64, _vp], _i32),
+    "kkm_copy_diag": ([_vp, _vp], _i32),
+    "kkm_set_timing": ([_vp, _i32], _i32),
+    "kkm_get_timing": ([_vp, ctypes.POINTER(kkm_timing)], _i32),
+    "kkm_get_info": ([_vp, ctypes.POINTER(kkm_info)], _i32),
+}
+
+
+def lib():
+    """Load libkkm.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python __graft_entry__.py build` "
+                               "(hipcc --offload-arch=gfx950); the engine has no fallback")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes, f.restype = args, res
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, ctx=None):
+    if rc != KKM_OK:
+        msg = lib().kkm_last_error(ctx)
+        raise KKMError(rc, msg.decode() if msg else "")
+
+
+def _dev_ptr(t, dtype, name, numel=None):
+    """Raw device address of a contiguous CUDA/HIP tensor, with its checks."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements, got {t.numel()}")
+    return t.data_ptr()
+
+
+def current_stream_handle():
+    """hipStream_t of torch's current stream on the current device."""
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ------------------------------------------------------------------ the C ABI
+
+def kkm_abi_version() -> int:
+    return lib().kkm_abi_version()
+
+
+def kkm_last_error(ctx=None) -> str:
+    m = lib().kkm_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def kkm_create(stream=None, mem_budget: int = 0):
+    ctx = _vp()
+    _check(lib().kkm_create(ctypes.byref(ctx), stream, int(mem_budget)))
+    return ctx
+
+
+def kkm_destroy(ctx) -> None:
+    _check(lib().kkm_destroy(ctx))
+
+
+def kkm_plan(n: int, d: int, k: int, mem_budget: int, mode: int = KKM_MODE_AUTO):
+    """(resolved mode, device bytes); raises KKMError(KKM_ERR_OOM) if it cannot fit."""
+    m, b = _i32(), _sz()
+    _check(lib().kkm_plan(int(n), int(d), int(k), int(mem_budget), int(mode), ctypes.byref(m), ctypes.byref(b)))
+    return m.value, b.value
+
+
+def make_params(gamma=1.0, coef0=0.0, degree=1, mode=KKM_MODE_AUTO) -> kkm_params:
+    return kkm_params(float(gamma), float(coef0), int(degree), int(mode))
+
+
+def kkm_check_build_args(n, d, kind, params: kkm_params) -> int:
+    return lib().kkm_check_build_args(int(n), int(d), int(kind), ctypes.byref(params))
+
+
+def kkm_check_iterate_args(n, k, max_iter) -> int:
+    return lib().kkm_check_iterate_args(int(n), int(k), int(max_iter))
+
+
+def kkm_build_kernel(ctx, X, n: int, d: int, kind: int, params: kkm_params) -> None:
+    import torch
+    _check(lib().kkm_build_kernel(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
+                                  int(kind), ctypes.byref(params)), ctx)
+
+
+def kkm_iterate(ctx, V, k: int, max_iter: int, tol: float = -1.0):
+    """Returns (iters_done, obj_hist[:iters_done] as numpy fp64)."""
+    import torch
+    it = _i32()
+    hist = np.zeros(max(int(max_iter), 1), dtype=np.float64)
+    _check(lib().kkm_iterate(ctx, _dev_ptr(V, torch.int32, "V"), int(k), int(max_iter), float(tol),
+                             ctypes.byref(it), hist.ctypes.data), ctx)
+    return it.value, hist[:it.value].copy()
+
+
+def kkm_objective(ctx, V, k: int) -> float:
+    import torch
+    J = _f64()
+    _check(lib().kkm_objective(ctx, _dev_ptr(V, torch.int32, "V"), int(k), ctypes.byref(J)), ctx)
+    return J.value
+
+
+def kkm_step(ctx, cl_in, k: int, E=None, z=None, D=None, cl_out=None, counts_out=None) -> float:
+    """One step with every intermediate; returns J(cl_in).  Outputs are device tensors or None."""
+    import torch
+    J = _f64()
+    _check(lib().kkm_step(ctx, _dev_ptr(cl_in, torch.int32, "cl_in"), int(k),
+                          _dev_ptr(E, torch.float32, "E"), _dev_ptr(z, torch.float32, "z", int(k)),
+                          _dev_ptr(D, torch.float32, "D"), _dev_ptr(cl_out, torch.int32, "cl_out"),
+                          _dev_ptr(counts_out, torch.int32, "counts_out", int(k)), ctypes.byref(J)), ctx)
+    return J.value
+
+
+def kkm_copy_kernel_rows(ctx, r0: int, r1: int, out) -> None:
+    import torch
+    _check(lib().kkm_copy_kernel_rows(ctx, int(r0), int(r1), _dev_ptr(out, torch.float32, "out")), ctx)
+
+
+def kkm_copy_diag(ctx, out) -> None:
+    import torch
+    _check(lib().kkm_copy_diag(ctx, _dev_ptr(out, torch.float32, "out")), ctx)
+
+
+def kkm_set_timing(ctx, enable: bool) -> None:
+    _check(lib().kkm_set_timing(ctx, 1 if enable else 0), ctx)
+
+
+def kkm_get_timing(ctx) -> dict:
+    t = kkm_timing()
+    _check(lib().kkm_get_timing(ctx, ctypes.byref(t)), ctx)
+    return {p: (t.ms[i], t.launches[i]) for i, p in enumerate(PHASES)}
+
+
+def kkm_get_info(ctx) -> dict:
+    i = kkm_info()
+    _check(lib().kkm_get_info(ctx, ctypes.byref(i)), ctx)
+    return {f: getattr(i, f) for f, _ in kkm_info._fields_}

@@ -1,0 +1,127 @@
+"""The C-ABI library on the host: it loads, exports every function include/kkm.h
+declares, and its pure-host logic (argument checks, capacity planning) behaves
+as documented.  Nothing here launches GPU work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_17136_amd import kkm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kkm.h")
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kkm_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(kkm.LIB_PATH):
+        pytest.fail("libkkm.so is not built; run `python __graft_entry__.py build` first")
+    return kkm.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = header_functions()
+    assert len(names) >= 15, names
+    for name in names:
+        assert hasattr(L, name), f"{name} declared in kkm.h but not exported"
+    assert set(kkm._SIGS) == set(names), "binding and header disagree"
+
+
+def test_abi_version(L):
+    assert kkm.kkm_abi_version() == 1
+    hdr = open(HEADER).read()
+    assert "#define KKM_ABI_VERSION 1" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+
+
+def test_library_is_built_for_gfx950_only(L):
+    blob = open(kkm.LIB_PATH, "rb").read()
+    assert b"gfx950" in blob
+    for other in (b"gfx942", b"gfx90a", b"gfx1100"):
+        assert other not in blob
+
+
+@pytest.mark.parametrize("n,d,kind,params,ok", [
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0), True),
+    (1, 1, kkm.KKM_LINEAR, (0.0, 0.0, 0, 0), True),
+    (1000, 16, kkm.KKM_GAUSS, (0.5, 0.0, 1, 1), True),
+    (0, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0), False),
+    (2 ** 31, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0), False),
+    (1000, 0, kkm.KKM_POLY, (1.0, 1.0, 2, 0), False),
+    (1000, 70000, kkm.KKM_POLY, (1.0, 1.0, 2, 0), False),
+    (1000, 16, 3, (1.0, 1.0, 2, 0), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 0, 0), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 17, 0), False),
+    (1000, 16, kkm.KKM_POLY, (float("nan"), 1.0, 2, 0), False),
+    (1000, 16, kkm.KKM_GAUSS, (0.0, 0.0, 1, 0), False),
+    (1000, 16, kkm.KKM_GAUSS, (-1.0, 0.0, 1, 0), False),
+    (1000, 16, kkm.KKM_GAUSS, (float("inf"), 0.0, 1, 0), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 5), False),
+])
+def test_build_argument_checks(L, n, d, kind, params, ok):
+    rc = kkm.kkm_check_build_args(n, d, kind, kkm.make_params(*params))
+    assert (rc == kkm.KKM_OK) == ok, kkm.kkm_last_error()
+    if not ok:
+        assert rc == kkm.KKM_ERR_ARG and kkm.kkm_last_error()
+
+
+@pytest.mark.parametrize("n,k,it,ok", [
+    (100, 1, 0, True), (100, 100, 5, True), (100, 101, 5, False), (100, 0, 5, False),
+    (100, 7, -1, False), (10 ** 6, kkm.KKM_MAX_K, 1, True), (10 ** 6, kkm.KKM_MAX_K + 1, 1, False),
+])
+def test_iterate_argument_checks(L, n, k, it, ok):
+    rc = kkm.kkm_check_iterate_args(n, k, it)
+    assert (rc == kkm.KKM_OK) == ok
+    if not ok:
+        assert rc == kkm.KKM_ERR_ARG
+
+
+def test_null_context_is_rejected_without_a_gpu(L):
+    p = kkm.make_params(1.0, 1.0, 2)
+    assert L.kkm_build_kernel(None, None, 10, 2, kkm.KKM_POLY, ctypes.byref(p)) == kkm.KKM_ERR_ARG
+    assert L.kkm_iterate(None, None, 2, 1, -1.0, None, None) == kkm.KKM_ERR_ARG
+    assert L.kkm_destroy(None) == kkm.KKM_OK
+    assert L.kkm_create(None, None, 0) == kkm.KKM_ERR_ARG
+
+
+def test_plan_resident_when_it_fits(L):
+    n, d, k = 20000, 784, 10
+    mode, need = kkm.kkm_plan(n, d, k, 288 << 30)
+    assert mode == kkm.KKM_MODE_RESIDENT
+    assert 4 * n * n <= need <= 4 * n * n * 1.1
+
+
+def test_plan_falls_back_to_on_the_fly(L):
+    n, d, k = 200000, 54, 7
+    mode, need = kkm.kkm_plan(n, d, k, 100 << 30)          # K alone is 160 GB
+    assert mode == kkm.KKM_MODE_ONTHEFLY and need < (1 << 30)
+    mode, need = kkm.kkm_plan(n, d, k, 288 << 30)
+    assert mode == kkm.KKM_MODE_RESIDENT and need > 4 * n * n
+
+
+def test_plan_reports_oom(L):
+    with pytest.raises(kkm.KKMError) as e:
+        kkm.kkm_plan(200000, 54, 7, 100 << 30, kkm.KKM_MODE_RESIDENT)
+    assert e.value.code == kkm.KKM_ERR_OOM
+    with pytest.raises(kkm.KKMError) as e:
+        kkm.kkm_plan(200000, 54, 7, 1 << 20, kkm.KKM_MODE_AUTO)
+    assert e.value.code == kkm.KKM_ERR_OOM
+
+
+def test_plan_rejects_bad_sizes(L):
+    for args in [(0, 5, 1), (10, 0, 1), (10, 5, 11), (10, 5, 0)]:
+        with pytest.raises(kkm.KKMError) as e:
+            kkm.kkm_plan(*args, 1 << 30)
+        assert e.value.code == kkm.KKM_ERR_ARG
+
+
+def test_binding_refuses_host_tensors(L):
+    torch = pytest.importorskip("torch")
+    with pytest.raises(TypeError):
+        kkm._dev_ptr(torch.zeros(4), torch.float32, "X")

@@ -1,0 +1,174 @@
+"""GPU parity: the HIP engine through its C ABI against the CPU oracle.
+
+Small problems (the oracle forms all of K in seconds) with ragged sizes that
+span several 128 x 128 tiles and partial 1024-column stripes, every kernel
+kind, and the degenerate cases (n = 1, k = 1, k = n, empty clusters, exact
+ties, invalid ids).  The bar: K, E and D within 1e-4 row-scaled, z and J
+within 1e-4 relative, sizes exact, assignments exact except at near-ties of
+the oracle's distances, and exact trajectories on well-separated input.
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import TOL, Engine, assignment_mismatches, rel_err, rowscaled_err
+from paper_2601_17136_amd import datagen
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch_cuda():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.fail("GPU test on a machine without a GPU")
+    return torch
+
+
+CASES = {
+    # name: (points, k, kind, gamma, coef0, degree, init seed)
+    "blobs-n2000-poly": (lambda: datagen.make_points(1)[0], 8, "poly", 1.0, 1.0, 2, None),
+    "ragged-poly3": (lambda: datagen.separated_blobs(1037, 13, 5, seed=3, spread=2.0, sigma=1.0)[0],
+                     5, "poly", 0.5, 1.0, 3, 11),
+    "ragged-gauss": (lambda: datagen.make_points(2, n=777, d=37)[0], 9, "gauss", 0.3, 0.0, 1, 12),
+    "linear-n300": (lambda: datagen.separated_blobs(300, 3, 4, seed=4, spread=3.0, sigma=1.0)[0],
+                    4, "linear", 1.0, 0.0, 1, 13),
+    "rings-n3000-gauss": (lambda: datagen.make_points(4, n=3000)[0], 64, "gauss", 0.5, 0.0, 1, 14),
+    "n129-d1": (lambda: datagen.separated_blobs(129, 1, 3, seed=5)[0], 3, "poly", 0.25, 2.0, 2, 15),
+    "n128-d16": (lambda: datagen.make_points(5, n=128, d=16)[0], 7, "gauss", 1.0 / 16, 0.0, 1, 16),
+    "n2-k2": (lambda: np.array([[0.0, 1.0], [2.0, -1.0]], np.float32), 2, "poly", 1.0, 1.0, 2, 17),
+    "n1-k1": (lambda: np.array([[0.5]], np.float32), 1, "gauss", 1.0, 0.0, 1, 18),
+    "stripes-n2100-k1": (lambda: datagen.make_points(3, n=2100, d=20)[0], 1, "poly", 0.1, 1.0, 2, 19),
+}
+
+
+def _setup(name, oracle):
+    pts, k, kind, g, c, p, seed = CASES[name]
+    X = pts()
+    n = X.shape[0]
+    cl = datagen.make_init(1, n, k) if seed is None else datagen.random_init(n, k, seed)
+    kern = oracle.Kernel(kind, g, c, p)
+    return X, k, kind, g, c, p, cl, kern
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_kernel_matrix(oracle, name):
+    _torch_cuda()
+    print(f"[gpu] K parity {name}", flush=True)
+    X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
+    with Engine(X, kind, g, c, p) as eng:
+        K = eng.K_rows()
+        diag = eng.diag()
+        info = eng.info()
+    Kref = kern.matrix(X)
+    err = rowscaled_err(K, Kref)
+    assert err <= TOL, f"K row-scaled error {err:.3e}"
+    assert np.array_equal(K, K.T), "K is not exactly symmetric"
+    np.testing.assert_array_equal(diag, np.diag(K))
+    if kind == "gauss":
+        assert np.all(diag == 1.0)
+    print(f"[gpu] {name}: K err {err:.2e}, fixups {info['fixups']}", flush=True)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_step(oracle, name):
+    _torch_cuda()
+    print(f"[gpu] step parity {name}", flush=True)
+    X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
+    ref = oracle.step_full(kern.matrix(X), cl, k)
+    with Engine(X, kind, g, c, p) as eng:
+        out = eng.step(cl, k)
+    np.testing.assert_array_equal(out["counts"], ref["counts"])
+    eE, eD = rowscaled_err(out["E"], ref["E"]), rowscaled_err(out["D"], ref["D"])
+    ez, eJ = rel_err(out["z"], ref["z"]), rel_err(out["J"], ref["J"]) if ref["J"] != 0 else abs(out["J"])
+    assert eE <= TOL and eD <= TOL and ez <= TOL and eJ <= TOL, (eE, eD, ez, eJ)
+    mism = assignment_mismatches(out["cl"], ref["cl"], ref["D"])
+    print(f"[gpu] {name}: E {eE:.2e} D {eD:.2e} z {ez:.2e} J {eJ:.2e} near-tie flips {mism}", flush=True)
+
+
+def test_blobs_trajectory_is_exact(oracle):
+    """Workload 1 (well separated): every update matches the oracle bit for bit."""
+    _torch_cuda()
+    w, X, _ = datagen.workload(1)
+    cl0 = datagen.make_init(1, w.n, w.k)
+    kern = oracle.Kernel(w.kind, w.gamma, w.coef0, w.degree)
+    K = kern.matrix(X)
+    _, done, hist_ref, traj = oracle.iterate_full(K, cl0, w.k, w.iters)
+    with Engine(X, w.kind, w.gamma, w.coef0, w.degree) as eng:
+        cl = cl0
+        for t in range(w.iters):
+            nxt, it, hist = eng.iterate(cl, w.k, 1)
+            assert it == 1 and np.array_equal(nxt, traj[t]), f"update {t} differs"
+            assert rel_err(hist[0], hist_ref[t]) <= TOL
+            cl = nxt
+        final, it, hist = eng.iterate(cl0, w.k, w.iters)
+    assert it == w.iters
+    np.testing.assert_array_equal(final, traj[-1])
+    assert np.max(np.abs(hist - hist_ref) / np.abs(hist_ref)) <= TOL
+
+
+def test_stop_rules_match_oracle(oracle):
+    _torch_cuda()
+    X, _ = datagen.separated_blobs(900, 4, 6, seed=30)
+    cl0 = datagen.random_init(900, 6, 31)
+    kern = oracle.Kernel("gauss", 0.05)
+    K = kern.matrix(X)
+    with Engine(X, "gauss", 0.05) as eng:
+        for tol in (0.0, 1e-3, -1.0):
+            cl_ref, done_ref, hist_ref, _ = oracle.iterate_full(K, cl0, 6, 40, tol=tol)
+            cl, done, hist = eng.iterate(cl0, 6, 40, tol=tol)
+            assert done == done_ref, (tol, done, done_ref)
+            np.testing.assert_array_equal(cl, cl_ref)
+            assert np.max(np.abs(hist - hist_ref) / np.abs(hist_ref)) <= TOL
+
+
+def test_empty_cluster_and_ties(oracle):
+    _torch_cuda()
+    X = np.array([[-1.0], [1.0], [0.0], [0.0], [3.0]], np.float32)
+    cl = np.array([0, 1, 0, 1, 1], np.int32)    # cluster 2 empty
+    kern = oracle.Kernel("linear")
+    ref = oracle.step_full(kern.matrix(X), cl, 3)
+    with Engine(X, "linear") as eng:
+        out = eng.step(cl, 3)
+    assert out["counts"][2] == 0 and np.all(np.isinf(out["D"][:, 2])) and out["z"][2] == 0
+    np.testing.assert_array_equal(out["cl"], ref["cl"])
+    assert rowscaled_err(out["D"], ref["D"]) <= TOL
+
+
+def test_each_point_its_own_cluster(oracle):
+    _torch_cuda()
+    X = datagen.make_points(2, n=70, d=9)[0]
+    with Engine(X, "gauss", 0.2) as eng:
+        out = eng.step(np.arange(70, dtype=np.int32), 70)
+    assert abs(out["J"]) <= 1e-4 * 70
+    np.testing.assert_array_equal(out["cl"], np.arange(70))
+    assert np.all(np.abs(np.diag(out["D"])) <= 1e-5)
+
+
+def test_invalid_ids_are_reported(oracle):
+    _torch_cuda()
+    from paper_2601_17136_amd import kkm
+    X = datagen.make_points(1, n=300)[0]
+    with Engine(X, "poly", 1.0, 1.0, 2) as eng:
+        for bad in (8, -1):
+            cl = datagen.random_init(300, 8, 3)
+            cl[123] = bad
+            with pytest.raises(kkm.KKMError) as e:
+                eng.iterate(cl, 8, 3)
+            assert e.value.code == kkm.KKM_ERR_DEVICE_DATA
+        cl, it, _ = eng.iterate(datagen.random_init(300, 8, 3), 8, 2)   # context still usable
+        assert it == 2
+
+
+def test_bitwise_reproducible(oracle):
+    _torch_cuda()
+    X = datagen.make_points(4, n=2500)[0]
+    cl = datagen.random_init(2500, 64, 40)
+    runs = []
+    for _ in range(2):
+        with Engine(X, "gauss", 0.5) as eng:
+            runs.append((eng.K_rows(0, 64), eng.step(cl, 64), eng.iterate(cl, 64, 5)))
+    (K1, s1, i1), (K2, s2, i2) = runs
+    assert np.array_equal(K1, K2)
+    for key in ("E", "D", "z", "cl", "counts"):
+        assert np.array_equal(s1[key], s2[key]), key
+    assert s1["J"] == s2["J"]
+    assert np.array_equal(i1[0], i2[0]) and np.array_equal(i1[2], i2[2])
