@@ -1,0 +1,178 @@
+"""Benchmark: exact Kernel K-means on one MI355X through the engine's C ABI.
+
+A step is one whole clustering job on synthetic input already resident in
+HBM: build K = kappa(X X^T), then run the workload's number of assignment
+updates (E = K V^T, z, D, argmin, sizes) from the seeded initial ids.
+``value`` is clustering updates per second over the whole job (K build
+included).  Per-kernel times come from HIP events the library records on
+its stream during the timed steps; the K-build and per-update roofline
+figures are derived from them.
+
+Default workload: n=20,000 points, d=784, k=10, Gaussian kernel gamma=1/784,
+30 updates, K resident (1.6 GB).  ``--config N`` picks another workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+FP32_MFMA_PEAK_TF = 157.3    # MI355X dense fp32 matrix peak
+METRIC = "clustering iters/sec + K-build TFLOP/s, % of HBM / MFMA peak, 1 GPU"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (default 2: n=20000, d=784)")
+    ap.add_argument("--mode", choices=["resident", "onthefly"], default="resident")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="oracle sample sized for about this much host time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
+    return ap.parse_args()
+
+
+def cpu_baseline_sized(w, X, cl0, seconds):
+    """Pilot on 256 rows, then a sample sized for about ``seconds`` of host work."""
+    pilot = cpu_baseline(w, X, cl0, 256)
+    per_row = (w.iters / pilot["value"]) / X.shape[0]      # seconds of oracle work per row
+    rows = int(min(X.shape[0], max(256, seconds / max(per_row, 1e-9))))
+    return cpu_baseline(w, X, cl0, rows)
+
+
+def cpu_baseline(w, X, cl0, rows):
+    """The oracle (fp64 kernel entries from their definitions + NumPy steps) on a
+    row sample: K rows and w.iters updates restricted to those rows, scaled by
+    n / rows to the whole job.  The self-terms z are taken once from the sample
+    rows' own-cluster sums (what the update needs besides E)."""
+    import numpy as np
+
+    from oracle import kkm_oracle as oracle
+    n = X.shape[0]
+    rows = min(rows, n)
+    rng = np.random.default_rng(7)
+    sample = np.sort(rng.choice(n, size=rows, replace=False)).astype(np.int64)
+    kern = oracle.Kernel(w.kind, w.gamma, w.coef0, w.degree)
+    t0 = time.perf_counter()
+    K_rows = kern.block(X, sample, None)
+    diag = kern.pairs(X, sample, sample)
+    t1 = time.perf_counter()
+    cl = cl0.copy()
+    for _ in range(w.iters):
+        counts = oracle.cluster_sizes(cl, w.k)
+        E = oracle.one_hot_product(K_rows, cl, w.k)
+        own = oracle.mask(E, cl[sample])
+        z = oracle.self_terms(own, cl[sample], np.maximum(oracle.cluster_sizes(cl[sample], w.k), 1))
+        D = oracle.distances(diag, E, z, counts)
+        new = oracle.assign(D)
+        cl = cl.copy()
+        cl[sample] = new
+    t2 = time.perf_counter()
+    scale = n / rows
+    total = (t1 - t0 + t2 - t1) * scale
+    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    return {"value": w.iters / total, "unit": "iters/s", "cores": threads, "kind": "oracle",
+            "sample": f"K rows and {w.iters} updates on {rows} of {n} rows (fp64), "
+                      f"times scaled by n/rows={scale:.1f}: K {1e3 * (t1 - t0) * scale:.0f} ms, "
+                      f"updates {1e3 * (t2 - t1) * scale:.0f} ms"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the engine is single-GPU; multi-GPU sharding is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2601_17136_amd import datagen, kkm
+
+    w = datagen.WORKLOADS[args.config]
+    X, _ = datagen.make_points(args.config)
+    cl0 = datagen.make_init(args.config, w.n, w.k)
+    n, d, k = w.n, w.d, w.k
+    print(f"bench: {w.describe()} mode={args.mode} steps={args.steps} warmup={args.warmup}",
+          file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    torch.cuda.empty_cache()
+    Xd = torch.from_numpy(X).cuda()
+    V0 = torch.from_numpy(cl0).cuda()
+    Vs = [V0.clone() for _ in range(args.steps + args.warmup)]
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.MODES[args.mode])
+    kind = kkm.KINDS[w.kind]
+
+    def job(V):
+        kkm.kkm_build_kernel(ctx, Xd, n, d, kind, params)
+        return kkm.kkm_iterate(ctx, V, k, w.iters, -1.0)
+
+    for s in range(args.warmup):
+        job(Vs[s])
+        print(f"bench: warmup step {s} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    kkm.kkm_set_timing(ctx, not args.no_timing)
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        it, hist = job(Vs[args.warmup + s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    phases = kkm.kkm_get_timing(ctx)
+    info = kkm.kkm_get_info(ctx)
+    kkm.kkm_set_timing(ctx, False)
+    print(f"bench: timed {args.steps} steps in {t1 - t0:.3f} s", file=sys.stderr, flush=True)
+
+    ms_per_step = 1e3 * (t1 - t0) / args.steps
+    value = w.iters / (ms_per_step / 1e3)
+    out = {"metric": METRIC, "value": round(value, 3), "unit": "iters/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic",
+           "config": {"workload": w.describe() + f", K {args.mode}", "n": n, "d": d, "k": k,
+                      "iters": w.iters, "kernel": w.kind, "mode": args.mode, "parallelism": "1 GPU"}}
+
+    def avg(ph):
+        ms, cnt = phases[ph]
+        return (ms / cnt if cnt else float("nan")), cnt
+
+    if not args.no_timing:
+        spmm_ms, spmm_cnt = avg("spmm")
+        gemm_ms, _ = avg("gemm")
+        kbuild_ms = sum(phases[p][0] for p in ("stage", "gemm", "fixup")) / args.steps
+        iter_ms = sum(phases[p][0] for p in ("labels", "scatter", "spmm", "assign", "onthefly")) / args.steps
+        flops = float(n) * (n + 1) * d                     # symmetric half of X X^T, 2 flops per MAC
+        out["kbuild_ms"] = round(kbuild_ms, 4)
+        out["kbuild_tflops"] = round(flops / (gemm_ms * 1e-3) / 1e12, 3) if gemm_ms == gemm_ms else None
+        out["kbuild_frac_mfma"] = round(out["kbuild_tflops"] / FP32_MFMA_PEAK_TF, 4) if out["kbuild_tflops"] else None
+        out["update_ms"] = round(iter_ms / w.iters, 4)
+        out["updates_per_s_loop"] = round(w.iters / (iter_ms * 1e-3), 2)
+        out["phases_ms_per_step"] = {p: round(phases[p][0] / args.steps, 4) for p in kkm.PHASES if phases[p][1]}
+        if args.mode == "resident":
+            bytes_per = 4.0 * n * n                        # K streamed once per update
+            gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
+            out["roofline"] = {"kernel": "spmm_onehot", "bound": "hbm", "achieved": round(gbs, 1),
+                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                               "traffic": None, "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt}
+        tf = out["kbuild_tflops"]
+        out["roofline_kbuild"] = {"kernel": "gemm_kappa", "bound": "mfma", "achieved": tf,
+                                  "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
+                                  "frac": round(tf / FP32_MFMA_PEAK_TF, 4) if tf else None,
+                                  "traffic": None, "avg_launch_ms": round(gemm_ms, 5),
+                                  "gauss_fixups": info["fixups"]}
+    if not args.no_cpu_baseline:
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline_sized(w, X, cl0, args.cpu_seconds)
+    kkm.kkm_destroy(ctx)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
