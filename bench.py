@@ -147,7 +147,7 @@ def main():
         spmm_ms, spmm_cnt = avg("spmm")
         gemm_ms, _ = avg("gemm")
         kbuild_ms = sum(phases[p][0] for p in ("stage", "gemm", "fixup")) / args.steps
-        iter_ms = sum(phases[p][0] for p in ("labels", "scatter", "spmm", "assign", "onthefly")) / args.steps
+        iter_ms = sum(phases[p][0] for p in ("labels", "scatter", "spmm", "reduce", "assign", "onthefly")) / args.steps
         flops = float(n) * (n + 1) * d                     # symmetric half of X X^T, 2 flops per MAC
         out["kbuild_ms"] = round(kbuild_ms, 4)
         out["kbuild_tflops"] = round(flops / (gemm_ms * 1e-3) / 1e12, 3) if gemm_ms == gemm_ms else None

@@ -42,7 +42,7 @@ extern "C" {
 #endif
 
 #define KKM_ABI_VERSION 1
-#define KKM_MAX_K 4096 /* largest supported cluster count */
+#define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
   KKM_OK = 0,
@@ -85,8 +85,9 @@ enum {
   KKM_PHASE_SPMM = 5,    /* E = K V^T over stored K */
   KKM_PHASE_ASSIGN = 6,  /* z, distances, argmin, new sizes */
   KKM_PHASE_ONTHEFLY = 7,/* recomputed K tiles folded into E */
-  KKM_PHASE_OTHER = 8,   /* gathers, copies, trace */
-  KKM_NPHASE = 9
+  KKM_PHASE_REDUCE = 8,  /* per-cluster sums of the SpMM's chunk partials, self-term parts */
+  KKM_PHASE_OTHER = 9,   /* gathers, copies, trace */
+  KKM_NPHASE = 10
 };
 typedef struct kkm_timing {
   double ms[KKM_NPHASE];       /* summed kernel time per phase, milliseconds */

@@ -9,10 +9,12 @@
 // element of K, each row segment read as 4 KB of contiguous memory.  K is
 // symmetric, so the columns of E^T are the rows of E.
 //
-// Per iteration:  scatter (sorted order)  ->  spmm_onehot (E^T, partial self
-// terms)  ->  assign (z, distances, argmin, new sizes, next sort offsets).
+// Per update:  scatter (sorted order, chunk table)  ->  spmm_onehot (chunk
+// partial sums)  ->  spmm_reduce (E^T, partial self-terms)  ->  assign (z,
+// distances, argmin, new sizes, per-block histograms for the next scatter).
 // All reductions of floating-point values run in a fixed order, so results
-// are bitwise reproducible; only integer counters use atomics.
+// are bitwise reproducible; only integer counters use atomics, and no kernel
+// waits on another workgroup: every hand-off is a kernel boundary.
 #include "kkm_internal.h"
 
 namespace kkm {
@@ -23,78 +25,11 @@ __device__ inline int clamp_id(int c, int k) { return c < 0 ? 0 : (c >= k ? k - 
 
 // ----------------------------------------------------------------- assign
 //
-// mode 0 (labels): check ids, count cluster sizes and per-block histograms.
+// mode 0 (labels): check ids, cluster sizes and per-block histograms.
 // mode 1 (full):   z_j = (1/|L_j|^2) sum_s zpart[j][s]            (Eqs. 5-7)
 //                  D(i,j) = K(i,i) - 2 E(i,j)/|L_j| + z_j         (Eq. 8 + diag K)
 //                  cl'(i) = lowest j attaining min_j D(i,j); sizes of cl'.
-// Both modes end with the last-arriving workgroup turning the per-block
-// histograms into the sorted-order offsets and the SpMM chunk table.
-
-__device__ void sort_tables(const IterBufs& b, const int* __restrict__ counts, int* offs, int* qf,
-                            int* segsum) {
-  const int k = b.k, nb = b.nblk, tid = threadIdx.x;
-  if (tid == 0) {
-    int o = 0, q = 0;
-    for (int j = 0; j < k; ++j) {
-      const int c = counts[j];
-      offs[j] = o;
-      qf[j] = q;
-      o += c;
-      q += (c + kChunk - 1) / kChunk;
-    }
-    offs[k] = o;
-    qf[k] = q;
-    *b.nchunks = q;
-  }
-  __syncthreads();
-  for (int j = tid; j <= k; j += 256) {
-    b.off[j] = offs[j];
-    b.qfirst[j] = qf[j];
-  }
-  // base[j][blk] = offs[j] + number of members of j in blocks before blk
-  if (k <= 256) {
-    const int G = 256 / k, j = tid / G, g = tid % G;
-    const int seg = (nb + G - 1) / G, lo = g * seg, hi = (lo + seg < nb) ? lo + seg : nb;
-    int s = 0;
-    if (j < k)
-      for (int bb = lo; bb < hi; ++bb) s += b.hist[(int64_t)j * nb + bb];
-    segsum[tid] = s;
-    __syncthreads();
-    if (j < k) {
-      int run = offs[j];
-      for (int gg = 0; gg < g; ++gg) run += segsum[j * G + gg];
-      for (int bb = lo; bb < hi; ++bb) {
-        b.base[(int64_t)j * nb + bb] = run;
-        run += b.hist[(int64_t)j * nb + bb];
-      }
-    }
-  } else {
-    for (int j = tid; j < k; j += 256) {
-      int run = offs[j];
-      for (int bb = 0; bb < nb; ++bb) {
-        b.base[(int64_t)j * nb + bb] = run;
-        run += b.hist[(int64_t)j * nb + bb];
-      }
-    }
-  }
-  // chunk q of cluster j covers sorted positions [p0, p1), at most kChunk long
-  const int nq = qf[k];
-  for (int q = tid; q < nq; q += 256) {
-    int lo = 0, hi = k - 1;  // last j with qf[j] <= q
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (qf[mid] <= q) lo = mid;
-      else hi = mid - 1;
-    }
-    const int j = lo;
-    const int p0 = offs[j] + (q - qf[j]) * kChunk;
-    const int end = offs[j + 1];
-    b.chunk_j[q] = j;
-    b.chunk_p0[q] = p0;
-    b.chunk_p1[q] = (p0 + kChunk < end) ? p0 + kChunk : end;
-  }
-}
-
+// The per-block histograms (cluster-major) feed the next scatter.
 template <int MODE>
 __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __restrict__ counts_in,
                                                      const int* __restrict__ cl_in,
@@ -110,10 +45,6 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
   float* zf = (float*)(zd + k);        // k
   float* sc = zf + k;                  // k
   int* hist = (int*)(sc + k);          // k
-  int* offs = hist + k;                // k + 1
-  int* qf = offs + k + 1;              // k + 1
-  int* segsum = qf + k + 1;            // 256
-  __shared__ int is_last;
 
   for (int j = tid; j < k; j += 256) hist[j] = 0;
   if (MODE == 1) {
@@ -175,19 +106,9 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
     if (c) atomicAdd(&counts_out[j], c);
   }
   if (MODE == 1 && tid == 0 && nchg && changed) atomicAdd(changed, nchg);
-
-  // the last workgroup to finish builds the tables for the next scatter/SpMM
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) is_last = (atomicAdd(b.done_ctr, 1u) == (unsigned)(gridDim.x - 1));
-  __syncthreads();
-  if (!is_last) return;
-  __threadfence();
-  if (tid == 0) *b.done_ctr = 0u;
-  sort_tables(b, counts_out, offs, qf, segsum);
 }
 
-static size_t assign_smem(int k) { return (size_t)k * 28 + 8 + 1024 + 64; }
+static size_t assign_smem(int k) { return (size_t)k * 20 + 64; }
 
 hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
                          int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
@@ -205,23 +126,84 @@ hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, cons
 
 // ----------------------------------------------------------------- scatter
 //
-// Stable counting sort: point i of block blk goes to
-//   base[cl(i)][blk] + (members of cl(i) in earlier wavefronts of blk)
-//                    + (members of cl(i) in earlier lanes of its wavefront).
-// Workgroup 0 also clears this iteration's size and change counters.
+// Stable counting sort of the points by cluster.  Point i of block blk goes to
+//   off[c] + (members of c in blocks before blk) + (members of c in earlier
+//   wavefronts of blk) + (members of c in earlier lanes of its wavefront),
+// c = cl(i), from the per-block histograms of the previous kernel.  Each
+// workgroup sums the histograms it needs itself.  Workgroup 0 also writes
+// the SpMM chunk table (chunk q: cluster j, sorted positions [p0, p1), at
+// most kChunk long) and clears this update's size and change counters.
 __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __restrict__ cl,
+                                                      const int* __restrict__ counts,
                                                       int* __restrict__ zero_counts,
                                                       int* __restrict__ zero_changed) {
-  extern __shared__ int wc[];  // 4 wavefronts x k
-  const int k = b.k, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (blockIdx.x == 0) {
+  extern __shared__ int smem_i[];
+  const int k = b.k, nb = b.nblk, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int blk = blockIdx.x;
+  int* wc = smem_i;          // 4 x k: per-wavefront counts of each cluster
+  int* offs = wc + 4 * k;    // k + 1: cluster offsets in the sorted order
+  int* qf = offs + k + 1;    // k + 1: first chunk of each cluster
+  int* basej = qf + k + 1;   // k: sorted position of this block's first member of j
+  int* segsum = basej + k;   // 256
+
+  for (int q = tid; q < 4 * k; q += 256) wc[q] = 0;
+  if (tid == 0) {
+    int o = 0, q = 0;
+    for (int j = 0; j < k; ++j) {
+      const int c = counts[j];
+      offs[j] = o;
+      qf[j] = q;
+      o += c;
+      q += (c + kChunk - 1) / kChunk;
+    }
+    offs[k] = o;
+    qf[k] = q;
+  }
+  __syncthreads();
+  if (k <= 256) {
+    const int G = 256 / k, j = tid / G, g = tid % G;
+    const int seg = (blk + G - 1) / G, lo = g * seg, hi = (lo + seg < blk) ? lo + seg : blk;
+    int s = 0;
+    if (j < k)
+      for (int bb = lo; bb < hi; ++bb) s += b.hist[(int64_t)j * nb + bb];
+    segsum[tid] = s;
+    __syncthreads();
+    if (j < k && g == 0) {
+      int run = offs[j];
+      for (int gg = 0; gg < G; ++gg) run += segsum[j * G + gg];
+      basej[j] = run;
+    }
+  } else {
+    for (int j = tid; j < k; j += 256) {
+      int run = offs[j];
+      for (int bb = 0; bb < blk; ++bb) run += b.hist[(int64_t)j * nb + bb];
+      basej[j] = run;
+    }
+  }
+  if (blk == 0) {
     if (zero_counts)
       for (int j = tid; j < k; j += 256) zero_counts[j] = 0;
     if (zero_changed && tid == 0) *zero_changed = 0;
+    for (int j = tid; j <= k; j += 256) {
+      b.off[j] = offs[j];
+      b.qfirst[j] = qf[j];
+    }
+    if (tid == 0) *b.nchunks = qf[k];
+    for (int q = tid; q < qf[k]; q += 256) {
+      int lo = 0, hi = k - 1;  // last j with qf[j] <= q
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (qf[mid] <= q) lo = mid;
+        else hi = mid - 1;
+      }
+      const int p0 = offs[lo] + (q - qf[lo]) * kChunk, end = offs[lo + 1];
+      b.chunk_j[q] = lo;
+      b.chunk_p0[q] = p0;
+      b.chunk_p1[q] = (p0 + kChunk < end) ? p0 + kChunk : end;
+    }
   }
-  for (int q = tid; q < 4 * k; q += 256) wc[q] = 0;
-  __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * kBlk + tid;
+
+  const int64_t i = (int64_t)blk * kBlk + tid;
   const bool valid = i < b.n;
   const int lab = valid ? clamp_id(cl[i], k) : -1;
   int rank = 0;
@@ -236,17 +218,18 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
   }
   __syncthreads();
   if (valid) {
-    int r = b.base[(int64_t)lab * b.nblk + blockIdx.x] + rank;
+    int r = basej[lab] + rank;
     for (int ww = 0; ww < w; ++ww) r += wc[ww * k + lab];
     b.perm[r] = (int)i;
     b.pos[i] = r;
   }
 }
 
-hipError_t launch_scatter(const IterBufs& b, const int* cl, int* zero_counts, int* zero_changed,
-                          hipStream_t s) {
-  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)b.nblk), dim3(256), (size_t)4 * b.k * sizeof(int),
-                     s, b, cl, zero_counts, zero_changed);
+hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
+                          int* zero_changed, hipStream_t s) {
+  const size_t sm = (size_t)(7 * b.k + 2 + 256) * sizeof(int);
+  hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)b.nblk), dim3(256), sm, s, b, cl, counts,
+                     zero_counts, zero_changed);
   return hipGetLastError();
 }
 
@@ -254,60 +237,57 @@ hipError_t launch_scatter(const IterBufs& b, const int* cl, int* zero_counts, in
 //
 // Workgroup (stripe, q): columns [stripe*1024, +1024) of the rows listed in
 // chunk q (one cluster j, at most 256 rows in sorted order).  Each lane keeps
-// one float4 accumulator; rows are summed in sorted order.  The chunk's sum
-// goes to P[q]; the last chunk of cluster j to arrive for this stripe adds
-// the chunks of j in chunk order, writes E^T(j, stripe), and the stripe's
-// share of sum_{i in L_j} E(i, j) for the self-term z_j.
-__global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restrict__ K, IterBufs b,
-                                                          const int* __restrict__ cl) {
+// one float4 accumulator; rows are summed in sorted order with non-temporal
+// 16-byte loads (K has no reuse within an update) and the chunk's sum goes
+// to P[q].  A second kernel adds the chunks of each cluster in chunk order;
+// the kernel boundary makes the partial sums visible across XCDs without a
+// device-scope fence per workgroup, which costs more than half the bandwidth.
+__global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restrict__ K, IterBufs b) {
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int q = (int)(blockIdx.x / (unsigned)ns);
   if (q >= *b.nchunks) return;
-  const int j = b.chunk_j[q], p0 = b.chunk_p0[q], p1 = b.chunk_p1[q];
+  const int p0 = b.chunk_p0[q], p1 = b.chunk_p1[q];
   const int tid = threadIdx.x;
   __shared__ int rows[kChunk];
-  __shared__ int last;
-  __shared__ double red[4];
   for (int p = p0 + tid; p < p1; p += 256) rows[p - p0] = b.perm[p];
   __syncthreads();
 
   const int64_t ld = b.ld;
   const int64_t col = (int64_t)stripe * kStripe + tid * 4;
-  const bool active = col < ld;
+  if (col >= ld) return;
   f4 acc = {0.f, 0.f, 0.f, 0.f};
   const int nr = p1 - p0;
-  if (active) {
-    const float* base = K + col;
-    int r = 0;
-    for (; r + 8 <= nr; r += 8) {
-      f4 v[8];
+  const float* base = K + col;
+  int r = 0;
+  for (; r + 8 <= nr; r += 8) {
+    f4 v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        v[u] = __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r + u] * ld));
+    for (int u = 0; u < 8; ++u)
+      v[u] = __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r + u] * ld));
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc += v[u];
-    }
-    for (; r < nr; ++r) acc += __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r] * ld));
+    for (int u = 0; u < 8; ++u) acc += v[u];
   }
+  for (; r < nr; ++r) acc += __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r] * ld));
+  *(f4*)(b.P + (int64_t)q * ld + col) = acc;
+}
 
+// Workgroup (stripe, j): E^T(j, stripe) = sum of cluster j's chunk partials in
+// chunk order, and the stripe's share of sum_{i in L_j} E(i, j) (fp64) for z_j.
+__global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int* __restrict__ cl) {
+  const int ns = b.nstripes;
+  const int stripe = (int)(blockIdx.x % (unsigned)ns);
+  const int j = (int)(blockIdx.x / (unsigned)ns);
   const int qa = b.qfirst[j], qb = b.qfirst[j + 1];
-  f4 e = acc;
-  if (qb - qa > 1) {
-    if (active) *(f4*)(b.P + (int64_t)q * ld + col) = acc;
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) last = (atomicAdd(&b.spmm_cnt[stripe * b.k + j], 1u) == (unsigned)(qb - qa - 1));
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    if (tid == 0) b.spmm_cnt[stripe * b.k + j] = 0u;
-    e = (f4){0.f, 0.f, 0.f, 0.f};
-    if (active)
-      for (int qq = qa; qq < qb; ++qq) e += (qq == q) ? acc : *(const f4*)(b.P + (int64_t)qq * ld + col);
-  }
+  if (qa == qb) return;  // empty cluster: E^T(j, .) and z_j are never read
+  const int tid = threadIdx.x;
+  __shared__ double red[4];
+  const int64_t ld = b.ld;
+  const int64_t col = (int64_t)stripe * kStripe + tid * 4;
   double zs = 0.0;
-  if (active) {
+  if (col < ld) {
+    f4 e = *(const f4*)(b.P + (int64_t)qa * ld + col);
+    for (int q = qa + 1; q < qb; ++q) e += *(const f4*)(b.P + (int64_t)q * ld + col);
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -319,9 +299,14 @@ __global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restric
   if (tid == 0) b.zpart[(int64_t)j * ns + stripe] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, const int* cl, hipStream_t s) {
+hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s) {
   const long long grid = (long long)b.nstripes * b.qmax;
-  hipLaunchKernelGGL(spmm_onehot_kernel, dim3((unsigned)grid), dim3(256), 0, s, K, b, cl);
+  hipLaunchKernelGGL(spmm_onehot_kernel, dim3((unsigned)grid), dim3(256), 0, s, K, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s) {
+  hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl);
   return hipGetLastError();
 }
 

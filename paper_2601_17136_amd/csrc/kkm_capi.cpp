@@ -69,13 +69,12 @@ size_t ws_bytes(const Sizes& s, int k) {
   size_t b = 0;
   b += (size_t)k * s.ld * 4;              // Et
   b += (size_t)qmax * s.ld * 4;           // P
-  b += (size_t)s.nstripes * k * 4;        // spmm counters
   b += (size_t)k * s.nstripes * 8;        // zpart
   b += (size_t)2 * k * s.nblk * 4;        // hist, base
   b += (size_t)2 * (k + 1) * 4;           // off, qfirst
   b += (size_t)3 * qmax * 4 + 4;          // chunk table
   b += (size_t)4 * s.n * 4;               // perm, pos, two id buffers
-  b += (size_t)2 * k * 4 + 64;            // counts, status, done counter
+  b += (size_t)2 * k * 4 + 64;            // counts, status
   return b + 32 * 256;                    // alignment slack
 }
 
@@ -253,7 +252,6 @@ int carve_ws(kkm_ctx* c, int k) {
   b.trK = c->trK;
   b.Et = (float*)take((size_t)k * s.ld * 4);
   b.P = (float*)take((size_t)qmax * s.ld * 4);
-  b.spmm_cnt = (unsigned*)take((size_t)s.nstripes * k * 4);
   b.zpart = (double*)take((size_t)k * s.nstripes * 8);
   b.hist = (int*)take((size_t)k * s.nblk * 4);
   b.base = (int*)take((size_t)k * s.nblk * 4);
@@ -270,11 +268,7 @@ int carve_ws(kkm_ctx* c, int k) {
   c->counts[0] = (int*)take((size_t)k * 4);
   c->counts[1] = (int*)take((size_t)k * 4);
   b.status = (int*)take(4);
-  b.done_ctr = (unsigned*)take(4);
   c->k_ws = k;
-  // counters that kernels expect at zero between uses
-  HIP_TRY(c, launch_zero_ints((int*)b.spmm_cnt, (int64_t)s.nstripes * k, c->stream), "zero counters");
-  HIP_TRY(c, launch_zero_ints((int*)b.done_ctr, 1, c->stream), "zero counters");
   return KKM_OK;
 }
 
@@ -323,15 +317,17 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
   int* cout = c->counts[(t + 1) & 1];
   int rc;
   if ((rc = run(c, KKM_PHASE_SCATTER, "scatter", [&] {
-         return launch_scatter(b, cur, cout, c->changed + t, c->stream);
+         return launch_scatter(b, cur, cin, cout, c->changed + t, c->stream);
        })))
     return rc;
   if (c->mode == KKM_MODE_RESIDENT) {
-    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, cur, c->stream); })))
+    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
       return rc;
   } else {
     return fail(c, KKM_ERR_STATE, "on-the-fly mode is not available in this build");
   }
+  if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
+    return rc;
   return run(c, KKM_PHASE_ASSIGN, "assign", [&] {
     return launch_assign(1, b, cin, cur, nxt, cout, c->changed + t, c->obj + t, z_out, D_out, c->stream);
   });

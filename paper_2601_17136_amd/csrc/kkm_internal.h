@@ -41,7 +41,6 @@ struct IterBufs {
   const double* trK;    // 1
   float* Et;            // k x ld: E transposed, E(i,j) at Et[j*ld + i]
   float* P;             // qmax x ld: per-chunk partial row sums
-  unsigned* spmm_cnt;   // nstripes x k arrival counters
   double* zpart;        // k x nstripes partial self-term sums
   int* hist;            // k x nblk per-block cluster counts (cluster-major)
   int* base;            // k x nblk sorted position of each block's first member
@@ -54,7 +53,6 @@ struct IterBufs {
   int* perm;            // n: sorted position -> point
   int* pos;             // n: point -> sorted position
   int* status;          // 1: bit 0 = id out of range
-  unsigned* done_ctr;   // 1: arrival counter of the assign kernel
 };
 
 // ---------------------------------------------------------------- launchers
@@ -73,12 +71,14 @@ hipError_t launch_fill_diag(float* diagK, int64_t n, float v, hipStream_t s);
 hipError_t launch_zero_ints(int* p, int64_t count, hipStream_t s);
 // mode 0: validate cl_in, count, per-block histogram (no distances).
 // mode 1: distances from Et/zpart/counts_in, argmin -> cl_out, new counts.
+// counts_out must be zero on entry (scatter clears the next update's).
 hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
                          int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
                          float* D_out, hipStream_t s);
-hipError_t launch_scatter(const IterBufs& b, const int* cl, int* zero_counts, int* zero_changed,
-                          hipStream_t s);
-hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, const int* cl, hipStream_t s);
+hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
+                          int* zero_changed, hipStream_t s);
+hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_et_to_e(const IterBufs& b, const int* counts, float* E, hipStream_t s);
 
 }  // namespace kkm
