@@ -33,6 +33,7 @@ __device__ inline int clamp_id(int c, int k) { return c < 0 ? 0 : (c >= k ? k - 
 template <int MODE>
 __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __restrict__ counts_in,
                                                      const int* __restrict__ cl_in,
+                                                     const int* __restrict__ pos,
                                                      int* __restrict__ cl_out,
                                                      int* __restrict__ counts_out,
                                                      int* __restrict__ changed,
@@ -79,13 +80,14 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
       }
     } else {
       const float dg = b.diagK[i];
+      const int64_t ei = pos ? (int64_t)pos[i] : i;  // column of E^T holding point i
       float best = INFINITY;
       int arg = -1;
       for (int j = 0; j < k; ++j) {
         const float s = sc[j];
         float Dv = INFINITY;
         if (s != 0.f) {
-          Dv = fmaf(s, b.Et[(int64_t)j * b.ld + i], dg + zf[j]);
+          Dv = fmaf(s, b.Et[(int64_t)j * b.ld + ei], dg + zf[j]);
           if (arg < 0 || Dv < best) {
             best = Dv;
             arg = j;
@@ -111,15 +113,15 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
 static size_t assign_smem(int k) { return (size_t)k * 20 + 64; }
 
 hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
-                         int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
-                         float* D_out, hipStream_t s) {
+                         const int* pos, int* cl_out, int* counts_out, int* changed, double* obj,
+                         float* z_out, float* D_out, hipStream_t s) {
   dim3 grid((unsigned)b.nblk), block(256);
   const size_t sm = assign_smem(b.k);
   if (mode == 0)
-    hipLaunchKernelGGL(assign_kernel<0>, grid, block, sm, s, b, counts_in, cl_in, cl_out,
+    hipLaunchKernelGGL(assign_kernel<0>, grid, block, sm, s, b, counts_in, cl_in, pos, cl_out,
                        counts_out, changed, obj, z_out, D_out);
   else
-    hipLaunchKernelGGL(assign_kernel<1>, grid, block, sm, s, b, counts_in, cl_in, cl_out,
+    hipLaunchKernelGGL(assign_kernel<1>, grid, block, sm, s, b, counts_in, cl_in, pos, cl_out,
                        counts_out, changed, obj, z_out, D_out);
   return hipGetLastError();
 }
@@ -311,18 +313,21 @@ hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s) {
 }
 
 // E (n x k, row-major) from E^T; empty clusters read as 0.
-__global__ void et_to_e_kernel(IterBufs b, const int* __restrict__ counts, float* __restrict__ E) {
+__global__ void et_to_e_kernel(IterBufs b, const int* __restrict__ counts, const int* __restrict__ pos,
+                               float* __restrict__ E) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= b.n * b.k) return;
   const int64_t i = t / b.k;
   const int j = (int)(t % b.k);
-  E[t] = counts[j] > 0 ? b.Et[(int64_t)j * b.ld + i] : 0.f;
+  const int64_t ei = pos ? (int64_t)pos[i] : i;
+  E[t] = counts[j] > 0 ? b.Et[(int64_t)j * b.ld + ei] : 0.f;
 }
 
-hipError_t launch_et_to_e(const IterBufs& b, const int* counts, float* E, hipStream_t s) {
+hipError_t launch_et_to_e(const IterBufs& b, const int* counts, const int* pos, float* E,
+                          hipStream_t s) {
   const int64_t tot = b.n * b.k;
   hipLaunchKernelGGL(et_to_e_kernel, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, b,
-                     counts, E);
+                     counts, pos, E);
   return hipGetLastError();
 }
 

@@ -18,11 +18,9 @@
 // the epilogue estimates the error of each entry and lists the ones whose
 // estimate is above a tolerance, and a second kernel recomputes those from
 // the coordinate differences.
-#include "kkm_internal.h"
+#include "tile_mma.h"
 
 namespace kkm {
-
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 // The t-th tile of the upper triangle in row-major order (row I holds
 // J = I .. nt-1), counted from the end so the search runs on the short rows.
@@ -38,28 +36,11 @@ __device__ inline void triangle_tile(int64_t t, int64_t nt, int64_t& I, int64_t&
 }
 
 template <int KIND>
-__device__ inline float kappa(float b, float ni, float nj, const KappaParams& kp) {
-  if (KIND == LINEAR) return b;
-  if (KIND == POLY) {
-    float t = fmaf(kp.gamma, b, kp.coef0), v = 1.f;
-    for (int e = kp.degree; e > 0; e >>= 1) {  // t^degree by squaring
-      if (e & 1) v *= t;
-      t *= t;
-    }
-    return v;
-  }
-  const float s = fmaxf(ni + nj - 2.f * b, 0.f);
-  return __builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
-}
-
-template <int KIND>
 __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm, int64_t n, int d_pad, int64_t ld,
     int64_t nt, int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
     int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long fix_cap) {
-  constexpr int LDSK = kBK + 4;  // padded k stride: conflict-free 16-byte reads
-  constexpr int BUF = 2 * kTile * LDSK;
-  __shared__ __attribute__((aligned(16))) float lds[2 * BUF];
+  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
 
   // Workgroup b runs on XCD b % 8.  Give each XCD a contiguous run of tiles
   // so that concurrent workgroups of one XCD share row block I in its L2.
@@ -74,71 +55,8 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, h = lane >> 5;
 
-  // Global -> LDS copy: 512 float4 per operand tile and k chunk, two per thread.
-  const int f0 = tid, f1 = tid + 256;
-  const float* Ag0 = Xp + (row0 + (f0 >> 2)) * d_pad + (f0 & 3) * 4;
-  const float* Ag1 = Xp + (row0 + (f1 >> 2)) * d_pad + (f1 & 3) * 4;
-  const float* Bg0 = Xp + (col0 + (f0 >> 2)) * d_pad + (f0 & 3) * 4;
-  const float* Bg1 = Xp + (col0 + (f1 >> 2)) * d_pad + (f1 & 3) * 4;
-  const int so0 = (f0 >> 2) * LDSK + (f0 & 3) * 4;
-  const int so1 = (f1 >> 2) * LDSK + (f1 & 3) * 4;
-
   floatx16 acc[2][2];
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
-
-  float4 ra0 = *(const float4*)Ag0, ra1 = *(const float4*)Ag1;
-  float4 rb0 = *(const float4*)Bg0, rb1 = *(const float4*)Bg1;
-  *(float4*)(lds + so0) = ra0;
-  *(float4*)(lds + so1) = ra1;
-  *(float4*)(lds + kTile * LDSK + so0) = rb0;
-  *(float4*)(lds + kTile * LDSK + so1) = rb1;
-  __syncthreads();
-
-  const int nk = d_pad / kBK;
-  for (int kc = 0; kc < nk; ++kc) {
-    const int cur = kc & 1;
-    if (kc + 1 < nk) {  // prefetch the next chunk into registers
-      const int ko = (kc + 1) * kBK;
-      ra0 = *(const float4*)(Ag0 + ko);
-      ra1 = *(const float4*)(Ag1 + ko);
-      rb0 = *(const float4*)(Bg0 + ko);
-      rb1 = *(const float4*)(Bg1 + ko);
-    }
-    const float* As = lds + cur * BUF;
-    const float* Bs = As + kTile * LDSK;
-    float a[2][8], bv[2][8];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const float* pa = As + (wm * 64 + q * 32 + l32) * LDSK + h * 8;
-      const float* pb = Bs + (wn * 64 + q * 32 + l32) * LDSK + h * 8;
-      float4 a0 = *(const float4*)pa, a1 = *(const float4*)(pa + 4);
-      float4 b0 = *(const float4*)pb, b1 = *(const float4*)(pb + 4);
-      a[q][0] = a0.x; a[q][1] = a0.y; a[q][2] = a0.z; a[q][3] = a0.w;
-      a[q][4] = a1.x; a[q][5] = a1.y; a[q][6] = a1.z; a[q][7] = a1.w;
-      bv[q][0] = b0.x; bv[q][1] = b0.y; bv[q][2] = b0.z; bv[q][3] = b0.w;
-      bv[q][4] = b1.x; bv[q][5] = b1.y; bv[q][6] = b1.z; bv[q][7] = b1.w;
-    }
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
-          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[bi][s], bv[bj][s], acc[bi][bj], 0, 0, 0);
-    if (kc + 1 < nk) {
-      float* nxt = lds + (cur ^ 1) * BUF;
-      *(float4*)(nxt + so0) = ra0;
-      *(float4*)(nxt + so1) = ra1;
-      *(float4*)(nxt + kTile * LDSK + so0) = rb0;
-      *(float4*)(nxt + kTile * LDSK + so1) = rb1;
-    }
-    __syncthreads();
-  }
+  mma_tile(Xp + row0 * d_pad, Xp + col0 * d_pad, d_pad, lds, acc);
 
   // ---- epilogue: acc[bi][bj][r] is B(i, j) with
   //      i = row0 + wm*64 + bi*32 + 8*(r/4) + 4*h + r%4,  j = col0 + wn*64 + bj*32 + l32
@@ -164,7 +82,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
           if (gi < n) diagK[gi] = v;
         }
         if (KIND == GAUSS) {
-          const bool f = (gi < gj) && (gj < n) && (kp.fix_scale * (ni + nj[bj]) * v > kp.fix_tol);
+          const bool f = (gi < gj) && (gj < n) && gauss_needs_fix(v, ni, nj[bj], kp);
           const unsigned long long m = __ballot(f);
           if (m) {
             const int leader = __ffsll((long long)m) - 1;
@@ -300,13 +218,8 @@ __global__ __launch_bounds__(256) void gauss_fixup_scan_kernel(const float* __re
   const float ni = nrm[i];
   for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
     const float v = K[i * ld + j];
-    if (kp.fix_scale * (ni + nrm[j]) * v > kp.fix_tol) {
-      float s = 0.f;
-      for (int c = 0; c < d_pad; ++c) {
-        const float dx = Xp[i * d_pad + c] - Xp[j * d_pad + c];
-        s = fmaf(dx, dx, s);
-      }
-      const float w = __builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
+    if (gauss_needs_fix(v, ni, nrm[j], kp)) {
+      const float w = gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
       K[i * ld + j] = w;
       K[j * ld + i] = w;
     }

@@ -64,11 +64,17 @@ size_t staged_bytes(const Sizes& s) {
 size_t k_bytes(const Sizes& s) { return (size_t)s.n * (size_t)s.ld * 4; }
 int64_t qmax_for(const Sizes& s, int k) { return (s.n + kChunk - 1) / kChunk + k; }
 
-size_t ws_bytes(const Sizes& s, int k) {
+size_t ws_bytes(const Sizes& s, int k, int mode) {
   const int64_t qmax = qmax_for(s, k);
   size_t b = 0;
   b += (size_t)k * s.ld * 4;              // Et
-  b += (size_t)qmax * s.ld * 4;           // P
+  if (mode == KKM_MODE_RESIDENT) {
+    b += (size_t)qmax * s.ld * 4;         // P: chunk partials
+  } else {
+    b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
+    b += (size_t)s.n_pad * 8;             // their norms and cluster ids
+    b += (size_t)onthefly_segments(s.n) * k * s.ld * 4;  // segment partials
+  }
   b += (size_t)k * s.nstripes * 8;        // zpart
   b += (size_t)2 * k * s.nblk * 4;        // hist, base
   b += (size_t)2 * (k + 1) * 4;           // off, qfirst
@@ -101,6 +107,9 @@ struct kkm_ctx {
 
   int k_ws = 0, iter_ws = 0;
   IterBufs ib{};
+  float *Xs = nullptr, *nrm_s = nullptr, *Epart = nullptr;  // on-the-fly scratch
+  int* cs = nullptr;
+  const int* epos = nullptr;  // column order of E^T after the last update (null: identity)
   int* counts[2] = {nullptr, nullptr};
   int* clbuf[2] = {nullptr, nullptr};
   std::vector<Alloc> ws_allocs;
@@ -206,6 +215,8 @@ void free_ws(kkm_ctx* c) {
   release(c, c->ws_allocs);
   c->k_ws = 0;
   c->ib = IterBufs{};
+  c->Xs = c->nrm_s = c->Epart = nullptr;
+  c->cs = nullptr;
 }
 
 void free_hist(kkm_ctx* c) {
@@ -231,7 +242,7 @@ void free_build(kkm_ctx* c) {
 int carve_ws(kkm_ctx* c, int k) {
   const Sizes& s = c->sz;
   void* base = nullptr;
-  int rc = dalloc(c, &base, ws_bytes(s, k), c->ws_allocs, "iteration scratch");
+  int rc = dalloc(c, &base, ws_bytes(s, k, c->mode), c->ws_allocs, "iteration scratch");
   if (rc) return rc;
   char* p = (char*)base;
   auto take = [&](size_t bytes) {
@@ -251,7 +262,14 @@ int carve_ws(kkm_ctx* c, int k) {
   b.diagK = c->diagK;
   b.trK = c->trK;
   b.Et = (float*)take((size_t)k * s.ld * 4);
-  b.P = (float*)take((size_t)qmax * s.ld * 4);
+  if (c->mode == KKM_MODE_RESIDENT) {
+    b.P = (float*)take((size_t)qmax * s.ld * 4);
+  } else {
+    c->Xs = (float*)take((size_t)s.n_pad * s.d_pad * 4);
+    c->nrm_s = (float*)take((size_t)s.n_pad * 4);
+    c->cs = (int*)take((size_t)s.n_pad * 4);
+    c->Epart = (float*)take((size_t)onthefly_segments(s.n) * k * s.ld * 4);
+  }
   b.zpart = (double*)take((size_t)k * s.nstripes * 8);
   b.hist = (int*)take((size_t)k * s.nblk * 4);
   b.base = (int*)take((size_t)k * s.nblk * 4);
@@ -299,8 +317,8 @@ int check_ids_on_device(kkm_ctx* c, const int32_t* V) {
   if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(b.status, 1, c->stream); })))
     return rc;
   if ((rc = run(c, KKM_PHASE_LABELS, "assign(labels)", [&] {
-         return launch_assign(0, b, nullptr, V, nullptr, c->counts[0], nullptr, nullptr, nullptr,
-                              nullptr, c->stream);
+         return launch_assign(0, b, nullptr, V, nullptr, nullptr, c->counts[0], nullptr, nullptr,
+                              nullptr, nullptr, c->stream);
        })))
     return rc;
   int status = 0;
@@ -320,16 +338,31 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
          return launch_scatter(b, cur, cin, cout, c->changed + t, c->stream);
        })))
     return rc;
+  const int* pos = nullptr;
   if (c->mode == KKM_MODE_RESIDENT) {
     if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
       return rc;
+    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
+      return rc;
   } else {
-    return fail(c, KKM_ERR_STATE, "on-the-fly mode is not available in this build");
+    const Sizes& s = c->sz;
+    if ((rc = run(c, KKM_PHASE_OTHER, "gather_sorted", [&] {
+           return launch_gather_sorted(c->Xp, c->nrm, b, cur, s.n_pad, s.d_pad, c->Xs, c->nrm_s, c->cs, c->stream);
+         })))
+      return rc;
+    if ((rc = run(c, KKM_PHASE_ONTHEFLY, "onthefly", [&] {
+           return launch_onthefly(c->Xs, c->nrm_s, c->cs, b, s.d_pad, c->kp, c->Epart, c->stream);
+         })))
+      return rc;
+    if ((rc = run(c, KKM_PHASE_REDUCE, "onthefly_reduce", [&] {
+           return launch_onthefly_reduce(b, c->Epart, c->cs, c->stream);
+         })))
+      return rc;
+    pos = b.pos;
   }
-  if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
-    return rc;
+  c->epos = pos;
   return run(c, KKM_PHASE_ASSIGN, "assign", [&] {
-    return launch_assign(1, b, cin, cur, nxt, cout, c->changed + t, c->obj + t, z_out, D_out, c->stream);
+    return launch_assign(1, b, cin, cur, pos, nxt, cout, c->changed + t, c->obj + t, z_out, D_out, c->stream);
   });
 }
 
@@ -382,9 +415,8 @@ int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t request
   if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_ONTHEFLY)
     return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
   const Sizes s = sizes_for(n, d);
-  const size_t base = staged_bytes(s) + ws_bytes(s, k) + 4096;
-  const size_t resident = base + k_bytes(s);
-  const size_t onthefly = base + staged_bytes(s);  // sorted copy of the points
+  const size_t resident = staged_bytes(s) + ws_bytes(s, k, KKM_MODE_RESIDENT) + 4096 + k_bytes(s);
+  const size_t onthefly = staged_bytes(s) + ws_bytes(s, k, KKM_MODE_ONTHEFLY) + 4096;
   int mode = requested_mode;
   if (mode == KKM_MODE_AUTO) mode = resident <= mem_budget ? KKM_MODE_RESIDENT : KKM_MODE_ONTHEFLY;
   const size_t need = mode == KKM_MODE_RESIDENT ? resident : onthefly;
@@ -440,8 +472,6 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
   if (kkm_plan(n, d, 1, budget_left, params->mode, &mode, &need) != KKM_OK)
     return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
-  if (mode == KKM_MODE_ONTHEFLY)
-    return fail(c, KKM_ERR_ARG, "on-the-fly mode is not available in this build");
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
   collect_timing(c);
   free_build(c);
@@ -479,7 +509,7 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     return rc;
 
   c->fixups = 0;
-  if (kind == KKM_GAUSS) {
+  if (kind == KKM_GAUSS && mode == KKM_MODE_RESIDENT) {
     const long long upper = (long long)(n * (n - 1) / 2);
     long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
     const size_t room = c->budget > c->held ? c->budget - c->held : 0;
@@ -493,6 +523,11 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   }
   c->built = true;  // buffers exist from here on; free_build releases them
 
+  if (mode == KKM_MODE_ONTHEFLY) {
+    if ((rc = run(c, KKM_PHASE_STAGE, "diag", [&] { return launch_diag_from_norms(c->nrm, n, kp, c->diagK, c->stream); })))
+      return rc;
+    return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
+  }
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
          return launch_gemm_kappa(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->K, c->diagK, c->fix_list,
                                   c->fix_count, c->fix_cap, c->stream);
@@ -567,7 +602,7 @@ int kkm_step(kkm_ctx* c, const int32_t* cl_in, int32_t k, float* E, float* z, fl
   if ((rc = check_ids_on_device(c, cl_in))) return rc;
   int* nxt = cl_out ? cl_out : c->clbuf[0];
   if ((rc = one_update(c, 0, cl_in, nxt, z, D))) return rc;
-  if (E && (rc = run(c, KKM_PHASE_OTHER, "et_to_e", [&] { return launch_et_to_e(c->ib, c->counts[0], E, c->stream); })))
+  if (E && (rc = run(c, KKM_PHASE_OTHER, "et_to_e", [&] { return launch_et_to_e(c->ib, c->counts[0], c->epos, E, c->stream); })))
     return rc;
   if (counts_out)
     HIP_TRY(c, hipMemcpyAsync(counts_out, c->counts[0], (size_t)k * 4, hipMemcpyDeviceToDevice, c->stream), "copy counts");
@@ -586,7 +621,14 @@ int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
   if (!out || r0 < 0 || r1 > c->sz.n || r0 > r1) return fail(c, KKM_ERR_ARG, "bad row range [%lld, %lld)", (long long)r0, (long long)r1);
   if (r1 == r0) return KKM_OK;
-  if (c->mode != KKM_MODE_RESIDENT) return fail(c, KKM_ERR_STATE, "on-the-fly mode is not available in this build");
+  if (c->mode == KKM_MODE_ONTHEFLY) {
+    int rc = run(c, KKM_PHASE_OTHER, "kernel_rows", [&] {
+      return launch_kernel_rows(c->Xp, c->nrm, c->sz.n, c->sz.d_pad, c->kp, r0, r1, out, c->stream);
+    });
+    if (rc) return rc;
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    return KKM_OK;
+  }
   const size_t row = (size_t)c->sz.n * 4;
   HIP_TRY(c, hipMemcpy2DAsync(out, row, c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, row, (size_t)(r1 - r0),
                               hipMemcpyDeviceToDevice, c->stream), "copy rows");

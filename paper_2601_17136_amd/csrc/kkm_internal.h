@@ -72,13 +72,28 @@ hipError_t launch_zero_ints(int* p, int64_t count, hipStream_t s);
 // mode 0: validate cl_in, count, per-block histogram (no distances).
 // mode 1: distances from Et/zpart/counts_in, argmin -> cl_out, new counts.
 // counts_out must be zero on entry (scatter clears the next update's).
+// pos (may be null): E^T is in sorted row order; point i reads column pos[i].
 hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
-                         int* cl_out, int* counts_out, int* changed, double* obj, float* z_out,
-                         float* D_out, hipStream_t s);
+                         const int* pos, int* cl_out, int* counts_out, int* changed, double* obj,
+                         float* z_out, float* D_out, hipStream_t s);
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s);
 hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
 hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
-hipError_t launch_et_to_e(const IterBufs& b, const int* counts, float* E, hipStream_t s);
+hipError_t launch_et_to_e(const IterBufs& b, const int* counts, const int* pos, float* E,
+                          hipStream_t s);
+
+// on-the-fly mode
+int onthefly_segments(int64_t n);
+hipError_t launch_gather_sorted(const float* Xp, const float* nrm, const IterBufs& b, const int* cl,
+                                int64_t n_pad, int d_pad, float* Xs, float* nrm_s, int* cs,
+                                hipStream_t s);
+hipError_t launch_diag_from_norms(const float* nrm, int64_t n, const KappaParams& kp, float* diagK,
+                                  hipStream_t s);
+hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs, const IterBufs& b,
+                           int d_pad, const KappaParams& kp, float* Epart, hipStream_t s);
+hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const int* cs, hipStream_t s);
+hipError_t launch_kernel_rows(const float* Xp, const float* nrm, int64_t n, int d_pad,
+                              const KappaParams& kp, int64_t r0, int64_t r1, float* out, hipStream_t s);
 
 }  // namespace kkm

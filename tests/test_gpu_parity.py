@@ -49,32 +49,42 @@ def _setup(name, oracle):
     return X, k, kind, g, c, p, cl, kern
 
 
+MODES = ["resident", "onthefly"]
+
+
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", list(CASES))
-def test_kernel_matrix(oracle, name):
+def test_kernel_matrix(oracle, name, mode):
+    """K (resident: the stored matrix; on the fly: rows from the same tile
+    kernel and epilogue the update sweep uses) against the oracle."""
     _torch_cuda()
-    print(f"[gpu] K parity {name}", flush=True)
+    print(f"[gpu] K parity {name} {mode}", flush=True)
     X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
-    with Engine(X, kind, g, c, p) as eng:
+    with Engine(X, kind, g, c, p, mode=mode) as eng:
         K = eng.K_rows()
         diag = eng.diag()
         info = eng.info()
+    assert info["mode"] == (1 if mode == "resident" else 2)
     Kref = kern.matrix(X)
     err = rowscaled_err(K, Kref)
     assert err <= TOL, f"K row-scaled error {err:.3e}"
-    assert np.array_equal(K, K.T), "K is not exactly symmetric"
-    np.testing.assert_array_equal(diag, np.diag(K))
+    if mode == "resident":
+        assert np.array_equal(K, K.T), "K is not exactly symmetric"
+        np.testing.assert_array_equal(diag, np.diag(K))
+    assert rel_err(diag, np.diag(Kref)) <= TOL
     if kind == "gauss":
-        assert np.all(diag == 1.0)
-    print(f"[gpu] {name}: K err {err:.2e}, fixups {info['fixups']}", flush=True)
+        assert np.all(diag == 1.0) and np.all(np.diag(K) == 1.0)
+    print(f"[gpu] {name} {mode}: K err {err:.2e}, fixups {info['fixups']}", flush=True)
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", list(CASES))
-def test_step(oracle, name):
+def test_step(oracle, name, mode):
     _torch_cuda()
-    print(f"[gpu] step parity {name}", flush=True)
+    print(f"[gpu] step parity {name} {mode}", flush=True)
     X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
     ref = oracle.step_full(kern.matrix(X), cl, k)
-    with Engine(X, kind, g, c, p) as eng:
+    with Engine(X, kind, g, c, p, mode=mode) as eng:
         out = eng.step(cl, k)
     np.testing.assert_array_equal(out["counts"], ref["counts"])
     eE, eD = rowscaled_err(out["E"], ref["E"]), rowscaled_err(out["D"], ref["D"])
@@ -107,8 +117,9 @@ WELL_SEPARATED = [  # (kernel, gamma, coef0, degree, scrambled fraction of the i
 ]
 
 
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("case", WELL_SEPARATED, ids=lambda c: f"{c[0]}-{c[1]:g}-{c[4]}-{c[5]}")
-def test_well_separated_trajectory_is_exact(oracle, case):
+def test_well_separated_trajectory_is_exact(oracle, case, mode):
     """On input the oracle certifies as well separated (every point's best and
     second-best distance differ by more than 1e-3 of its row at every update)
     the whole trajectory matches bit for bit, including where it stops."""
@@ -123,7 +134,7 @@ def test_well_separated_trajectory_is_exact(oracle, case):
     m = _margins(oracle, K, cl0, 8, 30)
     assert min(m) > 1e-3, f"input not well separated (margins {m})"
     cl_ref, done_ref, hist_ref, traj = oracle.iterate_full(K, cl0, 8, 30, tol=0.0)
-    with Engine(X, kind, g, c, p) as eng:
+    with Engine(X, kind, g, c, p, mode=mode) as eng:
         cl = cl0
         for t in range(done_ref):
             nxt, it, _ = eng.iterate(cl, 8, 1)
@@ -180,34 +191,37 @@ def test_stop_rules_match_oracle(oracle):
     assert dones == [3, 2, 30]
 
 
-def test_empty_cluster_and_ties(oracle):
+@pytest.mark.parametrize("mode", MODES)
+def test_empty_cluster_and_ties(oracle, mode):
     _torch_cuda()
     X = np.array([[-1.0], [1.0], [0.0], [0.0], [3.0]], np.float32)
     cl = np.array([0, 1, 0, 1, 1], np.int32)    # cluster 2 empty
     kern = oracle.Kernel("linear")
     ref = oracle.step_full(kern.matrix(X), cl, 3)
-    with Engine(X, "linear") as eng:
+    with Engine(X, "linear", mode=mode) as eng:
         out = eng.step(cl, 3)
     assert out["counts"][2] == 0 and np.all(np.isinf(out["D"][:, 2])) and out["z"][2] == 0
     np.testing.assert_array_equal(out["cl"], ref["cl"])
     assert rowscaled_err(out["D"], ref["D"]) <= TOL
 
 
-def test_each_point_its_own_cluster(oracle):
+@pytest.mark.parametrize("mode", MODES)
+def test_each_point_its_own_cluster(oracle, mode):
     _torch_cuda()
     X = datagen.make_points(2, n=70, d=9)[0]
-    with Engine(X, "gauss", 0.2) as eng:
+    with Engine(X, "gauss", 0.2, mode=mode) as eng:
         out = eng.step(np.arange(70, dtype=np.int32), 70)
     assert abs(out["J"]) <= 1e-4 * 70
     np.testing.assert_array_equal(out["cl"], np.arange(70))
     assert np.all(np.abs(np.diag(out["D"])) <= 1e-5)
 
 
-def test_invalid_ids_are_reported(oracle):
+@pytest.mark.parametrize("mode", MODES)
+def test_invalid_ids_are_reported(oracle, mode):
     _torch_cuda()
     from paper_2601_17136_amd import kkm
     X = datagen.make_points(1, n=300)[0]
-    with Engine(X, "poly", 1.0, 1.0, 2) as eng:
+    with Engine(X, "poly", 1.0, 1.0, 2, mode=mode) as eng:
         for bad in (8, -1):
             cl = datagen.random_init(300, 8, 3)
             cl[123] = bad
@@ -218,13 +232,14 @@ def test_invalid_ids_are_reported(oracle):
         assert it == 2
 
 
-def test_bitwise_reproducible(oracle):
+@pytest.mark.parametrize("mode", MODES)
+def test_bitwise_reproducible(oracle, mode):
     _torch_cuda()
     X = datagen.make_points(4, n=2500)[0]
     cl = datagen.random_init(2500, 64, 40)
     runs = []
     for _ in range(2):
-        with Engine(X, "gauss", 0.5) as eng:
+        with Engine(X, "gauss", 0.5, mode=mode) as eng:
             runs.append((eng.K_rows(0, 64), eng.step(cl, 64), eng.iterate(cl, 64, 5)))
     (K1, s1, i1), (K2, s2, i2) = runs
     assert np.array_equal(K1, K2)

@@ -25,17 +25,19 @@ def _rows(n, seed):
     return np.unique(np.concatenate([fixed, extra]).astype(np.int64))
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
-def test_workload_step_full_size(oracle, cfg):
+@pytest.mark.parametrize("cfg,mode", [(2, "resident"), (3, "resident"), (4, "resident"),
+                                      (5, "resident"), (5, "onthefly"), (2, "onthefly")])
+def test_workload_step_full_size(oracle, cfg, mode):
     torch = pytest.importorskip("torch")
     assert torch.cuda.is_available()
     w, X, cl = datagen.workload(cfg)
     n, k = w.n, w.k
-    print(f"[gpu] full-size step parity: {w.describe()}", flush=True)
+    print(f"[gpu] full-size step parity: {w.describe()} K {mode}", flush=True)
     kern = oracle.Kernel(w.kind, w.gamma, w.coef0, w.degree)
     rows = _rows(n, cfg)
-    with Engine(X, w.kind, w.gamma, w.coef0, w.degree) as eng:
+    with Engine(X, w.kind, w.gamma, w.coef0, w.degree, mode=mode) as eng:
         info = eng.info()
+        assert info["mode"] == (1 if mode == "resident" else 2)
         K_rows = np.stack([eng.K_rows(int(r), int(r) + 1)[0] for r in rows])
         diag = eng.diag()
         out = eng.step(cl, k)
@@ -61,13 +63,13 @@ def test_workload_step_full_size(oracle, cfg):
           flush=True)
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
-def test_workload_loop_properties(oracle, cfg):
+@pytest.mark.parametrize("cfg,mode", [(2, "resident"), (4, "resident"), (2, "onthefly")])
+def test_workload_loop_properties(oracle, cfg, mode):
     torch = pytest.importorskip("torch")
     assert torch.cuda.is_available()
     w, X, cl0 = datagen.workload(cfg)
-    print(f"[gpu] full-size loop: {w.describe()}", flush=True)
-    with Engine(X, w.kind, w.gamma, w.coef0, w.degree) as eng:
+    print(f"[gpu] full-size loop: {w.describe()} K {mode}", flush=True)
+    with Engine(X, w.kind, w.gamma, w.coef0, w.degree, mode=mode) as eng:
         final, it, hist = eng.iterate(cl0, w.k, w.iters)
         cl = cl0
         for t in range(3):
