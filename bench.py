@@ -24,6 +24,31 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 FP32_MFMA_PEAK_TF = 157.3    # MI355X dense fp32 matrix peak
 METRIC = "clustering iters/sec + K-build TFLOP/s, % of HBM / MFMA peak, 1 GPU"
 
+# HBM bytes per launch from two rocprofv3 counter runs (FETCH_SIZE, then
+# WRITE_SIZE; KiB per dispatch) on a workload, scaled by what the same
+# counters read for a plain 1 GiB device copy (fetch x1.9999, write x1.0).
+# Reported only while the kernel's sources still hash to what was counted.
+FETCH_SCALE, WRITE_SCALE = 1.9999, 1.0
+TRAFFIC = {
+    ("spmm_onehot", 2, "resident"): (("csrc/cluster_ops.hip",), ("df8f43467328b7b0",), 782837.9, 6273.0),
+    ("gemm_kappa", 2, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
+                                    ("f59fe3003cb073f2", "f259045186003e25"), 2495429.9, 1565104.9),
+}
+
+
+def counted_traffic(kernel, cfg, mode):
+    """Scaled HBM bytes per launch (GB) if the counters match the current sources, else None."""
+    import hashlib
+    entry = TRAFFIC.get((kernel, cfg, mode))
+    if entry is None:
+        return None
+    srcs, hashes, fetch_kib, write_kib = entry
+    for src, h in zip(srcs, hashes):
+        path = os.path.join(ROOT, "paper_2601_17136_amd", src)
+        if hashlib.sha256(open(path, "rb").read()).hexdigest()[:16] != h:
+            return None
+    return round((fetch_kib * FETCH_SCALE + write_kib * WRITE_SCALE) * 1024 / 1e9, 4)
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -36,6 +61,9 @@ def parse():
                     help="oracle sample sized for about this much host time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="first run one plain device-to-device copy of MIB MiB (a known-size "
+                         "reference for memory-traffic counters)")
     return ap.parse_args()
 
 
@@ -104,6 +132,15 @@ def main():
 
     torch.cuda.set_device(0)
     torch.cuda.empty_cache()
+    if args.copy_calibration > 0:
+        src = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"bench: calibration copy of {args.copy_calibration} MiB done", file=sys.stderr, flush=True)
+        del src, dst
+        torch.cuda.empty_cache()
     Xd = torch.from_numpy(X).cuda()
     V0 = torch.from_numpy(cl0).cuda()
     Vs = [V0.clone() for _ in range(args.steps + args.warmup)]
@@ -160,12 +197,15 @@ def main():
             gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
             out["roofline"] = {"kernel": "spmm_onehot", "bound": "hbm", "achieved": round(gbs, 1),
                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                               "traffic": None, "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt}
+                               "traffic": counted_traffic("spmm_onehot", args.config, args.mode),
+                               "traffic_unit": "GB per launch (algorithmic %.4f)" % (bytes_per / 1e9),
+                               "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt}
         tf = out["kbuild_tflops"]
         out["roofline_kbuild"] = {"kernel": "gemm_kappa", "bound": "mfma", "achieved": tf,
                                   "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
                                   "frac": round(tf / FP32_MFMA_PEAK_TF, 4) if tf else None,
-                                  "traffic": None, "avg_launch_ms": round(gemm_ms, 5),
+                                  "traffic": counted_traffic("gemm_kappa", args.config, args.mode),
+                                  "traffic_unit": "GB per launch", "avg_launch_ms": round(gemm_ms, 5),
                                   "gauss_fixups": info["fixups"]}
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
