@@ -24,8 +24,9 @@
  *    data_ptr()); they stay owned by the caller.  Host pointers are marked.
  *  - Points X are n x d, fp32, row-major, contiguous (row i at X + i*d).
  *  - Cluster ids are int32 in [0, k).  An id outside that range is detected
- *    on the device and reported as KKM_ERR_DEVICE_DATA; kernels clamp ids so
- *    that no access goes out of bounds before the report.
+ *    on the device and reported as KKM_ERR_DEVICE_DATA when the call
+ *    synchronises; kernels clamp ids so that no access goes out of bounds.
+ *    After that error the contents of every output are unspecified.
  *  - All work runs on the stream given to kkm_create.  kkm_build_kernel is
  *    asynchronous; kkm_iterate, kkm_objective, kkm_step, kkm_copy_* return
  *    after their work has completed.
@@ -102,7 +103,9 @@ typedef struct kkm_info {
   int64_t ld;             /* row stride of K in floats (resident mode) */
   size_t bytes_K;         /* device bytes held by K (0 on the fly) */
   size_t bytes_total;     /* device bytes held by the context */
-  int64_t fixups;         /* Gaussian entries recomputed from differences at build */
+  int64_t fixups;         /* Gaussian entries flagged for recomputation at build */
+  int64_t fixup_capacity; /* entries the fix-up list holds; beyond it the whole
+                             triangle is re-tested instead */
 } kkm_info;
 
 /* Create a context on the current HIP device.
@@ -143,7 +146,8 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are
  *   recomputed from the coordinate differences.
  * ONTHEFLY: stages X and row norms only.
- * Replaces any earlier build on ctx.  Asynchronous.
+ * Replaces any earlier build on ctx; a build of the same n, d, kind and mode
+ * reuses the device buffers of the previous one.  Asynchronous.
  * Errors: KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP. */
 int kkm_build_kernel(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t kind,
                      const kkm_params *params);
@@ -188,10 +192,14 @@ int kkm_copy_kernel_rows(kkm_ctx *ctx, int64_t r0, int64_t r1, float *out);
 /* diag K into out (device, n fp32). */
 int kkm_copy_diag(kkm_ctx *ctx, float *out);
 
-/* Timing: enable (1) or disable (0) per-kernel HIP-event timing; enabling
- * also clears the accumulated figures.  kkm_get_timing synchronises the
- * stream and returns the sums so far. */
-int kkm_set_timing(kkm_ctx *ctx, int32_t enable);
+/* Timing: phase_mask selects the phases whose kernel launches are bracketed
+ * by HIP events on the context's stream (bit 1 << KKM_PHASE_x; KKM_TIME_ALL
+ * for every phase; 0 disables timing).  Each bracket costs a few
+ * microseconds of stream time, so time only the kernels of interest in a
+ * measured run.  Setting a mask also clears the accumulated figures.
+ * kkm_get_timing synchronises the stream and returns the sums so far. */
+#define KKM_TIME_ALL ((1 << KKM_NPHASE) - 1)
+int kkm_set_timing(kkm_ctx *ctx, int32_t phase_mask);
 int kkm_get_timing(kkm_ctx *ctx, kkm_timing *out);
 
 int kkm_get_info(kkm_ctx *ctx, kkm_info *out);

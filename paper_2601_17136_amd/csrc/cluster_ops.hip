@@ -238,7 +238,7 @@ hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, i
 // ----------------------------------------------------------------- SpMM
 //
 // Workgroup (stripe, q): columns [stripe*1024, +1024) of the rows listed in
-// chunk q (one cluster j, at most 256 rows in sorted order).  Each lane keeps
+// chunk q (one cluster j, at most kChunk rows in sorted order).  Each lane keeps
 // one float4 accumulator; rows are summed in sorted order with non-temporal
 // 16-byte loads (K has no reuse within an update) and the chunk's sum goes
 // to P[q].  A second kernel adds the chunks of each cluster in chunk order;

@@ -37,10 +37,14 @@ __device__ inline void triangle_tile(int64_t t, int64_t nt, int64_t& I, int64_t&
 
 template <int KIND>
 __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
-    const float* __restrict__ Xp, const float* __restrict__ nrm, int64_t n, int d_pad, int64_t ld,
-    int64_t nt, int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
-    int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long fix_cap) {
+    const float* __restrict__ Xp, const float* __restrict__ nrm,
+    const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, int64_t nt,
+    int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
+    int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long seg_cap) {
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
+  // No Gaussian entry can need the fix-up unless the largest norms allow it.
+  const bool may_fix = KIND == GAUSS && gauss_needs_fix(1.f, __uint_as_float(*maxnrm_bits),
+                                                         __uint_as_float(*maxnrm_bits), kp);
 
   // Workgroup b runs on XCD b % 8.  Give each XCD a contiguous run of tiles
   // so that concurrent workgroups of one XCD share row block I in its L2.
@@ -81,17 +85,19 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
           if (KIND == GAUSS) v = 1.f;  // exp(0): exact, whatever B(i,i) rounded to
           if (gi < n) diagK[gi] = v;
         }
-        if (KIND == GAUSS) {
+        if (KIND == GAUSS && may_fix) {
           const bool f = (gi < gj) && (gj < n) && gauss_needs_fix(v, ni, nj[bj], kp);
           const unsigned long long m = __ballot(f);
           if (m) {
+            const int seg = (int)(blockIdx.x % kFixSegs);
             const int leader = __ffsll((long long)m) - 1;
             unsigned long long base = 0;
-            if (lane == leader) base = atomicAdd(fix_count, (unsigned long long)__popcll(m));
+            if (lane == leader) base = atomicAdd(fix_count + seg, (unsigned long long)__popcll(m));
             base = __shfl(base, leader, 64);
             if (f) {
               const unsigned long long idx = base + __popcll(m & ((1ull << lane) - 1ull));
-              if (idx < (unsigned long long)fix_cap) fix_list[idx] = make_int2((int)gi, (int)gj);
+              if (idx < (unsigned long long)seg_cap)
+                fix_list[(int64_t)seg * seg_cap + (int64_t)idx] = make_int2((int)gi, (int)gj);
             }
           }
         }
@@ -100,7 +106,8 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
     }
   }
 
-  // ---- stores, staged through LDS so each instruction writes 256 contiguous bytes
+  // ---- stores, staged through LDS so each instruction writes 256 contiguous
+  //      bytes; non-temporal, since K is not read again by this kernel
   float* Tw = lds + wave * (32 * 65);
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {  // tile (I, J): rows i, columns j
@@ -113,7 +120,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
     const int64_t gj = col0 + wn * 64 + lane;
     for (int rr = 0; rr < 32; ++rr) {
       const int64_t gi = row0 + wm * 64 + bi * 32 + rr;
-      if (gi < n && gj < ld) K[gi * ld + gj] = (gj < n) ? Tw[rr * 65 + lane] : 0.f;
+      if (gi < n && gj < ld) __builtin_nontemporal_store((gj < n) ? Tw[rr * 65 + lane] : 0.f, K + gi * ld + gj);
     }
     __syncthreads();
   }
@@ -129,53 +136,70 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
       const int64_t gj = row0 + wm * 64 + lane;  // I < J, so gj < n
       for (int rr = 0; rr < 32; ++rr) {
         const int64_t gi = col0 + wn * 64 + bj * 32 + rr;
-        if (gi < n) K[gi * ld + gj] = Tw[rr * 65 + lane];
+        if (gi < n) __builtin_nontemporal_store(Tw[rr * 65 + lane], K + gi * ld + gj);
       }
       __syncthreads();
     }
   }
 }
 
-hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                             const KappaParams& kp, float* K, float* diagK, int2* fix_list,
-                             unsigned long long* fix_count, long long fix_cap, hipStream_t s) {
+hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
+                             int64_t n, int d_pad, int64_t ld, const KappaParams& kp, float* K,
+                             float* diagK, int2* fix_list, unsigned long long* fix_count,
+                             long long seg_cap, hipStream_t s) {
   const int64_t nt = (n + kTile - 1) / kTile;
   const int64_t T = nt * (nt + 1) / 2;
   dim3 grid((unsigned)T), block(256);
   switch (kp.kind) {
     case LINEAR:
-      hipLaunchKernelGGL(gemm_kappa_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, n, d_pad, ld, nt, T,
-                         kp, K, diagK, fix_list, fix_count, fix_cap);
+      hipLaunchKernelGGL(gemm_kappa_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
+                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
     case POLY:
-      hipLaunchKernelGGL(gemm_kappa_kernel<POLY>, grid, block, 0, s, Xp, nrm, n, d_pad, ld, nt, T,
-                         kp, K, diagK, fix_list, fix_count, fix_cap);
+      hipLaunchKernelGGL(gemm_kappa_kernel<POLY>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
+                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
     default:
-      hipLaunchKernelGGL(gemm_kappa_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, n, d_pad, ld, nt, T,
-                         kp, K, diagK, fix_list, fix_count, fix_cap);
+      hipLaunchKernelGGL(gemm_kappa_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
+                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
   }
   return hipGetLastError();
 }
 
 // ---- Gaussian fix-up: |x_i - x_j|^2 summed from the coordinate differences.
-
+//
+// Phase 1: workgroups b, b + kFixSegs, ... share list segment b % kFixSegs;
 // 16 lanes per listed pair, float4 steps along k, fixed shuffle tree.
-__global__ __launch_bounds__(256) void gauss_fixup_list_kernel(const float* __restrict__ Xp,
-                                                               int d_pad, int64_t ld, float neg_g_log2e,
-                                                               const int2* __restrict__ list,
-                                                               long long count,
-                                                               float* __restrict__ K) {
+// Phase 2 (only when some segment received more entries than it holds):
+// every entry of the upper triangle is re-tested from the stored K with the
+// epilogue's estimate.  The counts are read on the device, so the build needs
+// no host round trip.
+__global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp,
+                                                          const float* __restrict__ nrm, int64_t n,
+                                                          int d_pad, int64_t ld, KappaParams kp,
+                                                          const int2* __restrict__ list,
+                                                          const unsigned long long* __restrict__ counts,
+                                                          long long seg_cap, float* __restrict__ K) {
+  __shared__ int overflow;
+  if (threadIdx.x == 0) overflow = 0;
+  __syncthreads();
+  for (int q = threadIdx.x; q < kFixSegs; q += 256)
+    if (counts[q] > (unsigned long long)seg_cap) overflow = 1;
+  const int seg = (int)(blockIdx.x % kFixSegs), part = (int)(blockIdx.x / kFixSegs);
+  const int parts = (int)(gridDim.x / kFixSegs);
+  const unsigned long long c = counts[seg];
+  const long long count = c < (unsigned long long)seg_cap ? (long long)c : seg_cap;
+  const int2* seg_list = list + (int64_t)seg * seg_cap;
   const int g = threadIdx.x >> 4, gl = threadIdx.x & 15;
   const int nq = d_pad >> 2;
-  for (long long p = (long long)blockIdx.x * 16 + g; p < count; p += (long long)gridDim.x * 16) {
-    const int2 ij = list[p];
+  for (long long p = (long long)part * 16 + g; p < count; p += (long long)parts * 16) {
+    const int2 ij = seg_list[p];
     const float4* xi = (const float4*)(Xp + (int64_t)ij.x * d_pad);
     const float4* xj = (const float4*)(Xp + (int64_t)ij.y * d_pad);
     float s = 0.f;
-    for (int c = gl; c < nq; c += 16) {
-      const float4 a = xi[c], b = xj[c];
+    for (int cc = gl; cc < nq; cc += 16) {
+      const float4 a = xi[cc], b = xj[cc];
       float dx = a.x - b.x;
       s = fmaf(dx, dx, s);
       dx = a.y - b.y;
@@ -190,46 +214,32 @@ __global__ __launch_bounds__(256) void gauss_fixup_list_kernel(const float* __re
     s += __shfl_xor(s, 2, 16);
     s += __shfl_xor(s, 1, 16);
     if (gl == 0) {
-      const float v = __builtin_amdgcn_exp2f(neg_g_log2e * s);
+      const float v = __builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
       K[(int64_t)ij.x * ld + ij.y] = v;
       K[(int64_t)ij.y * ld + ij.x] = v;
     }
   }
-}
-
-hipError_t launch_gauss_fixup_list(const float* Xp, int d_pad, int64_t ld, const KappaParams& kp,
-                                   const int2* fix_list, long long count, float* K, hipStream_t s) {
-  if (count <= 0) return hipSuccess;
-  long long blocks = (count + 15) / 16;
-  if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(gauss_fixup_list_kernel, dim3((unsigned)blocks), dim3(256), 0, s, Xp, d_pad,
-                     ld, kp.neg_g_log2e, fix_list, count, K);
-  return hipGetLastError();
-}
-
-// Overflow path: when more entries qualify than the list holds, re-test every
-// entry of the upper triangle from the stored K with the epilogue's estimate.
-__global__ __launch_bounds__(256) void gauss_fixup_scan_kernel(const float* __restrict__ Xp,
-                                                               const float* __restrict__ nrm,
-                                                               int64_t n, int d_pad, int64_t ld,
-                                                               KappaParams kp,
-                                                               float* __restrict__ K) {
-  const int64_t i = blockIdx.x;
-  const float ni = nrm[i];
-  for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
-    const float v = K[i * ld + j];
-    if (gauss_needs_fix(v, ni, nrm[j], kp)) {
-      const float w = gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
-      K[i * ld + j] = w;
-      K[j * ld + i] = w;
+  __syncthreads();
+  if (!overflow) return;
+  for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+    const float ni = nrm[i];
+    for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
+      const float v = K[i * ld + j];
+      if (gauss_needs_fix(v, ni, nrm[j], kp)) {
+        const float w = gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
+        K[i * ld + j] = w;
+        K[j * ld + i] = w;
+      }
     }
   }
 }
 
-hipError_t launch_gauss_fixup_scan(const float* Xp, const float* nrm, int64_t n, int d_pad,
-                                   int64_t ld, const KappaParams& kp, float* K, hipStream_t s) {
-  hipLaunchKernelGGL(gauss_fixup_scan_kernel, dim3((unsigned)n), dim3(256), 0, s, Xp, nrm, n,
-                     d_pad, ld, kp, K);
+hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
+                              const KappaParams& kp, const int2* fix_list,
+                              const unsigned long long* fix_count, long long seg_cap, float* K,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(gauss_fixup_kernel, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
+                     ld, kp, fix_list, fix_count, seg_cap, K);
   return hipGetLastError();
 }
 

@@ -99,9 +99,10 @@ struct kkm_ctx {
   KappaParams kp{};
   float *Xp = nullptr, *nrm = nullptr, *diagK = nullptr, *K = nullptr;
   double* trK = nullptr;
+  unsigned* maxnrm = nullptr;  // bits of the largest squared norm (next to tr K)
   int2* fix_list = nullptr;
-  unsigned long long* fix_count = nullptr;
-  long long fix_cap = 0;
+  unsigned long long* fix_count = nullptr;  // kFixSegs counters
+  long long fix_cap = 0;                    // entries in all segments together
   int64_t fixups = 0;
   std::vector<Alloc> build_allocs;
 
@@ -117,7 +118,7 @@ struct kkm_ctx {
   double* obj = nullptr;
   std::vector<Alloc> hist_allocs;
 
-  bool timing = false;
+  int32_t timing = 0;  // mask of timed phases
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> pool;
   kkm_timing tacc{};
@@ -184,13 +185,14 @@ hipEvent_t take_event(kkm_ctx* c) {
 template <class F>
 int run(kkm_ctx* c, int phase, const char* what, F&& f) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (c->timing) {
+  const bool timed = (c->timing >> phase) & 1;
+  if (timed) {
     a = take_event(c);
     b = take_event(c);
     if (a) (void)hipEventRecord(a, c->stream);
   }
   hipError_t e = f();
-  if (c->timing && a && b) {
+  if (timed && a && b) {
     (void)hipEventRecord(b, c->stream);
     c->pending.push_back({phase, a, b});
   }
@@ -309,22 +311,23 @@ int ensure_ws(kkm_ctx* c, int k, int iters) {
   return KKM_OK;
 }
 
-int check_ids_on_device(kkm_ctx* c, const int32_t* V) {
+// Validate ids, count cluster sizes and per-block histograms (asynchronous;
+// the status word is read at the caller's final synchronisation).
+int label_pass(kkm_ctx* c, const int32_t* V) {
   IterBufs& b = c->ib;
   int rc;
   if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(c->counts[0], b.k, c->stream); })))
     return rc;
   if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(b.status, 1, c->stream); })))
     return rc;
-  if ((rc = run(c, KKM_PHASE_LABELS, "assign(labels)", [&] {
-         return launch_assign(0, b, nullptr, V, nullptr, nullptr, c->counts[0], nullptr, nullptr,
-                              nullptr, nullptr, c->stream);
-       })))
-    return rc;
-  int status = 0;
-  HIP_TRY(c, hipMemcpyAsync(&status, b.status, sizeof(int), hipMemcpyDeviceToHost, c->stream), "read status");
-  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
-  if (status & 1) return fail(c, KKM_ERR_DEVICE_DATA, "a cluster id is outside [0, %d)", b.k);
+  return run(c, KKM_PHASE_LABELS, "assign(labels)", [&] {
+    return launch_assign(0, b, nullptr, V, nullptr, nullptr, c->counts[0], nullptr, nullptr,
+                         nullptr, nullptr, c->stream);
+  });
+}
+
+int status_error(kkm_ctx* c, int status) {
+  if (status & 1) return fail(c, KKM_ERR_DEVICE_DATA, "a cluster id is outside [0, %d)", c->ib.k);
   return KKM_OK;
 }
 
@@ -351,7 +354,7 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
          })))
       return rc;
     if ((rc = run(c, KKM_PHASE_ONTHEFLY, "onthefly", [&] {
-           return launch_onthefly(c->Xs, c->nrm_s, c->cs, b, s.d_pad, c->kp, c->Epart, c->stream);
+           return launch_onthefly(c->Xs, c->nrm_s, c->cs, c->maxnrm, b, s.d_pad, c->kp, c->Epart, c->stream);
          })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "onthefly_reduce", [&] {
@@ -474,7 +477,10 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
   collect_timing(c);
-  free_build(c);
+  // A rebuild of the same shape keeps every buffer (K alone can be 160 GB,
+  // and allocating it costs far more than building it).
+  const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind;
+  if (!reuse) free_build(c);
 
   c->sz = sizes_for(n, d);
   c->d = d;
@@ -493,34 +499,42 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   const Sizes& s = c->sz;
   int rc;
   void* p = nullptr;
-  if ((rc = dalloc(c, &p, staged_bytes(s), c->build_allocs, "staged points"))) return rc;
-  c->Xp = (float*)p;
-  c->nrm = c->Xp + (size_t)s.n_pad * s.d_pad;
-  c->diagK = c->nrm + s.n_pad;
-  if ((rc = dalloc(c, &p, 64, c->build_allocs, "trace"))) return rc;
-  c->trK = (double*)p;
-  if (mode == KKM_MODE_RESIDENT) {
-    if ((rc = dalloc(c, &p, k_bytes(s), c->build_allocs, "kernel matrix K"))) return rc;
-    c->K = (float*)p;
+  if (!reuse) {
+    if ((rc = dalloc(c, &p, staged_bytes(s), c->build_allocs, "staged points"))) return rc;
+    c->Xp = (float*)p;
+    c->nrm = c->Xp + (size_t)s.n_pad * s.d_pad;
+    c->diagK = c->nrm + s.n_pad;
+    if ((rc = dalloc(c, &p, 64, c->build_allocs, "trace"))) return rc;
+    c->trK = (double*)p;
+    c->maxnrm = (unsigned*)((char*)p + 8);
+    if (mode == KKM_MODE_RESIDENT) {
+      if ((rc = dalloc(c, &p, k_bytes(s), c->build_allocs, "kernel matrix K"))) return rc;
+      c->K = (float*)p;
+    }
+    if (kind == KKM_GAUSS && mode == KKM_MODE_RESIDENT) {
+      const long long upper = (long long)(n * (n - 1) / 2);
+      long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
+      const size_t room = c->budget > c->held ? c->budget - c->held : 0;
+      cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
+      cap = std::max<long long>(cap / kFixSegs, 1) * kFixSegs;
+      if ((rc = dalloc(c, &p, (size_t)cap * sizeof(int2) + kFixSegs * 8, c->build_allocs, "fix-up list")))
+        return rc;
+      c->fix_list = (int2*)p;
+      c->fix_count = (unsigned long long*)((char*)p + (size_t)cap * sizeof(int2));
+      c->fix_cap = cap;
+    }
   }
+  if ((rc = run(c, KKM_PHASE_STAGE, "zero", [&] { return launch_zero_ints((int*)c->maxnrm, 1, c->stream); })))
+    return rc;
   if ((rc = run(c, KKM_PHASE_STAGE, "stage", [&] {
-         return launch_stage(X, n, d, s.d_pad, s.n_pad, c->Xp, c->nrm, c->stream);
+         return launch_stage(X, n, d, s.d_pad, s.n_pad, c->Xp, c->nrm, c->maxnrm, c->stream);
        })))
     return rc;
-
-  c->fixups = 0;
-  if (kind == KKM_GAUSS && mode == KKM_MODE_RESIDENT) {
-    const long long upper = (long long)(n * (n - 1) / 2);
-    long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
-    const size_t room = c->budget > c->held ? c->budget - c->held : 0;
-    cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
-    cap = std::max<long long>(cap, 1);
-    if ((rc = dalloc(c, &p, (size_t)cap * sizeof(int2) + 256, c->build_allocs, "fix-up list"))) return rc;
-    c->fix_list = (int2*)p;
-    c->fix_count = (unsigned long long*)((char*)p + (size_t)cap * sizeof(int2));
-    c->fix_cap = cap;
-    HIP_TRY(c, hipMemsetAsync(c->fix_count, 0, sizeof(unsigned long long), c->stream), "clear fix-up count");
-  }
+  c->fixups = -1;  // read from the device on demand
+  if (c->fix_count && (rc = run(c, KKM_PHASE_FIXUP, "zero", [&] {
+        return launch_zero_ints((int*)c->fix_count, 2 * kFixSegs, c->stream);
+      })))
+    return rc;
   c->built = true;  // buffers exist from here on; free_build releases them
 
   if (mode == KKM_MODE_ONTHEFLY) {
@@ -529,27 +543,16 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
   }
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
-         return launch_gemm_kappa(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->K, c->diagK, c->fix_list,
-                                  c->fix_count, c->fix_cap, c->stream);
+         return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, kp, c->K, c->diagK,
+                                  c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->stream);
        })))
     return rc;
-  if (kind == KKM_GAUSS) {
-    unsigned long long cnt = 0;
-    HIP_TRY(c, hipMemcpyAsync(&cnt, c->fix_count, sizeof cnt, hipMemcpyDeviceToHost, c->stream), "read fix-up count");
-    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
-    c->fixups = (int64_t)cnt;
-    const long long listed = std::min<long long>((long long)cnt, c->fix_cap);
-    if ((rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
-           return launch_gauss_fixup_list(c->Xp, s.d_pad, s.ld, kp, c->fix_list, listed, c->K, c->stream);
-         })))
-      return rc;
-    if ((long long)cnt > c->fix_cap) {
-      if ((rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup_scan", [&] {
-             return launch_gauss_fixup_scan(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->K, c->stream);
-           })))
-        return rc;
-    }
-  }
+  if (kind == KKM_GAUSS &&
+      (rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
+         return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->fix_list, c->fix_count,
+                                   c->fix_cap / kFixSegs, c->K, c->stream);
+       })))
+    return rc;
   return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
 }
 
@@ -560,9 +563,9 @@ int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol,
   if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
   if (iters_done) *iters_done = 0;
   if ((rc = ensure_ws(c, k, max_iter))) return rc;
-  if ((rc = check_ids_on_device(c, V))) return rc;
+  if ((rc = label_pass(c, V))) return rc;
   const int* cur = V;
-  int t = 0;
+  int t = 0, status = 0;
   double Jprev = 0.0;
   for (; t < max_iter; ++t) {
     int* nxt = c->clbuf[t & 1];
@@ -573,7 +576,9 @@ int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol,
       double J = 0.0;
       HIP_TRY(c, hipMemcpyAsync(&chg, c->changed + t, sizeof chg, hipMemcpyDeviceToHost, c->stream), "read changes");
       HIP_TRY(c, hipMemcpyAsync(&J, c->obj + t, sizeof J, hipMemcpyDeviceToHost, c->stream), "read objective");
+      HIP_TRY(c, hipMemcpyAsync(&status, c->ib.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
       HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+      if ((rc = status_error(c, status))) return rc;
       bool stop = chg == 0;
       if (!stop && tol > 0.0 && t > 0 && (Jprev - J) <= tol * std::fabs(Jprev)) stop = true;
       Jprev = J;
@@ -588,7 +593,9 @@ int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol,
   if (obj_hist && t > 0)
     HIP_TRY(c, hipMemcpyAsync(obj_hist, c->obj, (size_t)t * sizeof(double), hipMemcpyDeviceToHost, c->stream),
             "read objective history");
+  HIP_TRY(c, hipMemcpyAsync(&status, c->ib.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if ((rc = status_error(c, status))) return rc;
   if (iters_done) *iters_done = t;
   return KKM_OK;
 }
@@ -599,15 +606,20 @@ int kkm_step(kkm_ctx* c, const int32_t* cl_in, int32_t k, float* E, float* z, fl
   if ((rc = check_ready(c, k, 1))) return rc;
   if (!cl_in) return fail(c, KKM_ERR_ARG, "cl_in is NULL");
   if ((rc = ensure_ws(c, k, 1))) return rc;
-  if ((rc = check_ids_on_device(c, cl_in))) return rc;
+  if ((rc = label_pass(c, cl_in))) return rc;
   int* nxt = cl_out ? cl_out : c->clbuf[0];
   if ((rc = one_update(c, 0, cl_in, nxt, z, D))) return rc;
   if (E && (rc = run(c, KKM_PHASE_OTHER, "et_to_e", [&] { return launch_et_to_e(c->ib, c->counts[0], c->epos, E, c->stream); })))
     return rc;
   if (counts_out)
     HIP_TRY(c, hipMemcpyAsync(counts_out, c->counts[0], (size_t)k * 4, hipMemcpyDeviceToDevice, c->stream), "copy counts");
-  if (J) HIP_TRY(c, hipMemcpyAsync(J, c->obj, sizeof(double), hipMemcpyDeviceToHost, c->stream), "read objective");
+  double Jv = 0.0;
+  int status = 0;
+  HIP_TRY(c, hipMemcpyAsync(&Jv, c->obj, sizeof(double), hipMemcpyDeviceToHost, c->stream), "read objective");
+  HIP_TRY(c, hipMemcpyAsync(&status, c->ib.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if ((rc = status_error(c, status))) return rc;
+  if (J) *J = Jv;
   return KKM_OK;
 }
 
@@ -623,7 +635,7 @@ int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
   if (r1 == r0) return KKM_OK;
   if (c->mode == KKM_MODE_ONTHEFLY) {
     int rc = run(c, KKM_PHASE_OTHER, "kernel_rows", [&] {
-      return launch_kernel_rows(c->Xp, c->nrm, c->sz.n, c->sz.d_pad, c->kp, r0, r1, out, c->stream);
+      return launch_kernel_rows(c->Xp, c->nrm, c->maxnrm, c->sz.n, c->sz.d_pad, c->kp, r0, r1, out, c->stream);
     });
     if (rc) return rc;
     HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
@@ -645,11 +657,11 @@ int kkm_copy_diag(kkm_ctx* c, float* out) {
   return KKM_OK;
 }
 
-int kkm_set_timing(kkm_ctx* c, int32_t enable) {
+int kkm_set_timing(kkm_ctx* c, int32_t phase_mask) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   (void)hipStreamSynchronize(c->stream);
   collect_timing(c);
-  c->timing = enable != 0;
+  c->timing = phase_mask & KKM_TIME_ALL;
   if (c->timing) c->tacc = kkm_timing{};
   return KKM_OK;
 }
@@ -672,7 +684,18 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   out->ld = c->sz.ld;
   out->bytes_K = c->mode == KKM_MODE_RESIDENT ? k_bytes(c->sz) : 0;
   out->bytes_total = c->held;
+  if (c->fixups < 0) {
+    unsigned long long cnt[kFixSegs] = {0};
+    if (c->fix_count) {
+      HIP_TRY(c, hipMemcpyAsync(cnt, c->fix_count, sizeof cnt, hipMemcpyDeviceToHost, c->stream), "read fix-up counts");
+      HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    }
+    int64_t tot = 0;
+    for (int q = 0; q < kFixSegs; ++q) tot += (int64_t)cnt[q];
+    c->fixups = tot;
+  }
   out->fixups = c->fixups;
+  out->fixup_capacity = c->fix_cap;
   return KKM_OK;
 }
 

@@ -14,12 +14,18 @@ constexpr int kTile = 128;
 constexpr int kBK = 16;
 
 // One-hot SpMM: a workgroup streams a stripe of kStripe columns of K over a
-// chunk of at most kChunk rows that all belong to one cluster.
+// chunk of at most kChunk rows that all belong to one cluster (long chunks:
+// fewer workgroup prologues and partial sums; 1024 rows measured best).
 constexpr int kStripe = 1024;
-constexpr int kChunk = 256;
+constexpr int kChunk = 1024;
 
 // Points per workgroup in the label/assign/scatter kernels.
 constexpr int kBlk = 256;
+
+// The Gaussian fix-up list is split into kFixSegs segments with a counter
+// each; workgroup b appends to segment b % kFixSegs, so no single atomic
+// counter serialises the K build.
+constexpr int kFixSegs = 256;
 
 enum Kind { LINEAR = 0, POLY = 1, GAUSS = 2 };
 
@@ -57,14 +63,18 @@ struct IterBufs {
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
-                        float* nrm, hipStream_t s);
-hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                             const KappaParams& kp, float* K, float* diagK, int2* fix_list,
-                             unsigned long long* fix_count, long long fix_cap, hipStream_t s);
-hipError_t launch_gauss_fixup_list(const float* Xp, int d_pad, int64_t ld, const KappaParams& kp,
-                                   const int2* fix_list, long long count, float* K, hipStream_t s);
-hipError_t launch_gauss_fixup_scan(const float* Xp, const float* nrm, int64_t n, int d_pad,
-                                   int64_t ld, const KappaParams& kp, float* K, hipStream_t s);
+                        float* nrm, unsigned* maxnrm_bits, hipStream_t s);
+hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
+                             int64_t n, int d_pad, int64_t ld, const KappaParams& kp, float* K,
+                             float* diagK, int2* fix_list, unsigned long long* fix_count,
+                             long long seg_cap, hipStream_t s);
+// Recomputes the listed Gaussian entries (counts read on the device); if a
+// segment received more entries than it holds, re-tests the whole triangle.
+// fix_list holds kFixSegs segments of seg_cap entries; fix_count kFixSegs counters.
+hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
+                              const KappaParams& kp, const int2* fix_list,
+                              const unsigned long long* fix_count, long long seg_cap, float* K,
+                              hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
 hipError_t launch_fill_diag(float* diagK, int64_t n, float v, hipStream_t s);
 
@@ -90,10 +100,12 @@ hipError_t launch_gather_sorted(const float* Xp, const float* nrm, const IterBuf
                                 hipStream_t s);
 hipError_t launch_diag_from_norms(const float* nrm, int64_t n, const KappaParams& kp, float* diagK,
                                   hipStream_t s);
-hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs, const IterBufs& b,
-                           int d_pad, const KappaParams& kp, float* Epart, hipStream_t s);
+hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
+                           const unsigned* maxnrm_bits, const IterBufs& b, int d_pad,
+                           const KappaParams& kp, float* Epart, hipStream_t s);
 hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const int* cs, hipStream_t s);
-hipError_t launch_kernel_rows(const float* Xp, const float* nrm, int64_t n, int d_pad,
-                              const KappaParams& kp, int64_t r0, int64_t r1, float* out, hipStream_t s);
+hipError_t launch_kernel_rows(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
+                              int64_t n, int d_pad, const KappaParams& kp, int64_t r0, int64_t r1,
+                              float* out, hipStream_t s);
 
 }  // namespace kkm

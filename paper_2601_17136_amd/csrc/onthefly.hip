@@ -58,7 +58,7 @@ __global__ void diag_from_norms_kernel(const float* __restrict__ nrm, int64_t n,
 template <int KIND>
 __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ Y,
                                   const float* __restrict__ ny, int64_t n, int d_pad,
-                                  int64_t row0, int64_t col0, const KappaParams& kp) {
+                                  int64_t row0, int64_t col0, const KappaParams& kp, bool may_fix) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
   float nj[2] = {0.f, 0.f};
@@ -78,7 +78,7 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
         float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
         if (KIND == GAUSS) {
           if (gi == gj) v = 1.f;
-          else if (gj < n && gi < n && gauss_needs_fix(v, ni, nj[bj], kp))
+          else if (may_fix && gj < n && gi < n && gauss_needs_fix(v, ni, nj[bj], kp))
             v = gauss_direct(Y + gi * d_pad, Y + gj * d_pad, d_pad, kp);
         }
         acc[bi][bj][r] = gj < n ? v : 0.f;
@@ -89,14 +89,22 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
 // Segment bounds: segment s of nseg covers column tiles [jt0, jt1).
 __device__ __host__ inline int seg_begin(int s, int nt, int nseg) { return (int)((int64_t)s * nt / nseg); }
 
+// Whether any Gaussian entry may need the fix-up, from the largest norm.
+__device__ inline bool any_fix(const unsigned* maxnrm_bits, const KappaParams& kp) {
+  const float m = __uint_as_float(*maxnrm_bits);
+  return kp.kind == GAUSS && gauss_needs_fix(1.f, m, m, kp);
+}
+
 template <int KIND>
 __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restrict__ Xs,
                                                           const float* __restrict__ nrm_s,
-                                                          const int* __restrict__ cs, int64_t n,
-                                                          int d_pad, int64_t ld, int nt, int nseg,
-                                                          int k, KappaParams kp,
+                                                          const int* __restrict__ cs,
+                                                          const unsigned* __restrict__ maxnrm_bits,
+                                                          int64_t n, int d_pad, int64_t ld, int nt,
+                                                          int nseg, int k, KappaParams kp,
                                                           float* __restrict__ Epart) {
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
+  const bool may_fix = any_fix(maxnrm_bits, kp);
   __shared__ float red[2][2][64];
   // Workgroup b runs on XCD b % 8; consecutive logical indices share a
   // segment, so the workgroups of one XCD sweep the same column tiles.
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restric
   for (int J = jt0; J < jt1; ++J) {
     const int64_t col0 = (int64_t)J * kTile;
     mma_tile(Xs + row0 * d_pad, Xs + col0 * d_pad, d_pad, lds, acc);
-    kappa_tile<KIND>(acc, Xs, nrm_s, n, d_pad, row0, col0, kp);
+    kappa_tile<KIND>(acc, Xs, nrm_s, n, d_pad, row0, col0, kp, may_fix);
     const int64_t last = (col0 + kTile - 1 < n) ? col0 + kTile - 1 : n - 1;
     const int cf = cs[col0], cl_last = cs[last];
     if (cf == cur && cl_last == cur) {
@@ -219,15 +227,17 @@ __global__ __launch_bounds__(256) void onthefly_reduce_kernel(IterBufs b,
 template <int KIND>
 __global__ __launch_bounds__(256, 2) void kernel_rows_kernel(const float* __restrict__ Xp,
                                                              const float* __restrict__ nrm,
+                                                             const unsigned* __restrict__ maxnrm_bits,
                                                              int64_t n, int d_pad, int64_t R0,
                                                              int64_t r0, int64_t r1, int nt,
                                                              KappaParams kp, float* __restrict__ out) {
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
+  const bool may_fix = any_fix(maxnrm_bits, kp);
   const int J = (int)(blockIdx.x % (unsigned)nt), I = (int)(blockIdx.x / (unsigned)nt);
   const int64_t row0 = R0 + (int64_t)I * kTile, col0 = (int64_t)J * kTile;
   floatx16 acc[2][2];
   mma_tile(Xp + row0 * d_pad, Xp + col0 * d_pad, d_pad, lds, acc);
-  kappa_tile<KIND>(acc, Xp, nrm, n, d_pad, row0, col0, kp);
+  kappa_tile<KIND>(acc, Xp, nrm, n, d_pad, row0, col0, kp, may_fix);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
 #pragma unroll
@@ -270,16 +280,17 @@ int onthefly_segments(int64_t n) {
   return nseg < 1 ? 1 : nseg;
 }
 
-hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs, const IterBufs& b,
-                           int d_pad, const KappaParams& kp, float* Epart, hipStream_t s) {
+hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
+                           const unsigned* maxnrm_bits, const IterBufs& b, int d_pad,
+                           const KappaParams& kp, float* Epart, hipStream_t s) {
   const int nt = (int)((b.n + kTile - 1) / kTile), nseg = onthefly_segments(b.n);
   dim3 grid((unsigned)((int64_t)nt * nseg)), block(256);
   if (kp.kind == LINEAR)
-    hipLaunchKernelGGL(onthefly_kernel<LINEAR>, grid, block, 0, s, Xs, nrm_s, cs, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
+    hipLaunchKernelGGL(onthefly_kernel<LINEAR>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
   else if (kp.kind == POLY)
-    hipLaunchKernelGGL(onthefly_kernel<POLY>, grid, block, 0, s, Xs, nrm_s, cs, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
+    hipLaunchKernelGGL(onthefly_kernel<POLY>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
   else
-    hipLaunchKernelGGL(onthefly_kernel<GAUSS>, grid, block, 0, s, Xs, nrm_s, cs, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
+    hipLaunchKernelGGL(onthefly_kernel<GAUSS>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
   return hipGetLastError();
 }
 
@@ -290,18 +301,19 @@ hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const i
   return hipGetLastError();
 }
 
-hipError_t launch_kernel_rows(const float* Xp, const float* nrm, int64_t n, int d_pad,
-                              const KappaParams& kp, int64_t r0, int64_t r1, float* out, hipStream_t s) {
+hipError_t launch_kernel_rows(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
+                              int64_t n, int d_pad, const KappaParams& kp, int64_t r0, int64_t r1,
+                              float* out, hipStream_t s) {
   const int nt = (int)((n + kTile - 1) / kTile);
   const int64_t R0 = r0 / kTile * kTile;
   const int64_t rt = (r1 - R0 + kTile - 1) / kTile;
   dim3 grid((unsigned)(rt * nt)), block(256);
   if (kp.kind == LINEAR)
-    hipLaunchKernelGGL(kernel_rows_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, n, d_pad, R0, r0, r1, nt, kp, out);
+    hipLaunchKernelGGL(kernel_rows_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, R0, r0, r1, nt, kp, out);
   else if (kp.kind == POLY)
-    hipLaunchKernelGGL(kernel_rows_kernel<POLY>, grid, block, 0, s, Xp, nrm, n, d_pad, R0, r0, r1, nt, kp, out);
+    hipLaunchKernelGGL(kernel_rows_kernel<POLY>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, R0, r0, r1, nt, kp, out);
   else
-    hipLaunchKernelGGL(kernel_rows_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, n, d_pad, R0, r0, r1, nt, kp, out);
+    hipLaunchKernelGGL(kernel_rows_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, R0, r0, r1, nt, kp, out);
   return hipGetLastError();
 }
 

@@ -10,10 +10,13 @@
 namespace kkm {
 
 // One wavefront per row; a fixed shuffle tree makes the norm deterministic.
+// maxnrm_bits (zero on entry) receives the largest norm as its IEEE bits
+// (non-negative floats order like their bit patterns).
 __global__ __launch_bounds__(256) void stage_kernel(const float* __restrict__ X, int64_t n, int d,
                                                     int d_pad, int64_t n_pad,
                                                     float* __restrict__ Xp,
-                                                    float* __restrict__ nrm) {
+                                                    float* __restrict__ nrm,
+                                                    unsigned* __restrict__ maxnrm_bits) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= n_pad) return;
@@ -24,13 +27,16 @@ __global__ __launch_bounds__(256) void stage_kernel(const float* __restrict__ X,
     s = fmaf(v, v, s);
   }
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (lane == 0) nrm[i] = s;
+  if (lane == 0) {
+    nrm[i] = s;
+    atomicMax(maxnrm_bits, __float_as_uint(s));
+  }
 }
 
 hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
-                        float* nrm, hipStream_t s) {
+                        float* nrm, unsigned* maxnrm_bits, hipStream_t s) {
   dim3 grid((unsigned)((n_pad + 3) / 4));
-  hipLaunchKernelGGL(stage_kernel, grid, dim3(256), 0, s, X, n, d, d_pad, n_pad, Xp, nrm);
+  hipLaunchKernelGGL(stage_kernel, grid, dim3(256), 0, s, X, n, d, d_pad, n_pad, Xp, nrm, maxnrm_bits);
   return hipGetLastError();
 }
 

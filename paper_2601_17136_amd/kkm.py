@@ -43,7 +43,7 @@ class kkm_info(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int32), ("d_pad", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("mode", ctypes.c_int32), ("ld", ctypes.c_int64),
                 ("bytes_K", ctypes.c_size_t), ("bytes_total", ctypes.c_size_t),
-                ("fixups", ctypes.c_int64)]
+                ("fixups", ctypes.c_int64), ("fixup_capacity", ctypes.c_int64)]
 
 
 _lib = None
@@ -197,8 +197,17 @@ def kkm_copy_diag(ctx, out) -> None:
     _check(lib().kkm_copy_diag(ctx, _dev_ptr(out, torch.float32, "out")), ctx)
 
 
-def kkm_set_timing(ctx, enable: bool) -> None:
-    _check(lib().kkm_set_timing(ctx, 1 if enable else 0), ctx)
+KKM_TIME_ALL = (1 << len(PHASES)) - 1
+
+
+def phase_mask(*names) -> int:
+    """Bit mask of the named phases for kkm_set_timing."""
+    return sum(1 << PHASES.index(n) for n in names)
+
+
+def kkm_set_timing(ctx, phase_mask_: int) -> None:
+    """phase_mask_: phases to bracket with HIP events (KKM_TIME_ALL, 0 = off)."""
+    _check(lib().kkm_set_timing(ctx, int(phase_mask_)), ctx)
 
 
 def kkm_get_timing(ctx) -> dict:

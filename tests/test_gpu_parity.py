@@ -247,3 +247,22 @@ def test_bitwise_reproducible(oracle, mode):
         assert np.array_equal(s1[key], s2[key]), key
     assert s1["J"] == s2["J"]
     assert np.array_equal(i1[0], i2[0]) and np.array_equal(i1[2], i2[2])
+
+
+def test_gauss_fixup_overflow_path(oracle):
+    """With a memory budget that leaves room for only a few thousand fix-up
+    list entries, more entries qualify than the list holds and the fix-up
+    re-tests the whole triangle; K must still match the oracle."""
+    _torch_cuda()
+    from paper_2601_17136_amd import kkm
+    X = datagen.make_points(4, n=3000)[0]
+    _, need = kkm.kkm_plan(3000, X.shape[1], 1, 1 << 40, kkm.KKM_MODE_RESIDENT)
+    with Engine(X, "gauss", 0.5, mem_budget=need + 4096) as eng:
+        K = eng.K_rows()
+        info = eng.info()
+    assert info["fixups"] > info["fixup_capacity"] > 0, info
+    err = rowscaled_err(K, oracle.Kernel("gauss", 0.5).matrix(X))
+    assert err <= TOL, err
+    with Engine(X, "gauss", 0.5) as eng:
+        K2 = eng.K_rows()
+    assert rowscaled_err(K2, oracle.Kernel("gauss", 0.5).matrix(X)) <= TOL
