@@ -35,8 +35,10 @@ __device__ inline void triangle_tile(int64_t t, int64_t nt, int64_t& I, int64_t&
   J = nt - 1 - o;
 }
 
+// Four workgroups per CU (40 KB of LDS each): while some run their store
+// epilogue, others keep the matrix cores busy.
 template <int KIND>
-__global__ __launch_bounds__(256, 2) void gemm_kappa_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemm_kappa_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm,
     const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, int64_t nt,
     int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,

@@ -73,7 +73,9 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
   } else {
     b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
     b += (size_t)s.n_pad * 8;             // their norms and cluster ids
-    b += (size_t)onthefly_segments(s.n) * k * s.ld * 4;  // segment partials
+    b += (size_t)onthefly_segments(s.n) * k * s.ld * 4;  // row-side segment partials
+    b += (size_t)onthefly_cpart_floats(s.n, k) * 4;      // column-side partials
+    b += (size_t)(s.n_pad / kTile) * 16;                 // per-block tables
   }
   b += (size_t)k * s.nstripes * 8;        // zpart
   b += (size_t)2 * k * s.nblk * 4;        // hist, base
@@ -81,7 +83,7 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
   b += (size_t)3 * qmax * 4 + 4;          // chunk table
   b += (size_t)4 * s.n * 4;               // perm, pos, two id buffers
   b += (size_t)2 * k * 4 + 64;            // counts, status
-  return b + 32 * 256;                    // alignment slack
+  return b + 40 * 256;                    // alignment slack
 }
 
 }  // namespace
@@ -108,8 +110,9 @@ struct kkm_ctx {
 
   int k_ws = 0, iter_ws = 0;
   IterBufs ib{};
-  float *Xs = nullptr, *nrm_s = nullptr, *Epart = nullptr;  // on-the-fly scratch
+  float *Xs = nullptr, *nrm_s = nullptr, *Epart = nullptr, *Cpart = nullptr;  // on-the-fly scratch
   int* cs = nullptr;
+  OtfTables otb{};
   const int* epos = nullptr;  // column order of E^T after the last update (null: identity)
   int* counts[2] = {nullptr, nullptr};
   int* clbuf[2] = {nullptr, nullptr};
@@ -217,8 +220,9 @@ void free_ws(kkm_ctx* c) {
   release(c, c->ws_allocs);
   c->k_ws = 0;
   c->ib = IterBufs{};
-  c->Xs = c->nrm_s = c->Epart = nullptr;
+  c->Xs = c->nrm_s = c->Epart = c->Cpart = nullptr;
   c->cs = nullptr;
+  c->otb = OtfTables{};
 }
 
 void free_hist(kkm_ctx* c) {
@@ -271,6 +275,11 @@ int carve_ws(kkm_ctx* c, int k) {
     c->nrm_s = (float*)take((size_t)s.n_pad * 4);
     c->cs = (int*)take((size_t)s.n_pad * 4);
     c->Epart = (float*)take((size_t)onthefly_segments(s.n) * k * s.ld * 4);
+    c->Cpart = (float*)take((size_t)onthefly_cpart_floats(s.n, k) * 4);
+    const size_t nt = (size_t)(s.n_pad / kTile);
+    c->otb.cA = (int*)take(nt * 4);
+    c->otb.nruns = (int*)take(nt * 4);
+    c->otb.cbase = (int64_t*)take(nt * 8);
   }
   b.zpart = (double*)take((size_t)k * s.nstripes * 8);
   b.hist = (int*)take((size_t)k * s.nblk * 4);
@@ -354,11 +363,12 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
          })))
       return rc;
     if ((rc = run(c, KKM_PHASE_ONTHEFLY, "onthefly", [&] {
-           return launch_onthefly(c->Xs, c->nrm_s, c->cs, c->maxnrm, b, s.d_pad, c->kp, c->Epart, c->stream);
+           return launch_onthefly(c->Xs, c->nrm_s, c->cs, c->maxnrm, b, s.d_pad, c->kp, c->otb, c->Epart,
+                                  c->Cpart, c->stream);
          })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "onthefly_reduce", [&] {
-           return launch_onthefly_reduce(b, c->Epart, c->cs, c->stream);
+           return launch_onthefly_reduce(b, c->Epart, c->Cpart, c->cs, c->otb, c->stream);
          })))
       return rc;
     pos = b.pos;

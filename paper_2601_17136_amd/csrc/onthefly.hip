@@ -5,14 +5,20 @@
 //
 // The points are first gathered into cluster-sorted order (the same stable
 // sort the resident path uses), so along a row of K the columns of one
-// cluster form one contiguous run.  A workgroup owns a block of 128 sorted
-// rows and sweeps a segment of 128-column tiles in order.  Each lane keeps,
-// for each of its 32 rows, the running sum of its own columns' entries;
-// when the sweep leaves a cluster the lanes' sums are reduced across the
-// workgroup in a fixed order and written as that cluster's partial for the
-// segment.  A second kernel adds the segments in order.  E comes out in
-// sorted row order; the assign kernel reads it through the inverse
-// permutation.
+// cluster form one contiguous run, and a block of 128 sorted rows spans few
+// clusters.  K is symmetric, so only tiles (I, J) with I <= J are computed:
+//   * row side: a workgroup owns row block I and sweeps a segment of column
+//     tiles J >= I in order.  Each lane keeps, for each of its 32 rows, the
+//     running sum of its own columns' entries; when the sweep leaves a cluster
+//     the lanes' sums are reduced across the workgroup in a fixed order and
+//     written as that cluster's partial for the segment.
+//   * column side (J > I): the tile's column sums over the rows of I, one per
+//     cluster run of those rows, are the row sums of block J over columns I
+//     (K(i,j) = K(j,i)); they are written as partials of block J.
+// A second kernel adds, for every sorted row and cluster, the row-side
+// segment partials and the column-side partials of the earlier blocks, in a
+// fixed order.  E comes out in sorted row order; the assign kernel reads it
+// through the inverse permutation.
 #include "tile_mma.h"
 
 namespace kkm {
@@ -51,73 +57,148 @@ __global__ void diag_from_norms_kernel(const float* __restrict__ nrm, int64_t n,
   diagK[i] = KIND == GAUSS ? 1.f : kappa<KIND>(nrm[i], 0.f, 0.f, kp);
 }
 
-// One 128 x 128 tile of K from its B tile (acc), rows at row0 and columns at
-// col0 of the staged points Y (n_pad x d_pad, norms ny): kappa applied, the
-// Gaussian diagonal set to exactly 1, columns >= n zeroed, and Gaussian
-// entries flagged as cancellation-prone recomputed from the differences.
-template <int KIND>
-__device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ Y,
-                                  const float* __restrict__ ny, int64_t n, int d_pad,
-                                  int64_t row0, int64_t col0, const KappaParams& kp, bool may_fix) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
-  float nj[2] = {0.f, 0.f};
-  if (KIND == GAUSS) {
-    nj[0] = ny[col0 + wn * 64 + l32];
-    nj[1] = ny[col0 + wn * 64 + 32 + l32];
-  }
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-      const float ni = (KIND == GAUSS) ? ny[gi] : 0.f;
-#pragma unroll
-      for (int bj = 0; bj < 2; ++bj) {
-        const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
-        float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
-        if (KIND == GAUSS) {
-          if (gi == gj) v = 1.f;
-          else if (may_fix && gj < n && gi < n && gauss_needs_fix(v, ni, nj[bj], kp))
-            v = gauss_direct(Y + gi * d_pad, Y + gj * d_pad, d_pad, kp);
-        }
-        acc[bi][bj][r] = gj < n ? v : 0.f;
-      }
-    }
-}
-
-// Segment bounds: segment s of nseg covers column tiles [jt0, jt1).
-__device__ __host__ inline int seg_begin(int s, int nt, int nseg) { return (int)((int64_t)s * nt / nseg); }
-
 // Whether any Gaussian entry may need the fix-up, from the largest norm.
 __device__ inline bool any_fix(const unsigned* maxnrm_bits, const KappaParams& kp) {
   const float m = __uint_as_float(*maxnrm_bits);
   return kp.kind == GAUSS && gauss_needs_fix(1.f, m, m, kp);
 }
 
-template <int KIND>
-__global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restrict__ Xs,
-                                                          const float* __restrict__ nrm_s,
-                                                          const int* __restrict__ cs,
-                                                          const unsigned* __restrict__ maxnrm_bits,
-                                                          int64_t n, int d_pad, int64_t ld, int nt,
-                                                          int nseg, int k, KappaParams kp,
-                                                          float* __restrict__ Epart) {
-  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
-  const bool may_fix = any_fix(maxnrm_bits, kp);
-  __shared__ float red[2][2][64];
-  // Workgroup b runs on XCD b % 8; consecutive logical indices share a
-  // segment, so the workgroups of one XCD sweep the same column tiles.
-  const int64_t T = (int64_t)nt * nseg;
-  const int64_t b = blockIdx.x;
-  const int64_t per = T >> 3, rem = T & 7, x = b & 7;
-  const int64_t t = x * per + (x < rem ? x : rem) + (b >> 3);
-  const int I = (int)(t % nt), s = (int)(t / nt);
-  const int jt0 = seg_begin(s, nt, nseg), jt1 = seg_begin(s + 1, nt, nseg);
+// One 128 x 128 tile of K from its B tile (acc), rows at row0 and columns at
+// col0 of the staged points Y (n_pad x d_pad, column norms ny; row norms
+// rn[0..127] for the tile's rows): kappa applied, the Gaussian diagonal set to
+// exactly 1, entries outside n x n zeroed, and (FIX) Gaussian entries flagged
+// as cancellation-prone recomputed from the differences after the unrolled
+// pass.  Row indices are block-local 32-bit values, so no per-row 64-bit
+// index stays live across tiles.
+template <int KIND, bool FIX>
+__device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ Y,
+                                  const float* __restrict__ ny, const float* rn, int64_t n,
+                                  int d_pad, int64_t row0, int64_t col0, const KappaParams& kp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const int nrows = (int)(n - row0 < kTile ? n - row0 : kTile);
+  const int ncols = (int)(n - col0 < kTile ? n - col0 : kTile);
+  const bool diag = row0 == col0;
+  const bool interior = nrows == kTile && ncols == kTile && !diag;
+  const int rbase = wm * 64 + 4 * h, cbase = wn * 64 + l32;
+  float nj[2] = {0.f, 0.f};
+  if (KIND == GAUSS) {
+    nj[0] = ny[col0 + cbase];
+    nj[1] = ny[col0 + cbase + 32];
+  }
+  unsigned long long fixmask = 0;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3);
+      const float ni = (KIND == GAUSS) ? rn[il] : 0.f;
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) {
+        const int jl = cbase + bj * 32;
+        float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
+        if (FIX && gauss_needs_fix(v, ni, nj[bj], kp) && !(diag && il == jl))
+          fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
+        if (!interior) {
+          if (KIND == GAUSS && diag && il == jl) v = 1.f;
+          if (il >= nrows || jl >= ncols) v = 0.f;
+        }
+        acc[bi][bj][r] = v;
+      }
+    }
+  if (KIND == GAUSS && FIX) {
+    while (fixmask) {
+      const int e = __ffsll((long long)fixmask) - 1;
+      fixmask &= fixmask - 1;
+      const int bi = e >> 5, bj = (e >> 4) & 1, r = e & 15;
+      const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3), jl = cbase + bj * 32;
+      if (il < nrows && jl < ncols) {
+        const float w = gauss_direct(Y + (row0 + il) * d_pad, Y + (col0 + jl) * d_pad, d_pad, kp);
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr)
+              if (q == bi && p == bj && rr == r) acc[q][p][rr] = w;
+      }
+    }
+  }
+}
+
+// Segment bounds: segment s of nseg covers column tiles [seg_begin(s), seg_begin(s+1)).
+__device__ __host__ inline int seg_begin(int s, int nt, int nseg) { return (int)((int64_t)s * nt / nseg); }
+
+// Per update: for each row block P of the sorted order, the first cluster its
+// rows hold (cA), how many clusters they span (nruns), and where its
+// column-side partials start (cbase, in rows of 128 floats):
+//   cbase[P] = sum_{P' < P} (nt - 1 - P') * nruns[P'].
+// One workgroup: a thread per contiguous range of blocks, then a scan.
+__global__ __launch_bounds__(1024) void onthefly_tables_kernel(const int* __restrict__ cs, int64_t n,
+                                                               int nt, int* __restrict__ cA,
+                                                               int* __restrict__ nruns,
+                                                               int64_t* __restrict__ cbase) {
+  __shared__ int64_t part[1024];
+  const int tid = threadIdx.x;
+  const int per = (nt + 1023) / 1024, lo = tid * per, hi = min(nt, lo + per);
+  int64_t s = 0;
+  for (int P = lo; P < hi; ++P) {
+    const int64_t last = min((int64_t)P * kTile + kTile - 1, n - 1);
+    const int a = cs[(int64_t)P * kTile], b = cs[last];
+    cA[P] = a;
+    nruns[P] = b - a + 1;
+    s += (int64_t)(nt - 1 - P) * (b - a + 1);
+  }
+  part[tid] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive scan (Hillis-Steele)
+    const int64_t v = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int64_t run = tid > 0 ? part[tid - 1] : 0;
+  for (int P = lo; P < hi; ++P) {
+    cbase[P] = run;
+    run += (int64_t)(nt - 1 - P) * nruns[P];
+  }
+}
+
+// FIX: the variant with the Gaussian fix-up path.  Both variants are
+// launched; each returns at once unless the largest norm calls for it.
+template <int KIND, bool FIX>
+__global__ __launch_bounds__(256, 2) void onthefly_kernel(
+    const float* __restrict__ Xs, const float* __restrict__ nrm_s, const int* __restrict__ cs,
+    const unsigned* __restrict__ maxnrm_bits, const int* __restrict__ off,
+    const int* __restrict__ cA, const int* __restrict__ nruns, const int64_t* __restrict__ cbase,
+    int64_t n, int d_pad, int64_t ld, int nt, int nseg, int k, KappaParams kp,
+    float* __restrict__ Epart, float* __restrict__ Cpart) {
+  // The block's row norms sit after the mainloop buffers in the same array,
+  // so the compiler reloads them per tile instead of pinning 32 registers.
+  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats + kTile];
+  // Work items (segment s, row block I < seg_begin(s+1)), segment-major: the
+  // hardware deals consecutive workgroups round-robin to the 8 XCDs, so every
+  // XCD gets an even share, and the concurrent workgroups of one XCD sweep
+  // the same column tiles (shared in its L2).
+  int s = 0;
+  int64_t first = 0;  // items before segment s
+  while (s + 1 < nseg && first + seg_begin(s + 1, nt, nseg) <= (int64_t)blockIdx.x) {
+    first += seg_begin(s + 1, nt, nseg);
+    ++s;
+  }
+  const int I = (int)((int64_t)blockIdx.x - first);
+  const int sb = seg_begin(s, nt, nseg), se = seg_begin(s + 1, nt, nseg);
+  if (I >= se) return;  // only past the last item
+  if (KIND == GAUSS && any_fix(maxnrm_bits, kp) != FIX) return;
+  const int jt0 = sb > I ? sb : I, jt1 = se;
   const int64_t row0 = (int64_t)I * kTile;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const int runA = cA[I], nr = nruns[I];
+  float* const cp = Cpart + cbase[I] * kTile;  // this block's column-side partials
+  float* const rn = lds + kLdsFloats;
+  if (tid < kTile) rn[tid] = nrm_s[row0 + tid];
 
   float rowacc[2][16];
 #pragma unroll
@@ -125,9 +206,10 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restric
 #pragma unroll
     for (int r = 0; r < 16; ++r) rowacc[bi][r] = 0.f;
 
-  // Reduce the lanes' running sums over the 128 columns of each row and write
-  // them as cluster c's partial for this segment; fixed order throughout.
+  // Row side: reduce the lanes' running sums over the columns of each row and
+  // write them as cluster c's partial for this segment; fixed order.
   auto flush = [&](int c) {
+    float* red = lds;  // [wm][wn][64], free between tiles
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
@@ -138,14 +220,45 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restric
         v += __shfl_xor(v, 4, 64);
         v += __shfl_xor(v, 2, 64);
         v += __shfl_xor(v, 1, 64);
-        if (l32 == 0) red[wm][wn][bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = v;
+        if (l32 == 0) red[(wm * 2 + wn) * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = v;
         rowacc[bi][r] = 0.f;
       }
     __syncthreads();
     if (wn == 0) {
       const int64_t gi = row0 + wm * 64 + lane;
-      if (gi < n) Epart[((int64_t)s * k + c) * ld + gi] = red[wm][0][lane] + red[wm][1][lane];
+      if (gi < n)
+        Epart[((int64_t)s * k + c) * ld + gi] = red[(wm * 2) * 64 + lane] + red[(wm * 2 + 1) * 64 + lane];
     }
+    __syncthreads();
+  };
+
+  // Column side of tile (I, J), J > I: column sums over the rows in sorted
+  // positions [lo, hi) (all rows when the block holds one cluster) written as
+  // run u of the tile's partials; fixed order.
+  auto column_side = [&](int J, int u, bool all_rows, int lo, int hi, floatx16 (&a)[2][2]) {
+    float c0 = 0.f, c1 = 0.f;
+    const int llo = lo - (int)row0, lhi = hi - (int)row0;  // block-local row range
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        bool in = all_rows;
+        if (!all_rows) {
+          const int il = wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          in = il >= llo && il < lhi;
+        }
+        c0 += in ? a[bi][0][r] : 0.f;
+        c1 += in ? a[bi][1][r] : 0.f;
+      }
+    c0 += __shfl_xor(c0, 32, 64);
+    c1 += __shfl_xor(c1, 32, 64);
+    float* csum = lds;  // [wm][128]
+    if (h == 0) {
+      csum[wm * 128 + wn * 64 + l32] = c0;
+      csum[wm * 128 + wn * 64 + 32 + l32] = c1;
+    }
+    __syncthreads();
+    if (tid < kTile) cp[((int64_t)(J - I - 1) * nr + u) * kTile + tid] = csum[tid] + csum[kTile + tid];
     __syncthreads();
   };
 
@@ -154,7 +267,7 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restric
   for (int J = jt0; J < jt1; ++J) {
     const int64_t col0 = (int64_t)J * kTile;
     mma_tile(Xs + row0 * d_pad, Xs + col0 * d_pad, d_pad, lds, acc);
-    kappa_tile<KIND>(acc, Xs, nrm_s, n, d_pad, row0, col0, kp, may_fix);
+    kappa_tile<KIND, FIX>(acc, Xs, nrm_s, rn, n, d_pad, row0, col0, kp);
     const int64_t last = (col0 + kTile - 1 < n) ? col0 + kTile - 1 : n - 1;
     const int cf = cs[col0], cl_last = cs[last];
     if (cf == cur && cl_last == cur) {
@@ -177,17 +290,26 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(const float* __restric
             rowacc[bi][r] += (c0 == c ? acc[bi][0][r] : 0.f) + (c1 == c ? acc[bi][1][r] : 0.f);
       }
     }
+    if (J > I) {
+      if (nr == 1) {
+        column_side(J, 0, true, 0, 0, acc);
+      } else {
+        for (int u = 0; u < nr; ++u) column_side(J, u, false, off[runA + u], off[runA + u + 1], acc);
+      }
+    }
   }
   flush(cur);
 }
 
-// Workgroup (stripe, j): E^T_sorted(j, stripe) = sum over the segments that
-// overlap cluster j's sorted range, in segment order; plus the stripe's part
-// of sum_{p in L_j} E(p, j) in fp64 (sorted positions: cs[p] == j).
-__global__ __launch_bounds__(256) void onthefly_reduce_kernel(IterBufs b,
-                                                              const float* __restrict__ Epart,
-                                                              const int* __restrict__ cs, int nt,
-                                                              int nseg) {
+// Workgroup (stripe, j): E^T_sorted(j, q) for the stripe's sorted rows q:
+//   the row-side partials of the segments that block Q = q/128 swept over
+//   columns of cluster j, in segment order, then the column-side partials of
+//   the blocks P < Q holding rows of cluster j, in block order;
+// plus the stripe's part of sum_{q in L_j} E(q, j) in fp64 (cs[q] == j).
+__global__ __launch_bounds__(256) void onthefly_reduce_kernel(
+    IterBufs b, const float* __restrict__ Epart, const float* __restrict__ Cpart,
+    const int* __restrict__ cs, const int* __restrict__ cA, const int* __restrict__ nruns,
+    const int64_t* __restrict__ cbase, int nt, int nseg) {
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int j = (int)(blockIdx.x / (unsigned)ns);
@@ -200,23 +322,25 @@ __global__ __launch_bounds__(256) void onthefly_reduce_kernel(IterBufs b,
   const int64_t col = (int64_t)stripe * kStripe + tid * 4;
   double zs = 0.0;
   if (col < ld) {
+    const int Q = (int)(col / kTile);
     f4 e = {0.f, 0.f, 0.f, 0.f};
-    bool first = true;
     for (int s = 0; s < nseg; ++s) {
-      const int64_t c0 = (int64_t)seg_begin(s, nt, nseg) * kTile;
-      const int64_t c1 = (int64_t)seg_begin(s + 1, nt, nseg) * kTile;
-      if (c0 < hi && lo < c1) {
-        const f4 v = *(const f4*)(Epart + ((int64_t)s * b.k + j) * ld + col);
-        e = first ? v : e + v;
-        first = false;
-      }
+      const int sb = seg_begin(s, nt, nseg), se = seg_begin(s + 1, nt, nseg);
+      if (se <= Q) continue;
+      const int64_t c0 = (int64_t)(sb > Q ? sb : Q) * kTile;
+      const int64_t c1 = (int64_t)se * kTile < b.n ? (int64_t)se * kTile : b.n;
+      if (c0 < hi && lo < c1) e += *(const f4*)(Epart + ((int64_t)s * b.k + j) * ld + col);
     }
+    const int Pl = (hi - 1) / kTile;
+    for (int P = lo / kTile; P <= Pl && P < Q; ++P)
+      e += *(const f4*)(Cpart + ((cbase[P] + (int64_t)(Q - P - 1) * nruns[P] + (j - cA[P])) * kTile +
+                                 (col - (int64_t)Q * kTile)));
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
       if (col + c < b.n && cs[col + c] == j) zs += (double)e[c];
   }
-  for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off, 64);
+  for (int o = 32; o > 0; o >>= 1) zs += __shfl_xor(zs, o, 64);
   if ((tid & 63) == 0) red[tid >> 6] = zs;
   __syncthreads();
   if (tid == 0) b.zpart[(int64_t)j * ns + stripe] = (red[0] + red[1]) + (red[2] + red[3]);
@@ -231,13 +355,15 @@ __global__ __launch_bounds__(256, 2) void kernel_rows_kernel(const float* __rest
                                                              int64_t n, int d_pad, int64_t R0,
                                                              int64_t r0, int64_t r1, int nt,
                                                              KappaParams kp, float* __restrict__ out) {
-  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
-  const bool may_fix = any_fix(maxnrm_bits, kp);
+  __shared__ __attribute__((aligned(16))) float lds[kLdsFloats + kTile];
   const int J = (int)(blockIdx.x % (unsigned)nt), I = (int)(blockIdx.x / (unsigned)nt);
   const int64_t row0 = R0 + (int64_t)I * kTile, col0 = (int64_t)J * kTile;
+  float* const rn = lds + kLdsFloats;
+  if (threadIdx.x < kTile) rn[threadIdx.x] = nrm[row0 + threadIdx.x];
   floatx16 acc[2][2];
   mma_tile(Xp + row0 * d_pad, Xp + col0 * d_pad, d_pad, lds, acc);
-  kappa_tile<KIND>(acc, Xp, nrm, n, d_pad, row0, col0, kp, may_fix);
+  if (any_fix(maxnrm_bits, kp)) kappa_tile<KIND, true>(acc, Xp, nrm, rn, n, d_pad, row0, col0, kp);
+  else kappa_tile<KIND, false>(acc, Xp, nrm, rn, n, d_pad, row0, col0, kp);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
 #pragma unroll
@@ -274,30 +400,52 @@ hipError_t launch_diag_from_norms(const float* nrm, int64_t n, const KappaParams
 
 int onthefly_segments(int64_t n) {
   const int nt = (int)((n + kTile - 1) / kTile);
-  int nseg = (4096 + nt - 1) / nt;  // at least ~4096 workgroups: 8 per CU slot pair
+  int nseg = (8192 + nt - 1) / nt;  // ~4096 workgroups right of the diagonal
   if (nseg > nt) nseg = nt;
   if (nseg > 64) nseg = 64;
   return nseg < 1 ? 1 : nseg;
 }
 
+int64_t onthefly_cpart_floats(int64_t n, int k) {
+  const int64_t nt = (n + kTile - 1) / kTile;
+  // sum_P (nt-1-P) * nruns[P] with sum_P nruns[P] <= nt + k - 1
+  return (nt * (nt - 1) / 2 + (int64_t)(k - 1) * (nt > 0 ? nt - 1 : 0)) * kTile + kTile;
+}
+
 hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
                            const unsigned* maxnrm_bits, const IterBufs& b, int d_pad,
-                           const KappaParams& kp, float* Epart, hipStream_t s) {
+                           const KappaParams& kp, const OtfTables& tb, float* Epart, float* Cpart,
+                           hipStream_t s) {
   const int nt = (int)((b.n + kTile - 1) / kTile), nseg = onthefly_segments(b.n);
-  dim3 grid((unsigned)((int64_t)nt * nseg)), block(256);
-  if (kp.kind == LINEAR)
-    hipLaunchKernelGGL(onthefly_kernel<LINEAR>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
-  else if (kp.kind == POLY)
-    hipLaunchKernelGGL(onthefly_kernel<POLY>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
-  else
-    hipLaunchKernelGGL(onthefly_kernel<GAUSS>, grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart);
+  hipLaunchKernelGGL(onthefly_tables_kernel, dim3(1), dim3(1024), 0, s, cs, b.n, nt, tb.cA,
+                     tb.nruns, tb.cbase);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int64_t items = 0;  // (segment, row block) pairs right of the diagonal
+  for (int q = 0; q < nseg; ++q) items += seg_begin(q + 1, nt, nseg);
+  dim3 grid((unsigned)items), block(256);
+  if (kp.kind == LINEAR) {
+    hipLaunchKernelGGL((onthefly_kernel<LINEAR, false>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits,
+                       b.off, tb.cA, tb.nruns, tb.cbase, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart, Cpart);
+  } else if (kp.kind == POLY) {
+    hipLaunchKernelGGL((onthefly_kernel<POLY, false>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits,
+                       b.off, tb.cA, tb.nruns, tb.cbase, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart, Cpart);
+  } else {
+    hipLaunchKernelGGL((onthefly_kernel<GAUSS, false>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits,
+                       b.off, tb.cA, tb.nruns, tb.cbase, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart, Cpart);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((onthefly_kernel<GAUSS, true>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits,
+                       b.off, tb.cA, tb.nruns, tb.cbase, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart, Cpart);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const int* cs, hipStream_t s) {
+hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const float* Cpart,
+                                  const int* cs, const OtfTables& tb, hipStream_t s) {
   const int nt = (int)((b.n + kTile - 1) / kTile), nseg = onthefly_segments(b.n);
   hipLaunchKernelGGL(onthefly_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b,
-                     Epart, cs, nt, nseg);
+                     Epart, Cpart, cs, tb.cA, tb.nruns, tb.cbase, nt, nseg);
   return hipGetLastError();
 }
 
