@@ -60,11 +60,23 @@ typedef enum kkm_status {
 typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
 
 /* Where K lives.  RESIDENT stores K (n*n fp32) in device memory once and
- * streams it every iteration.  ONTHEFLY never stores K: every iteration
- * recomputes its tiles and folds them straight into E, which is the paper's
- * single-GPU sliding-window baseline (Section VI-D) done tile by tile.
- * AUTO picks RESIDENT when K fits the memory budget, else ONTHEFLY. */
-typedef enum kkm_mode { KKM_MODE_AUTO = 0, KKM_MODE_RESIDENT = 1, KKM_MODE_ONTHEFLY = 2 } kkm_mode;
+ * streams it every iteration.  PACKED stores only the upper block triangle
+ * of the symmetric K (row block I of 128 rows keeps columns 128*I ..
+ * ld-1, about half the bytes) and streams that: each stored entry K(i,j)
+ * serves both E(j, cl(i)) and E(i, cl(j)).  PACKED handles at most
+ * KKM_PACKED_MAX_K clusters; it is the fastest mode for small k.  ONTHEFLY
+ * never stores K: every iteration recomputes its tiles and folds them
+ * straight into E, which is the paper's single-GPU sliding-window baseline
+ * (Section VI-D) done tile by tile.  AUTO picks RESIDENT when K fits the
+ * memory budget, else ONTHEFLY (it never picks PACKED, whose k limit is not
+ * known when K is built). */
+typedef enum kkm_mode {
+  KKM_MODE_AUTO = 0,
+  KKM_MODE_RESIDENT = 1,
+  KKM_MODE_ONTHEFLY = 2,
+  KKM_MODE_PACKED = 3
+} kkm_mode;
+#define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
 
 typedef struct kkm_params {
   float gamma;    /* POLY: scale of x.y; GAUSS: > 0.  Ignored for LINEAR. */
@@ -100,7 +112,9 @@ typedef struct kkm_info {
   int64_t n;
   int32_t d, d_pad;       /* feature count and its zero-padded width */
   int32_t kind, mode;     /* kkm_kind, resolved kkm_mode (never AUTO) */
-  int64_t ld;             /* row stride of K in floats (resident mode) */
+  int64_t ld;             /* RESIDENT: row stride of K in floats; PACKED: the
+                             padded row length (row block I holds ld - 128*I
+                             columns); ONTHEFLY: row stride of E^T */
   size_t bytes_K;         /* device bytes held by K (0 on the fly) */
   size_t bytes_total;     /* device bytes held by the context */
   int64_t fixups;         /* Gaussian entries flagged for recomputation at build */
@@ -126,8 +140,9 @@ const char *kkm_last_error(const kkm_ctx *ctx);
 /* Pure host planning, no HIP call.  Picks the mode for a problem and the
  * device bytes it needs (K, staged points, per-iteration scratch for k
  * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget.
- * Errors: KKM_ERR_ARG (bad sizes), KKM_ERR_OOM (even the on-the-fly mode
- * does not fit, or RESIDENT was requested and K does not fit). */
+ * Errors: KKM_ERR_ARG (bad sizes, or PACKED with k > KKM_PACKED_MAX_K),
+ * KKM_ERR_OOM (even the on-the-fly mode does not fit, or the requested
+ * storing mode does not). */
 int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode,
              int32_t *mode_out, size_t *bytes_out);
 
@@ -145,6 +160,8 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  *   (Gaussian: exactly 1).  Gaussian entries whose expansion
  *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are
  *   recomputed from the coordinate differences.
+ * PACKED: as RESIDENT, but only the tiles I <= J of the 128 x 128 tiling
+ *   are stored (row i keeps columns 128*floor(i/128) .. ld-1).
  * ONTHEFLY: stages X and row norms only.
  * Replaces any earlier build on ctx; a build of the same n, d, kind and mode
  * reuses the device buffers of the previous one.  Asynchronous.
@@ -155,7 +172,8 @@ int kkm_build_kernel(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t
 /* Run the clustering loop (Alg. 1 with one process).
  * V:          device int32[n]: the initial cluster ids on entry, the final
  *             ids on return.
- * k:          clusters, 1 .. min(n, KKM_MAX_K).
+ * k:          clusters, 1 .. min(n, KKM_MAX_K); at most KKM_PACKED_MAX_K
+ *             when K was built PACKED.
  * max_iter:   >= 0 assignment updates at most.
  * tol:        < 0: run exactly max_iter updates (no host round trip per
  *             update).  = 0: stop after an update that changed no id.
@@ -185,7 +203,8 @@ int kkm_step(kkm_ctx *ctx, const int32_t *cl_in, int32_t k, float *E, float *z, 
              int32_t *cl_out, int32_t *counts_out, double *J);
 
 /* Rows r0 .. r1-1 of K into out (device, (r1-r0) x n fp32 row-major).  In
- * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses.
+ * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses;
+ * in PACKED mode the part left of the stored triangle is read by symmetry.
  * Errors: KKM_ERR_ARG (range), KKM_ERR_STATE, KKM_ERR_HIP. */
 int kkm_copy_kernel_rows(kkm_ctx *ctx, int64_t r0, int64_t r1, float *out);
 

@@ -156,7 +156,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
       offs[j] = o;
       qf[j] = q;
       o += c;
-      q += (c + kChunk - 1) / kChunk;
+      q += (c + b.chunk_len - 1) / b.chunk_len;
     }
     offs[k] = o;
     qf[k] = q;
@@ -198,10 +198,10 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
         if (qf[mid] <= q) lo = mid;
         else hi = mid - 1;
       }
-      const int p0 = offs[lo] + (q - qf[lo]) * kChunk, end = offs[lo + 1];
+      const int p0 = offs[lo] + (q - qf[lo]) * b.chunk_len, end = offs[lo + 1];
       b.chunk_j[q] = lo;
       b.chunk_p0[q] = p0;
-      b.chunk_p1[q] = (p0 + kChunk < end) ? p0 + kChunk : end;
+      b.chunk_p1[q] = (p0 + b.chunk_len < end) ? p0 + b.chunk_len : end;
     }
   }
 
@@ -276,7 +276,10 @@ __global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restric
 
 // Workgroup (stripe, j): E^T(j, stripe) = sum of cluster j's chunk partials in
 // chunk order, and the stripe's share of sum_{i in L_j} E(i, j) (fp64) for z_j.
-__global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int* __restrict__ cl) {
+// Packed K: a chunk wrote no partial left of its first row's tile, and the
+// column-side sums Ecol (sorted positions) are added last.
+__global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int* __restrict__ cl,
+                                                          bool packed) {
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int j = (int)(blockIdx.x / (unsigned)ns);
@@ -288,8 +291,14 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int*
   const int64_t col = (int64_t)stripe * kStripe + tid * 4;
   double zs = 0.0;
   if (col < ld) {
-    f4 e = *(const f4*)(b.P + (int64_t)qa * ld + col);
-    for (int q = qa + 1; q < qb; ++q) e += *(const f4*)(b.P + (int64_t)q * ld + col);
+    f4 e = {0.f, 0.f, 0.f, 0.f};
+    for (int q = qa; q < qb; ++q)
+      if (!packed || col >= (int64_t)(b.perm[b.chunk_p0[q]] / kTile) * kTile)
+        e += *(const f4*)(b.P + (int64_t)q * ld + col);
+    if (packed)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (col + c < b.n) e[c] += b.Ecol[(int64_t)j * b.n + b.pos[col + c]];
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -307,8 +316,9 @@ hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s) 
   return hipGetLastError();
 }
 
-hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s) {
-  hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl);
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, bool packed, hipStream_t s) {
+  hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl,
+                     packed);
   return hipGetLastError();
 }
 

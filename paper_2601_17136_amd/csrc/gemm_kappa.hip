@@ -2,10 +2,12 @@
 // (or the linear / Gaussian kernel) applied in the epilogue.
 //
 // B = X X^T is symmetric, so only tiles (I, J) with I <= J of the 128 x 128
-// tiling are computed; an off-diagonal tile is stored twice, as itself and,
-// transposed through LDS, as tile (J, I).  The product runs on the fp32
-// matrix cores (v_mfma_f32_32x32x2_f32).  Each 256-thread workgroup owns one
-// tile, each wavefront a 64 x 64 quarter of it (2 x 2 MFMA blocks of 32 x 32).
+// tiling are computed.  Full storage keeps an off-diagonal tile twice, as
+// itself and, transposed through LDS, as tile (J, I); packed storage keeps
+// only the computed tiles (the upper block triangle, see packed_row).  The
+// product runs on the fp32 matrix cores (v_mfma_f32_32x32x2_f32).  Each
+// 256-thread workgroup owns one tile, each wavefront a 64 x 64 quarter of it
+// (2 x 2 MFMA blocks of 32 x 32).
 //
 // Within a 16-wide k chunk a lane feeds the MFMA from eight consecutive k of
 // its row: the half-wave h = lane/32 takes k = 8h .. 8h+7 and step s pairs
@@ -40,8 +42,8 @@ __device__ inline void triangle_tile(int64_t t, int64_t nt, int64_t& I, int64_t&
 template <int KIND>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemm_kappa_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm,
-    const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, int64_t nt,
-    int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
+    const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, bool packed,
+    int64_t nt, int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
     int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long seg_cap) {
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
   // No Gaussian entry can need the fix-up unless the largest norms allow it.
@@ -122,11 +124,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int64_t gj = col0 + wn * 64 + lane;
     for (int rr = 0; rr < 32; ++rr) {
       const int64_t gi = row0 + wm * 64 + bi * 32 + rr;
-      if (gi < n && gj < ld) __builtin_nontemporal_store((gj < n) ? Tw[rr * 65 + lane] : 0.f, K + gi * ld + gj);
+      const int64_t rowp = packed ? packed_row(gi, ld) : gi * ld;
+      if (gi < n && gj < ld) __builtin_nontemporal_store((gj < n) ? Tw[rr * 65 + lane] : 0.f, K + rowp + gj);
     }
     __syncthreads();
   }
-  if (I != J) {
+  if (I != J && !packed) {
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj) {  // tile (J, I): rows j, columns i
 #pragma unroll
@@ -146,8 +149,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 }
 
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                             int64_t n, int d_pad, int64_t ld, const KappaParams& kp, float* K,
-                             float* diagK, int2* fix_list, unsigned long long* fix_count,
+                             int64_t n, int d_pad, int64_t ld, bool packed, const KappaParams& kp,
+                             float* K, float* diagK, int2* fix_list, unsigned long long* fix_count,
                              long long seg_cap, hipStream_t s) {
   const int64_t nt = (n + kTile - 1) / kTile;
   const int64_t T = nt * (nt + 1) / 2;
@@ -155,15 +158,15 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
   switch (kp.kind) {
     case LINEAR:
       hipLaunchKernelGGL(gemm_kappa_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
     case POLY:
       hipLaunchKernelGGL(gemm_kappa_kernel<POLY>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
     default:
       hipLaunchKernelGGL(gemm_kappa_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
       break;
   }
   return hipGetLastError();
@@ -179,7 +182,8 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
 // no host round trip.
 __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp,
                                                           const float* __restrict__ nrm, int64_t n,
-                                                          int d_pad, int64_t ld, KappaParams kp,
+                                                          int d_pad, int64_t ld, bool packed,
+                                                          KappaParams kp,
                                                           const int2* __restrict__ list,
                                                           const unsigned long long* __restrict__ counts,
                                                           long long seg_cap, float* __restrict__ K) {
@@ -215,33 +219,40 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
     s += __shfl_xor(s, 4, 16);
     s += __shfl_xor(s, 2, 16);
     s += __shfl_xor(s, 1, 16);
-    if (gl == 0) {
+    if (gl == 0) {  // listed pairs have i < j: (i, j) is stored in both layouts
       const float v = __builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
-      K[(int64_t)ij.x * ld + ij.y] = v;
-      K[(int64_t)ij.y * ld + ij.x] = v;
+      if (packed) {
+        K[packed_row(ij.x, ld) + ij.y] = v;
+        if (ij.x / kTile == ij.y / kTile) K[packed_row(ij.y, ld) + ij.x] = v;
+      } else {
+        K[(int64_t)ij.x * ld + ij.y] = v;
+        K[(int64_t)ij.y * ld + ij.x] = v;
+      }
     }
   }
   __syncthreads();
   if (!overflow) return;
   for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
     const float ni = nrm[i];
+    const int64_t ri = packed ? packed_row(i, ld) : i * ld;
     for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
-      const float v = K[i * ld + j];
+      const float v = K[ri + j];
       if (gauss_needs_fix(v, ni, nrm[j], kp)) {
         const float w = gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
-        K[i * ld + j] = w;
-        K[j * ld + i] = w;
+        K[ri + j] = w;
+        if (!packed) K[j * ld + i] = w;
+        else if (i / kTile == j / kTile) K[packed_row(j, ld) + i] = w;
       }
     }
   }
 }
 
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                              const KappaParams& kp, const int2* fix_list,
+                              bool packed, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, float* K,
                               hipStream_t s) {
   hipLaunchKernelGGL(gauss_fixup_kernel, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                     ld, kp, fix_list, fix_count, seg_cap, K);
+                     ld, packed, kp, fix_list, fix_count, seg_cap, K);
   return hipGetLastError();
 }
 

@@ -1,10 +1,10 @@
 // Host side of the engine: the C ABI declared in include/kkm.h.
 //
 // A context owns every device buffer.  kkm_build_kernel stages the points and
-// (resident mode) builds K; kkm_iterate runs the loop body of Alg. 1 with one
-// process: scatter -> spmm_onehot -> assign per update, enqueued back to back
-// on the context's stream with no host round trip unless a stop test needs
-// one.  Argument checks run before any HIP call.
+// (resident and packed modes) builds K; kkm_iterate runs the loop body of
+// Alg. 1 with one process: scatter -> SpMM -> reduce -> assign per update,
+// enqueued back to back on the context's stream with no host round trip
+// unless a stop test needs one.  Argument checks run before any HIP call.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -47,11 +47,12 @@ struct Sizes {
   int d_pad, nstripes;
 };
 
-Sizes sizes_for(int64_t n, int32_t d) {
+// Packed K keeps whole column tiles, so its rows run to n_pad.
+Sizes sizes_for(int64_t n, int32_t d, int mode) {
   Sizes s;
   s.n = n;
   s.n_pad = round_up(n, kTile);
-  s.ld = round_up(n, 64);
+  s.ld = mode == KKM_MODE_PACKED ? s.n_pad : round_up(n, 64);
   s.d_pad = (int)round_up(d, kBK);
   s.nblk = (n + kBlk - 1) / kBlk;
   s.nstripes = (int)((s.ld + kStripe - 1) / kStripe);
@@ -61,16 +62,29 @@ Sizes sizes_for(int64_t n, int32_t d) {
 size_t staged_bytes(const Sizes& s) {
   return (size_t)s.n_pad * s.d_pad * 4 + (size_t)s.n_pad * 4 + (size_t)s.n * 4 + 64;
 }
-size_t k_bytes(const Sizes& s) { return (size_t)s.n * (size_t)s.ld * 4; }
-int64_t qmax_for(const Sizes& s, int k) { return (s.n + kChunk - 1) / kChunk + k; }
+size_t k_bytes(const Sizes& s, int mode) {
+  if (mode == KKM_MODE_PACKED) return (size_t)packed_floats(s.n, s.ld) * 4;
+  return mode == KKM_MODE_RESIDENT ? (size_t)s.n * (size_t)s.ld * 4 : 0;
+}
+int chunk_len_for(int mode) { return mode == KKM_MODE_PACKED ? kSymChunk : kChunk; }
+int64_t qmax_for(const Sizes& s, int k, int mode) {
+  const int64_t c = chunk_len_for(mode);
+  return (s.n + c - 1) / c + k;
+}
+int nseg_for(const Sizes& s) { return (int)((s.n_pad / kTile + kSymSeg - 1) / kSymSeg); }
 
 size_t ws_bytes(const Sizes& s, int k, int mode) {
-  const int64_t qmax = qmax_for(s, k);
+  const int64_t qmax = qmax_for(s, k, mode);
   size_t b = 0;
   b += (size_t)k * s.ld * 4;              // Et
-  if (mode == KKM_MODE_RESIDENT) {
+  if (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) {
     b += (size_t)qmax * s.ld * 4;         // P: chunk partials
-  } else {
+  }
+  if (mode == KKM_MODE_PACKED) {
+    b += (size_t)nseg_for(s) * k * s.n * 4;  // Ecp: column-side partials per segment
+    b += (size_t)k * s.n * 4;                // Ecol
+    b += (size_t)kTile * 4;                  // zero page
+  } else if (mode == KKM_MODE_ONTHEFLY) {
     b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
     b += (size_t)s.n_pad * 8;             // their norms and cluster ids
     b += (size_t)onthefly_segments(s.n) * k * s.ld * 4;  // row-side segment partials
@@ -263,14 +277,25 @@ int carve_ws(kkm_ctx* c, int k) {
   b.k = k;
   b.nblk = (int)s.nblk;
   b.nstripes = s.nstripes;
-  const int64_t qmax = qmax_for(s, k);
+  const int64_t qmax = qmax_for(s, k, c->mode);
   b.qmax = (int)qmax;
+  b.chunk_len = chunk_len_for(c->mode);
   b.diagK = c->diagK;
   b.trK = c->trK;
   b.Et = (float*)take((size_t)k * s.ld * 4);
-  if (c->mode == KKM_MODE_RESIDENT) {
+  if (c->mode == KKM_MODE_RESIDENT || c->mode == KKM_MODE_PACKED) {
     b.P = (float*)take((size_t)qmax * s.ld * 4);
-  } else {
+  }
+  if (c->mode == KKM_MODE_PACKED) {
+    b.nt = (int)(s.n_pad / kTile);
+    b.nseg = nseg_for(s);
+    b.Ecp = (float*)take((size_t)b.nseg * k * s.n * 4);
+    b.Ecol = (float*)take((size_t)k * s.n * 4);
+    float* zero = (float*)take((size_t)kTile * 4);
+    b.zero = zero;
+    rc = run(c, KKM_PHASE_OTHER, "zero page", [&] { return launch_zero_ints((int*)zero, kTile, c->stream); });
+    if (rc) return rc;
+  } else if (c->mode == KKM_MODE_ONTHEFLY) {
     c->Xs = (float*)take((size_t)s.n_pad * s.d_pad * 4);
     c->nrm_s = (float*)take((size_t)s.n_pad * 4);
     c->cs = (int*)take((size_t)s.n_pad * 4);
@@ -354,7 +379,14 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
   if (c->mode == KKM_MODE_RESIDENT) {
     if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
       return rc;
-    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
+    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, false, c->stream); })))
+      return rc;
+  } else if (c->mode == KKM_MODE_PACKED) {
+    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_sym", [&] { return launch_spmm_sym(c->K, b, cur, c->stream); })))
+      return rc;
+    if ((rc = run(c, KKM_PHASE_REDUCE, "ecol_sum", [&] { return launch_ecol_sum(b, c->stream); })))
+      return rc;
+    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, true, c->stream); })))
       return rc;
   } else {
     const Sizes& s = c->sz;
@@ -383,6 +415,9 @@ int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
   if (kkm_check_iterate_args(c->sz.n, k, max_iter) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  if (c->mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
+    return fail(c, KKM_ERR_ARG, "k=%d exceeds %d, the most the packed storage handles; build RESIDENT or ONTHEFLY",
+                k, KKM_PACKED_MAX_K);
   return KKM_OK;
 }
 
@@ -400,8 +435,8 @@ int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params* p
   if (kind != KKM_LINEAR && kind != KKM_POLY && kind != KKM_GAUSS)
     return fail(nullptr, KKM_ERR_ARG, "kind=%d is not LINEAR(0), POLY(1) or GAUSS(2)", kind);
   if (!p) return fail(nullptr, KKM_ERR_ARG, "params is NULL");
-  if (p->mode < KKM_MODE_AUTO || p->mode > KKM_MODE_ONTHEFLY)
-    return fail(nullptr, KKM_ERR_ARG, "mode=%d is not AUTO(0), RESIDENT(1) or ONTHEFLY(2)", p->mode);
+  if (p->mode < KKM_MODE_AUTO || p->mode > KKM_MODE_PACKED)
+    return fail(nullptr, KKM_ERR_ARG, "mode=%d is not AUTO(0), RESIDENT(1), ONTHEFLY(2) or PACKED(3)", p->mode);
   if (kind == KKM_POLY) {
     if (!(std::isfinite(p->gamma) && std::isfinite(p->coef0)))
       return fail(nullptr, KKM_ERR_ARG, "polynomial gamma and coef0 must be finite");
@@ -425,19 +460,23 @@ int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t request
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
     return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
   if (k < 1 || k > KKM_MAX_K || (int64_t)k > n) return fail(nullptr, KKM_ERR_ARG, "bad k=%d", k);
-  if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_ONTHEFLY)
+  if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_PACKED)
     return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
-  const Sizes s = sizes_for(n, d);
-  const size_t resident = staged_bytes(s) + ws_bytes(s, k, KKM_MODE_RESIDENT) + 4096 + k_bytes(s);
-  const size_t onthefly = staged_bytes(s) + ws_bytes(s, k, KKM_MODE_ONTHEFLY) + 4096;
+  if (requested_mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
+    return fail(nullptr, KKM_ERR_ARG, "packed storage handles k <= %d, not %d", KKM_PACKED_MAX_K, k);
+  auto need_for = [&](int m) {
+    const Sizes s = sizes_for(n, d, m);
+    return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m);
+  };
   int mode = requested_mode;
-  if (mode == KKM_MODE_AUTO) mode = resident <= mem_budget ? KKM_MODE_RESIDENT : KKM_MODE_ONTHEFLY;
-  const size_t need = mode == KKM_MODE_RESIDENT ? resident : onthefly;
+  if (mode == KKM_MODE_AUTO)
+    mode = need_for(KKM_MODE_RESIDENT) <= mem_budget ? KKM_MODE_RESIDENT : KKM_MODE_ONTHEFLY;
+  const size_t need = need_for(mode);
   if (mode_out) *mode_out = mode;
   if (bytes_out) *bytes_out = need;
+  static const char* names[] = {"auto", "resident", "on-the-fly", "packed"};
   if (need > mem_budget)
-    return fail(nullptr, KKM_ERR_OOM, "%s mode needs %zu bytes, budget %zu",
-                mode == KKM_MODE_RESIDENT ? "resident" : "on-the-fly", need, mem_budget);
+    return fail(nullptr, KKM_ERR_OOM, "%s mode needs %zu bytes, budget %zu", names[mode], need, mem_budget);
   return KKM_OK;
 }
 
@@ -492,7 +531,7 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind;
   if (!reuse) free_build(c);
 
-  c->sz = sizes_for(n, d);
+  c->sz = sizes_for(n, d, mode);
   c->d = d;
   c->kind = kind;
   c->mode = mode;
@@ -517,11 +556,12 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     if ((rc = dalloc(c, &p, 64, c->build_allocs, "trace"))) return rc;
     c->trK = (double*)p;
     c->maxnrm = (unsigned*)((char*)p + 8);
-    if (mode == KKM_MODE_RESIDENT) {
-      if ((rc = dalloc(c, &p, k_bytes(s), c->build_allocs, "kernel matrix K"))) return rc;
+    const bool stores_k = mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED;
+    if (stores_k) {
+      if ((rc = dalloc(c, &p, k_bytes(s, mode), c->build_allocs, "kernel matrix K"))) return rc;
       c->K = (float*)p;
     }
-    if (kind == KKM_GAUSS && mode == KKM_MODE_RESIDENT) {
+    if (kind == KKM_GAUSS && stores_k) {
       const long long upper = (long long)(n * (n - 1) / 2);
       long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
       const size_t room = c->budget > c->held ? c->budget - c->held : 0;
@@ -553,14 +593,15 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
   }
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
-         return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, kp, c->K, c->diagK,
-                                  c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->stream);
+         return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, kp,
+                                  c->K, c->diagK, c->fix_list, c->fix_count, c->fix_cap / kFixSegs,
+                                  c->stream);
        })))
     return rc;
   if (kind == KKM_GAUSS &&
       (rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
-         return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, kp, c->fix_list, c->fix_count,
-                                   c->fix_cap / kFixSegs, c->K, c->stream);
+         return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, kp,
+                                   c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream);
        })))
     return rc;
   return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
@@ -651,6 +692,14 @@ int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
     HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
     return KKM_OK;
   }
+  if (c->mode == KKM_MODE_PACKED) {
+    int rc = run(c, KKM_PHASE_OTHER, "packed_rows", [&] {
+      return launch_packed_rows(c->K, c->sz.n, c->sz.ld, r0, r1, out, c->stream);
+    });
+    if (rc) return rc;
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    return KKM_OK;
+  }
   const size_t row = (size_t)c->sz.n * 4;
   HIP_TRY(c, hipMemcpy2DAsync(out, row, c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, row, (size_t)(r1 - r0),
                               hipMemcpyDeviceToDevice, c->stream), "copy rows");
@@ -692,7 +741,7 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   out->kind = c->kind;
   out->mode = c->mode;
   out->ld = c->sz.ld;
-  out->bytes_K = c->mode == KKM_MODE_RESIDENT ? k_bytes(c->sz) : 0;
+  out->bytes_K = k_bytes(c->sz, c->mode);
   out->bytes_total = c->held;
   if (c->fixups < 0) {
     unsigned long long cnt[kFixSegs] = {0};

@@ -22,6 +22,26 @@ constexpr int kChunk = 1024;
 // Points per workgroup in the label/assign/scatter kernels.
 constexpr int kBlk = 256;
 
+// Packed (upper block triangle) SpMM: a workgroup takes a chunk of at most
+// kSymChunk sorted rows of one cluster (one 16-row MFMA group per wavefront)
+// and a segment of kSymSeg column tiles.  kSymMaxK bounds the one-hot MFMA
+// label blocks (16 labels each) a wavefront carries.
+constexpr int kSymChunk = 64;
+constexpr int kSymSeg = 8;
+constexpr int kSymMaxK = 64;
+
+// Packed layout: row block I (rows I*kTile ..) stores columns I*kTile ..
+// ld-1 row-major with stride ld - I*kTile.  packed_row(i) is the offset of
+// the (unstored when I > 0) element (i, 0), so that (i, j) for
+// j >= kTile*(i/kTile) lives at packed_row(i) + j.
+__host__ __device__ inline int64_t packed_row(int64_t i, int64_t ld) {
+  const int64_t I = i / kTile, c0 = I * kTile;
+  return kTile * (I * ld - (int64_t)kTile * I * (I - 1) / 2) + (i - c0) * (ld - c0) - c0;
+}
+// Floats held by the packed K of n rows (ld a multiple of kTile): the last
+// stored element is (n-1, ld-1).
+inline int64_t packed_floats(int64_t n, int64_t ld) { return packed_row(n - 1, ld) + ld; }
+
 // The Gaussian fix-up list is split into kFixSegs segments with a counter
 // each; workgroup b appends to segment b % kFixSegs, so no single atomic
 // counter serialises the K build.
@@ -43,6 +63,7 @@ struct KappaParams {
 struct IterBufs {
   int64_t n, ld;
   int k, nblk, nstripes, qmax;
+  int chunk_len;        // rows per SpMM chunk: kChunk, or kSymChunk when K is packed
   const float* diagK;   // n
   const double* trK;    // 1
   float* Et;            // k x ld: E transposed, E(i,j) at Et[j*ld + i]
@@ -59,20 +80,26 @@ struct IterBufs {
   int* perm;            // n: sorted position -> point
   int* pos;             // n: point -> sorted position
   int* status;          // 1: bit 0 = id out of range
+  // packed K only
+  int nt, nseg;         // column tiles (ld / kTile); column segments of kSymSeg tiles
+  float* Ecp;           // nseg x k x n: column-side partials per segment, sorted positions
+  float* Ecol;          // k x n: column-side sums, sorted positions
+  const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
 };
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
                         float* nrm, unsigned* maxnrm_bits, hipStream_t s);
+// packed: store only tiles I <= J, at packed_row(i) + j (no mirror).
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                             int64_t n, int d_pad, int64_t ld, const KappaParams& kp, float* K,
-                             float* diagK, int2* fix_list, unsigned long long* fix_count,
+                             int64_t n, int d_pad, int64_t ld, bool packed, const KappaParams& kp,
+                             float* K, float* diagK, int2* fix_list, unsigned long long* fix_count,
                              long long seg_cap, hipStream_t s);
 // Recomputes the listed Gaussian entries (counts read on the device); if a
 // segment received more entries than it holds, re-tests the whole triangle.
 // fix_list holds kFixSegs segments of seg_cap entries; fix_count kFixSegs counters.
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                              const KappaParams& kp, const int2* fix_list,
+                              bool packed, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, float* K,
                               hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
@@ -89,7 +116,15 @@ hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, cons
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s);
 hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
-hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
+// packed: P from chunk partials with columns left of a chunk's first tile
+// skipped, plus the column-side sums Ecol (read at pos[i]).
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, bool packed, hipStream_t s);
+
+// packed K (upper block triangle)
+hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hipStream_t s);
+hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
+hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,
+                              float* out, hipStream_t s);
 hipError_t launch_et_to_e(const IterBufs& b, const int* counts, const int* pos, float* E,
                           hipStream_t s);
 

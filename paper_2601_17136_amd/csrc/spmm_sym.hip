@@ -1,0 +1,250 @@
+// One-hot SpMM over the packed (upper block triangle) K.
+//
+// E^T = V K (Eq. 4 in the E^T form of Section IV) with K symmetric and only
+// tiles I <= J stored: a stored entry K(r, c) belongs to both
+//   row side     E^T(cl(r), c) += K(r, c)   (every stored entry), and
+//   column side  E^T(cl(c), r) += K(r, c)   (entries right of r's diagonal tile),
+// so each stored byte is read once and serves two sums.  The rows are taken
+// in cluster-sorted chunks of at most kSymChunk rows (all in one cluster), so
+// the row side is a plain column sum over the chunk, as in the full-storage
+// SpMM.  The column side needs, for every row, its entries summed per label
+// of their column: a product with the one-hot matrix of the column labels,
+// which runs on the fp32 matrix cores (v_mfma_f32_16x16x4_f32, 16 labels per
+// block, exact: every product is 0 or the entry itself).
+//
+// Workgroup (chunk q, segment sg): 4 wavefronts, one 16-row group each, over
+// the column tiles of segment sg (kSymSeg tiles) that the chunk's rows store.
+// Per tile a wavefront
+//  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
+//    contiguous bytes per instruction, two tiles ahead of use;
+//  - adds the rows in registers (row side), combines the four wavefronts in
+//    LDS and writes the chunk's partial P[q] for the tile;
+//  - stages the block in LDS and reads it back in the MFMA operand layout
+//    (lane = row, k slot = column) for the column side.
+// The column-side sums of a row stay in the accumulators for the whole
+// segment and go to Ecp[sg] at sorted positions; ecol_sum_kernel adds the
+// segments and spmm_reduce_kernel adds them into E^T.  Fixed orders
+// throughout, so the result is bitwise reproducible.
+#include "kkm_internal.h"
+
+#include <algorithm>
+#include <climits>
+
+namespace kkm {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+namespace {
+
+template <int NB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
+    const float* __restrict__ Kp, IterBufs b, const int* __restrict__ cl, bool cl_vec) {
+  constexpr int NW = 4, R = kSymChunk;
+  static_assert(R == 16 * NW, "one 16-row group per wavefront");
+  const int nseg = b.nseg;
+  const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
+  if (q >= *b.nchunks) return;
+  const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
+  const int Js = sg * kSymSeg, Je = min(b.nt, Js + kSymSeg);
+  // Rows are in increasing index order within a chunk, so the first row has
+  // the smallest tile; a segment left of it holds nothing of this chunk.
+  if (b.perm[p0] / kTile >= Je) return;
+
+  __shared__ int rtile[R];
+  __shared__ int64_t roff[R];
+  __shared__ unsigned mskl[kSymSeg][NB][4][16];  // one-hot bits: [tile][label block][k slot][label]
+  __shared__ f4 tile[NW][16 * 32];                // per wavefront: 16 rows x 32 chunks of 16 B
+  __shared__ f4 red[2][NW][32];                   // row-side sums of the four wavefronts
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int li = lane & 15, lk = lane >> 4;   // MFMA layout: row li, k slot lk
+  const int h = lane >> 5, c32 = lane & 31;   // load layout: row 2g + h, columns 4*c32 .. +3
+  const int64_t ld = b.ld, n = b.n;
+
+  if (tid < R) {
+    if (tid < nr) {
+      const int r = b.perm[p0 + tid];
+      rtile[tid] = r / kTile;
+      roff[tid] = packed_row(r, ld);
+    } else {
+      rtile[tid] = INT_MAX;
+      roff[tid] = 0;
+    }
+  }
+  // One-hot bits for every tile of the segment: bit 4g+e of entry
+  // [tile][nb][lk][li] says whether column 16g + 4lk + e of the tile has
+  // label 16nb + li.  Columns at or past n have no label.  The ids are read
+  // 16 bytes at a time when their address allows it (cl_vec).
+  for (int t = tid; t < (Je - Js) * NB * 64; t += 256) {
+    const int bi = t / (NB * 64), rem = t % (NB * 64);
+    const int nb = rem >> 6, kk = (rem >> 4) & 3, lab = 16 * nb + (rem & 15);
+    const int64_t c0 = (int64_t)(Js + bi) * kTile + 4 * kk;
+    unsigned m = 0;
+    if (cl_vec && (int64_t)(Js + bi + 1) * kTile <= n) {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        const int4 v = *(const int4*)(cl + c0 + 16 * g);
+        m |= (unsigned)(v.x == lab) << (4 * g) | (unsigned)(v.y == lab) << (4 * g + 1) |
+             (unsigned)(v.z == lab) << (4 * g + 2) | (unsigned)(v.w == lab) << (4 * g + 3);
+      }
+    } else {
+      for (int g = 0; g < 8; ++g)
+        for (int e = 0; e < 4; ++e) {
+          const int64_t c = c0 + 16 * g + e;
+          if (c < n && cl[c] == lab) m |= 1u << (4 * g + e);
+        }
+    }
+    mskl[bi][nb][kk][rem & 15] = m;
+  }
+  __syncthreads();
+
+  const int I0 = rtile[0];
+  const int J_lo = max(Js, I0), J_hi = Je;
+  const int um = w * 16 + li;  // this lane's row in the MFMA layout
+  const int rt_m = rtile[um];
+  const int rt_first = rtile[w * 16], rt_last = rtile[min(w * 16 + 15, nr - 1)];
+  f4 D[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
+  f4 b0[8], b1[8];
+  f4* tw = tile[w];
+
+  // Rows not stored in tile J (their diagonal tile is further right), rows
+  // past the chunk and tiles past the segment read the zero page instead.
+  auto load = [&](f4(&buf)[8], int J) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int u = w * 16 + 2 * g + h;
+      const bool on = rtile[u] <= J && J < J_hi;
+      const float* rp = on ? Kp + roff[u] + (int64_t)J * kTile + 4 * c32 : b.zero + 4 * c32;
+      buf[g] = __builtin_nontemporal_load((const f4*)rp);
+    }
+  };
+
+  auto step = [&](f4(&buf)[8], int J, int par) {
+    // row side: this lane's 4 columns over its 8 rows, then the other half-wave's 8
+    f4 rs = buf[0];
+#pragma unroll
+    for (int g = 1; g < 8; ++g) rs += buf[g];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rs[e] += __shfl_xor(rs[e], 32, 64);
+    // stage the 16 x 128 block; chunk index xor row keeps both access patterns conflict-free
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int r = 2 * g + h;
+      tw[r * 32 + (c32 ^ r)] = buf[g];
+    }
+    // the buffer is free again: fetch the tile two ahead into it (kept after
+    // the staging stores so that no third buffer is needed)
+    __builtin_amdgcn_sched_barrier(0);
+    load(buf, J + 2);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // column side: entries right of the row's own diagonal tile
+    const int bi = J - Js;
+    unsigned msk[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) msk[nb] = mskl[bi][nb][lk][li];
+    const bool diag = rt_first <= J && J <= rt_last;  // some row of the group sits in tile J
+    const bool dz = rt_m >= J;
+    if (rt_first < J || diag) {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        f4 v = tw[li * 32 + ((4 * g + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
+        if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
+          }
+      }
+    }
+
+    // row side across the four wavefronts -> P[q], columns of tile J
+    if (h == 0) red[par][w][c32] = rs;
+    __syncthreads();
+    if (tid < kTile) {
+      const float* rr = (const float*)red[par];
+      float t = rr[tid];
+#pragma unroll
+      for (int ww = 1; ww < NW; ++ww) t += rr[ww * kTile + tid];
+      b.P[(int64_t)q * ld + (int64_t)J * kTile + tid] = t;
+    }
+  };
+
+  load(b0, J_lo);
+  load(b1, J_lo + 1);
+  for (int J = J_lo; J < J_hi; J += 2) {
+    step(b0, J, 0);
+    if (J + 1 < J_hi) step(b1, J + 1, 1);
+  }
+
+  // D[nb][r]: label 16nb + 4lk + r of row um
+  if (um < nr)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int lab = 16 * nb + 4 * lk + r;
+        if (lab < b.k) b.Ecp[((int64_t)sg * b.k + lab) * n + p0 + um] = D[nb][r];
+      }
+}
+
+// Ecol[j][p] = sum over the segments that hold row p's stored columns, in order.
+__global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
+  const int q = blockIdx.x;
+  if (q >= *b.nchunks) return;
+  const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
+  const int s0 = (b.perm[p0] / kTile) / kSymSeg;
+  for (int t = threadIdx.x; t < b.k * nr; t += 256) {
+    const int j = t / nr, u = t % nr;
+    float acc = 0.f;
+    for (int sg = s0; sg < b.nseg; ++sg) acc += b.Ecp[((int64_t)sg * b.k + j) * b.n + p0 + u];
+    b.Ecol[(int64_t)j * b.n + p0 + u] = acc;
+  }
+}
+
+// Rows r0 .. r1-1 of the full K from the packed triangle.
+__global__ __launch_bounds__(256) void packed_rows_kernel(const float* __restrict__ Kp, int64_t n,
+                                                          int64_t ld, int64_t r0, int64_t r1,
+                                                          float* __restrict__ out) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= n) return;
+  for (int64_t r = r0 + blockIdx.y; r < r1; r += gridDim.y) {
+    const int64_t c0 = (r / kTile) * kTile;
+    out[(r - r0) * n + c] = c >= c0 ? Kp[packed_row(r, ld) + c] : Kp[packed_row(c, ld) + r];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hipStream_t s) {
+  const unsigned grid = (unsigned)((int64_t)b.qmax * b.nseg);
+  const int nb = (b.k + 15) / 16;
+  const bool v = ((uintptr_t)cl & 15) == 0;
+  switch (nb) {
+    case 1: hipLaunchKernelGGL(spmm_sym_kernel<1>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
+    case 2: hipLaunchKernelGGL(spmm_sym_kernel<2>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
+    case 3: hipLaunchKernelGGL(spmm_sym_kernel<3>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
+    case 4: hipLaunchKernelGGL(spmm_sym_kernel<4>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
+    default: return hipErrorInvalidValue;  // k > kSymMaxK is rejected before launch
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s) {
+  hipLaunchKernelGGL(ecol_sum_kernel, dim3((unsigned)b.qmax), dim3(256), 0, s, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,
+                              float* out, hipStream_t s) {
+  const unsigned gy = (unsigned)std::min<int64_t>(r1 - r0, 65535);
+  hipLaunchKernelGGL(packed_rows_kernel, dim3((unsigned)((n + 255) / 256), gy), dim3(256), 0, s, Kp,
+                     n, ld, r0, r1, out);
+  return hipGetLastError();
+}
+
+}  // namespace kkm

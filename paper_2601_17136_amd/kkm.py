@@ -17,11 +17,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkkm.so")
 
 KKM_OK, KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP, KKM_ERR_STATE, KKM_ERR_DEVICE_DATA = 0, -1, -2, -3, -4, -5
 KKM_LINEAR, KKM_POLY, KKM_GAUSS = 0, 1, 2
-KKM_MODE_AUTO, KKM_MODE_RESIDENT, KKM_MODE_ONTHEFLY = 0, 1, 2
+KKM_MODE_AUTO, KKM_MODE_RESIDENT, KKM_MODE_ONTHEFLY, KKM_MODE_PACKED = 0, 1, 2, 3
 KKM_MAX_K = 1024
+KKM_PACKED_MAX_K = 64
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other")
 KINDS = {"linear": KKM_LINEAR, "poly": KKM_POLY, "gauss": KKM_GAUSS}
-MODES = {"auto": KKM_MODE_AUTO, "resident": KKM_MODE_RESIDENT, "onthefly": KKM_MODE_ONTHEFLY}
+MODES = {"auto": KKM_MODE_AUTO, "resident": KKM_MODE_RESIDENT, "onthefly": KKM_MODE_ONTHEFLY,
+         "packed": KKM_MODE_PACKED}
 
 
 class KKMError(RuntimeError):

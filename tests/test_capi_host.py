@@ -105,6 +105,24 @@ def test_plan_falls_back_to_on_the_fly(L):
     assert mode == kkm.KKM_MODE_RESIDENT and need > 4 * n * n
 
 
+def test_plan_packed_holds_half_of_k(L):
+    """Packed storage: the upper block triangle (row block I keeps n_pad - 128 I
+    columns), i.e. n_pad (n_pad + 128) / 2 floats, and the 200000-point problem
+    that needs 160 GB resident fits in 100 GB."""
+    n, d, k = 200000, 54, 7
+    mode, need = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_PACKED)
+    n_pad = -(-n // 128) * 128
+    tri = 4 * n_pad * (n_pad + 128) // 2
+    assert mode == kkm.KKM_MODE_PACKED and tri <= need <= 1.06 * tri
+    _, need_res = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT)
+    assert need < 0.53 * need_res
+    with pytest.raises(kkm.KKMError) as e:          # more clusters than the packed SpMM handles
+        kkm.kkm_plan(n, d, kkm.KKM_PACKED_MAX_K + 1, 1 << 40, kkm.KKM_MODE_PACKED)
+    assert e.value.code == kkm.KKM_ERR_ARG
+    mode, _ = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO)   # AUTO never picks packed
+    assert mode == kkm.KKM_MODE_ONTHEFLY
+
+
 def test_plan_reports_oom(L):
     with pytest.raises(kkm.KKMError) as e:
         kkm.kkm_plan(200000, 54, 7, 100 << 30, kkm.KKM_MODE_RESIDENT)

@@ -37,6 +37,10 @@ CASES = {
     "n2-k2": (lambda: np.array([[0.0, 1.0], [2.0, -1.0]], np.float32), 2, "poly", 1.0, 1.0, 2, 17),
     "n1-k1": (lambda: np.array([[0.5]], np.float32), 1, "gauss", 1.0, 0.0, 1, 18),
     "stripes-n2100-k1": (lambda: datagen.make_points(3, n=2100, d=20)[0], 1, "poly", 0.1, 1.0, 2, 19),
+    # the largest cluster count (KKM_MAX_K); with n=3000 many clusters hold 1-5 points or none
+    "kmax1024-n3000": (lambda: datagen.make_points(5, n=3000, d=8)[0], 1024, "gauss", 0.125, 0.0, 1, 20),
+    # a wide point (d_pad = 2512, 157 k chunks)
+    "d2500-n300": (lambda: datagen.make_points(2, n=300, d=2500)[0], 6, "poly", 1.0 / 2500, 1.0, 3, 21),
 }
 
 
@@ -49,14 +53,16 @@ def _setup(name, oracle):
     return X, k, kind, g, c, p, cl, kern
 
 
-MODES = ["resident", "onthefly"]
+MODES = ["resident", "onthefly", "packed"]
+PACKED_MAX_K = 64
 
 
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("name", list(CASES))
 def test_kernel_matrix(oracle, name, mode):
-    """K (resident: the stored matrix; on the fly: rows from the same tile
-    kernel and epilogue the update sweep uses) against the oracle."""
+    """K (resident: the stored matrix; packed: the stored upper block triangle,
+    the rest read by symmetry; on the fly: rows from the same tile kernel and
+    epilogue the update sweep uses) against the oracle."""
     _torch_cuda()
     print(f"[gpu] K parity {name} {mode}", flush=True)
     X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
@@ -64,11 +70,12 @@ def test_kernel_matrix(oracle, name, mode):
         K = eng.K_rows()
         diag = eng.diag()
         info = eng.info()
-    assert info["mode"] == (1 if mode == "resident" else 2)
+    from paper_2601_17136_amd import kkm
+    assert info["mode"] == kkm.MODES[mode]
     Kref = kern.matrix(X)
     err = rowscaled_err(K, Kref)
     assert err <= TOL, f"K row-scaled error {err:.3e}"
-    if mode == "resident":
+    if mode in ("resident", "packed"):
         assert np.array_equal(K, K.T), "K is not exactly symmetric"
         np.testing.assert_array_equal(diag, np.diag(K))
     assert rel_err(diag, np.diag(Kref)) <= TOL
@@ -83,6 +90,13 @@ def test_step(oracle, name, mode):
     _torch_cuda()
     print(f"[gpu] step parity {name} {mode}", flush=True)
     X, k, kind, g, c, p, cl, kern = _setup(name, oracle)
+    if mode == "packed" and k > PACKED_MAX_K:
+        from paper_2601_17136_amd import kkm
+        with Engine(X, kind, g, c, p, mode=mode) as eng:
+            with pytest.raises(kkm.KKMError) as e:
+                eng.step(cl, k)
+        assert e.value.code == kkm.KKM_ERR_ARG and "packed" in str(e.value)
+        return
     ref = oracle.step_full(kern.matrix(X), cl, k)
     with Engine(X, kind, g, c, p, mode=mode) as eng:
         out = eng.step(cl, k)
@@ -207,12 +221,14 @@ def test_empty_cluster_and_ties(oracle, mode):
 
 @pytest.mark.parametrize("mode", MODES)
 def test_each_point_its_own_cluster(oracle, mode):
+    """k = n (packed: n = k = its largest k, four full label blocks)."""
     _torch_cuda()
-    X = datagen.make_points(2, n=70, d=9)[0]
+    n = PACKED_MAX_K if mode == "packed" else 70
+    X = datagen.make_points(2, n=n, d=9)[0]
     with Engine(X, "gauss", 0.2, mode=mode) as eng:
-        out = eng.step(np.arange(70, dtype=np.int32), 70)
-    assert abs(out["J"]) <= 1e-4 * 70
-    np.testing.assert_array_equal(out["cl"], np.arange(70))
+        out = eng.step(np.arange(n, dtype=np.int32), n)
+    assert abs(out["J"]) <= 1e-4 * n
+    np.testing.assert_array_equal(out["cl"], np.arange(n))
     assert np.all(np.abs(np.diag(out["D"])) <= 1e-5)
 
 
@@ -249,20 +265,39 @@ def test_bitwise_reproducible(oracle, mode):
     assert np.array_equal(i1[0], i2[0]) and np.array_equal(i1[2], i2[2])
 
 
-def test_gauss_fixup_overflow_path(oracle):
-    """With a memory budget that leaves room for only a few thousand fix-up
+@pytest.mark.parametrize("mode", ["resident", "packed"])
+def test_gauss_fixup_overflow_path(oracle, mode):
+    """With a memory budget that leaves room for only a few ten thousand fix-up
     list entries, more entries qualify than the list holds and the fix-up
-    re-tests the whole triangle; K must still match the oracle."""
+    re-tests the whole triangle; K must still match the oracle.  The points
+    are shifted by a common offset: the Gaussian K does not change, but the
+    norms grow, so the expansion loses digits on most pairs and nearly every
+    entry with a non-negligible value is listed."""
     _torch_cuda()
     from paper_2601_17136_amd import kkm
-    X = datagen.make_points(4, n=3000)[0]
-    _, need = kkm.kkm_plan(3000, X.shape[1], 1, 1 << 40, kkm.KKM_MODE_RESIDENT)
-    with Engine(X, "gauss", 0.5, mem_budget=need + 4096) as eng:
+    X = datagen.make_points(4, n=3000)[0] + np.float32(30.0)
+    _, need = kkm.kkm_plan(3000, X.shape[1], 1, 1 << 40, kkm.MODES[mode])
+    with Engine(X, "gauss", 0.5, mode=mode, mem_budget=need + 4096) as eng:
         K = eng.K_rows()
         info = eng.info()
     assert info["fixups"] > info["fixup_capacity"] > 0, info
     err = rowscaled_err(K, oracle.Kernel("gauss", 0.5).matrix(X))
     assert err <= TOL, err
-    with Engine(X, "gauss", 0.5) as eng:
+    with Engine(X, "gauss", 0.5, mode=mode) as eng:
         K2 = eng.K_rows()
     assert rowscaled_err(K2, oracle.Kernel("gauss", 0.5).matrix(X)) <= TOL
+
+
+def test_packed_k_limit(oracle):
+    """Packed storage takes k <= 64 (four 16-label MFMA blocks); k = 65 is
+    refused before anything is enqueued, and the context stays usable."""
+    _torch_cuda()
+    from paper_2601_17136_amd import kkm
+    X = datagen.make_points(2, n=500, d=9)[0]
+    with Engine(X, "gauss", 0.2, mode="packed") as eng:
+        for k in (PACKED_MAX_K + 1, 1024):
+            with pytest.raises(kkm.KKMError) as e:
+                eng.iterate(datagen.random_init(500, k, 1), k, 2)
+            assert e.value.code == kkm.KKM_ERR_ARG
+        _, it, _ = eng.iterate(datagen.random_init(500, PACKED_MAX_K, 1), PACKED_MAX_K, 2)
+        assert it == 2

@@ -1,5 +1,6 @@
-"""GPU parity at the full workload sizes, in the launch configuration the
-benchmark times (resident K, the same build and update kernels).
+"""GPU parity at the full workload sizes, in the launch configurations the
+benchmark times (packed and resident K, K on the fly: the same build and
+update kernels).
 
 The oracle cannot form K at these sizes, so each check is on outputs it can
 compute one by one:
@@ -25,7 +26,8 @@ def _rows(n, seed):
     return np.unique(np.concatenate([fixed, extra]).astype(np.int64))
 
 
-@pytest.mark.parametrize("cfg,mode", [(2, "resident"), (3, "resident"), (4, "resident"),
+@pytest.mark.parametrize("cfg,mode", [(2, "packed"), (3, "packed"), (4, "packed"), (5, "packed"),
+                                      (2, "resident"), (3, "resident"), (4, "resident"),
                                       (5, "resident"), (5, "onthefly"), (2, "onthefly")])
 def test_workload_step_full_size(oracle, cfg, mode):
     torch = pytest.importorskip("torch")
@@ -37,7 +39,7 @@ def test_workload_step_full_size(oracle, cfg, mode):
     rows = _rows(n, cfg)
     with Engine(X, w.kind, w.gamma, w.coef0, w.degree, mode=mode) as eng:
         info = eng.info()
-        assert info["mode"] == (1 if mode == "resident" else 2)
+        assert info["mode"] == eng.kkm.MODES[mode]
         K_rows = np.stack([eng.K_rows(int(r), int(r) + 1)[0] for r in rows])
         diag = eng.diag()
         out = eng.step(cl, k)
@@ -63,7 +65,8 @@ def test_workload_step_full_size(oracle, cfg, mode):
           flush=True)
 
 
-@pytest.mark.parametrize("cfg,mode", [(2, "resident"), (4, "resident"), (2, "onthefly")])
+@pytest.mark.parametrize("cfg,mode", [(2, "packed"), (4, "packed"), (2, "resident"), (4, "resident"),
+                                      (2, "onthefly")])
 def test_workload_loop_properties(oracle, cfg, mode):
     torch = pytest.importorskip("torch")
     assert torch.cuda.is_available()
