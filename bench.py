@@ -9,7 +9,9 @@ its stream during the timed steps; the K-build and per-update roofline
 figures are derived from them.
 
 Default workload: n=20,000 points, d=784, k=10, Gaussian kernel gamma=1/784,
-30 updates, K resident (1.6 GB).  ``--config N`` picks another workload.
+30 updates, K stored packed (its upper block triangle, 0.81 GB; the default
+for k <= 16, else the full K).  ``--config N`` picks another workload and
+``--mode`` another storage.
 """
 import argparse
 import json
@@ -56,7 +58,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=2, help="workload 1-5 (default 2: n=20000, d=784)")
-    ap.add_argument("--mode", choices=["resident", "onthefly"], default="resident")
+    ap.add_argument("--mode", choices=["packed", "resident", "onthefly"], default=None,
+                    help="K storage (default: packed when k <= 16, else resident)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="oracle sample sized for about this much host time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -124,6 +127,10 @@ def main():
     from paper_2601_17136_amd import datagen, kkm
 
     w = datagen.WORKLOADS[args.config]
+    if args.mode is None:
+        # the packed SpMM's column side costs one MFMA per 16 labels per entry:
+        # below the HBM time for k <= 16, above it for larger k
+        args.mode = "packed" if w.k <= 16 else "resident"
     X, _ = datagen.make_points(args.config)
     cl0 = datagen.make_init(args.config, w.n, w.k)
     n, d, k = w.n, w.d, w.k
@@ -200,14 +207,19 @@ def main():
         out["update_ms"] = round(iter_ms / w.iters, 4)
         out["updates_per_s_loop"] = round(w.iters / (iter_ms * 1e-3), 2)
         out["phases_ms_one_step"] = {p: round(breakdown[p][0], 4) for p in kkm.PHASES if breakdown[p][1]}
-        if args.mode == "resident":
-            bytes_per = 4.0 * n * n                        # K streamed once per update
+        if args.mode in ("resident", "packed"):
+            # K streamed once per update: all of it, or its upper triangle
+            # n(n+1)/2 (what symmetry leaves to read; the stored diagonal
+            # tiles and column padding count against the kernel)
+            kname = "spmm_onehot" if args.mode == "resident" else "spmm_sym"
+            bytes_per = 4.0 * n * n if args.mode == "resident" else 2.0 * n * (n + 1)
             gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
-            out["roofline"] = {"kernel": "spmm_onehot", "bound": "hbm", "achieved": round(gbs, 1),
+            out["roofline"] = {"kernel": kname, "bound": "hbm", "achieved": round(gbs, 1),
                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                               "traffic": counted_traffic("spmm_onehot", args.config, args.mode),
+                               "traffic": counted_traffic(kname, args.config, args.mode),
                                "traffic_unit": "GB per launch (algorithmic %.4f)" % (bytes_per / 1e9),
-                               "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt}
+                               "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt,
+                               "stored_K_bytes": info["bytes_K"]}
         else:
             otf_ms, otf_cnt = avg("onthefly")
             otf_tf = flops / (otf_ms * 1e-3) / 1e12   # the symmetric half, per update

@@ -52,8 +52,18 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
     for (int j = tid; j < k; j += 256) {
       const int c = counts_in[j];
       double zs = 0.0;
-      if (c > 0)
-        for (int s = 0; s < b.nstripes; ++s) zs += b.zpart[(int64_t)j * b.nstripes + s];
+      if (c > 0) {
+        const double* zp = b.zpart + (int64_t)j * b.nzpart;
+        int s = 0;
+        for (; s + 8 <= b.nzpart; s += 8) {  // eight loads in flight, added in order
+          double v[8];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) v[x] = zp[s + x];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) zs += v[x];
+        }
+        for (; s < b.nzpart; ++s) zs += zp[s];
+      }
       const double z = c > 0 ? zs / ((double)c * (double)c) : 0.0;
       zd[j] = c > 0 ? zs / (double)c : 0.0;  // |L_j| z_j
       zf[j] = (float)z;
@@ -276,10 +286,7 @@ __global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restric
 
 // Workgroup (stripe, j): E^T(j, stripe) = sum of cluster j's chunk partials in
 // chunk order, and the stripe's share of sum_{i in L_j} E(i, j) (fp64) for z_j.
-// Packed K: a chunk wrote no partial left of its first row's tile, and the
-// column-side sums Ecol (sorted positions) are added last.
-__global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int* __restrict__ cl,
-                                                          bool packed) {
+__global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int* __restrict__ cl) {
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int j = (int)(blockIdx.x / (unsigned)ns);
@@ -291,14 +298,8 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int*
   const int64_t col = (int64_t)stripe * kStripe + tid * 4;
   double zs = 0.0;
   if (col < ld) {
-    f4 e = {0.f, 0.f, 0.f, 0.f};
-    for (int q = qa; q < qb; ++q)
-      if (!packed || col >= (int64_t)(b.perm[b.chunk_p0[q]] / kTile) * kTile)
-        e += *(const f4*)(b.P + (int64_t)q * ld + col);
-    if (packed)
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (col + c < b.n) e[c] += b.Ecol[(int64_t)j * b.n + b.pos[col + c]];
+    f4 e = *(const f4*)(b.P + (int64_t)qa * ld + col);
+    for (int q = qa + 1; q < qb; ++q) e += *(const f4*)(b.P + (int64_t)q * ld + col);
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -316,9 +317,8 @@ hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s) 
   return hipGetLastError();
 }
 
-hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, bool packed, hipStream_t s) {
-  hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl,
-                     packed);
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s) {
+  hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl);
   return hipGetLastError();
 }
 

@@ -66,12 +66,16 @@ size_t k_bytes(const Sizes& s, int mode) {
   if (mode == KKM_MODE_PACKED) return (size_t)packed_floats(s.n, s.ld) * 4;
   return mode == KKM_MODE_RESIDENT ? (size_t)s.n * (size_t)s.ld * 4 : 0;
 }
-int chunk_len_for(int mode) { return mode == KKM_MODE_PACKED ? kSymChunk : kChunk; }
+int chunk_len_for(const Sizes& s, int mode) { return mode == KKM_MODE_PACKED ? sym_chunk_for(s.n) : kChunk; }
 int64_t qmax_for(const Sizes& s, int k, int mode) {
-  const int64_t c = chunk_len_for(mode);
+  const int64_t c = chunk_len_for(s, mode);
   return (s.n + c - 1) / c + k;
 }
 int nseg_for(const Sizes& s) { return (int)((s.n_pad / kTile + kSymSeg - 1) / kSymSeg); }
+// self-term partials per cluster: one per stripe of the mode's reduction
+int nzpart_for(const Sizes& s, int mode) {
+  return mode == KKM_MODE_PACKED ? (int)((s.ld + kSymRedStripe - 1) / kSymRedStripe) : s.nstripes;
+}
 
 size_t ws_bytes(const Sizes& s, int k, int mode) {
   const int64_t qmax = qmax_for(s, k, mode);
@@ -83,6 +87,7 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
   if (mode == KKM_MODE_PACKED) {
     b += (size_t)nseg_for(s) * k * s.n * 4;  // Ecp: column-side partials per segment
     b += (size_t)k * s.n * 4;                // Ecol
+    b += (size_t)qmax * 4;                   // chunk start columns
     b += (size_t)kTile * 4;                  // zero page
   } else if (mode == KKM_MODE_ONTHEFLY) {
     b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
@@ -91,7 +96,7 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
     b += (size_t)onthefly_cpart_floats(s.n, k) * 4;      // column-side partials
     b += (size_t)(s.n_pad / kTile) * 16;                 // per-block tables
   }
-  b += (size_t)k * s.nstripes * 8;        // zpart
+  b += (size_t)k * nzpart_for(s, mode) * 8;  // zpart
   b += (size_t)2 * k * s.nblk * 4;        // hist, base
   b += (size_t)2 * (k + 1) * 4;           // off, qfirst
   b += (size_t)3 * qmax * 4 + 4;          // chunk table
@@ -277,9 +282,10 @@ int carve_ws(kkm_ctx* c, int k) {
   b.k = k;
   b.nblk = (int)s.nblk;
   b.nstripes = s.nstripes;
+  b.nzpart = nzpart_for(s, c->mode);
   const int64_t qmax = qmax_for(s, k, c->mode);
   b.qmax = (int)qmax;
-  b.chunk_len = chunk_len_for(c->mode);
+  b.chunk_len = chunk_len_for(s, c->mode);
   b.diagK = c->diagK;
   b.trK = c->trK;
   b.Et = (float*)take((size_t)k * s.ld * 4);
@@ -291,6 +297,7 @@ int carve_ws(kkm_ctx* c, int k) {
     b.nseg = nseg_for(s);
     b.Ecp = (float*)take((size_t)b.nseg * k * s.n * 4);
     b.Ecol = (float*)take((size_t)k * s.n * 4);
+    b.chunk_c0 = (int*)take((size_t)qmax * 4);
     float* zero = (float*)take((size_t)kTile * 4);
     b.zero = zero;
     rc = run(c, KKM_PHASE_OTHER, "zero page", [&] { return launch_zero_ints((int*)zero, kTile, c->stream); });
@@ -306,7 +313,7 @@ int carve_ws(kkm_ctx* c, int k) {
     c->otb.nruns = (int*)take(nt * 4);
     c->otb.cbase = (int64_t*)take(nt * 8);
   }
-  b.zpart = (double*)take((size_t)k * s.nstripes * 8);
+  b.zpart = (double*)take((size_t)k * b.nzpart * 8);
   b.hist = (int*)take((size_t)k * s.nblk * 4);
   b.base = (int*)take((size_t)k * s.nblk * 4);
   b.off = (int*)take((size_t)(k + 1) * 4);
@@ -379,14 +386,14 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
   if (c->mode == KKM_MODE_RESIDENT) {
     if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
       return rc;
-    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, false, c->stream); })))
+    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
       return rc;
   } else if (c->mode == KKM_MODE_PACKED) {
     if ((rc = run(c, KKM_PHASE_SPMM, "spmm_sym", [&] { return launch_spmm_sym(c->K, b, cur, c->stream); })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "ecol_sum", [&] { return launch_ecol_sum(b, c->stream); })))
       return rc;
-    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, true, c->stream); })))
+    if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce_sym", [&] { return launch_spmm_reduce_sym(b, cur, c->stream); })))
       return rc;
   } else {
     const Sizes& s = c->sz;

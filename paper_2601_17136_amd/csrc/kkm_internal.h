@@ -22,13 +22,18 @@ constexpr int kChunk = 1024;
 // Points per workgroup in the label/assign/scatter kernels.
 constexpr int kBlk = 256;
 
-// Packed (upper block triangle) SpMM: a workgroup takes a chunk of at most
-// kSymChunk sorted rows of one cluster (one 16-row MFMA group per wavefront)
-// and a segment of kSymSeg column tiles.  kSymMaxK bounds the one-hot MFMA
-// label blocks (16 labels each) a wavefront carries.
-constexpr int kSymChunk = 64;
+// Packed (upper block triangle) SpMM: a workgroup of W wavefronts takes a
+// chunk of at most 16 W sorted rows of one cluster (one 16-row MFMA group per
+// wavefront) and a segment of kSymSeg column tiles.  W = 4 up to
+// kSymSmallN points, W = 8 above: taller chunks halve the partial sums and
+// the workgroup prologues, shorter ones give small problems enough
+// workgroups to fill the GPU evenly.  kSymMaxK bounds the one-hot MFMA label
+// blocks (16 labels each) a wavefront carries.
+constexpr int64_t kSymSmallN = 40000;
+inline int sym_chunk_for(int64_t n) { return n <= kSymSmallN ? 64 : 128; }
 constexpr int kSymSeg = 8;
 constexpr int kSymMaxK = 64;
+constexpr int kSymRedStripe = 256;  // columns per workgroup of the packed reduction
 
 // Packed layout: row block I (rows I*kTile ..) stores columns I*kTile ..
 // ld-1 row-major with stride ld - I*kTile.  packed_row(i) is the offset of
@@ -63,12 +68,13 @@ struct KappaParams {
 struct IterBufs {
   int64_t n, ld;
   int k, nblk, nstripes, qmax;
-  int chunk_len;        // rows per SpMM chunk: kChunk, or kSymChunk when K is packed
+  int chunk_len;        // rows per SpMM chunk: kChunk, or sym_chunk_for(n) when K is packed
   const float* diagK;   // n
   const double* trK;    // 1
   float* Et;            // k x ld: E transposed, E(i,j) at Et[j*ld + i]
   float* P;             // qmax x ld: per-chunk partial row sums
-  double* zpart;        // k x nstripes partial self-term sums
+  double* zpart;        // k x nzpart partial self-term sums (one per reduce stripe)
+  int nzpart;
   int* hist;            // k x nblk per-block cluster counts (cluster-major)
   int* base;            // k x nblk sorted position of each block's first member
   int* off;             // k + 1 cluster offsets in the sorted order
@@ -84,6 +90,7 @@ struct IterBufs {
   int nt, nseg;         // column tiles (ld / kTile); column segments of kSymSeg tiles
   float* Ecp;           // nseg x k x n: column-side partials per segment, sorted positions
   float* Ecol;          // k x n: column-side sums, sorted positions
+  int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile start)
   const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
 };
 
@@ -116,13 +123,15 @@ hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, cons
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s);
 hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
-// packed: P from chunk partials with columns left of a chunk's first tile
-// skipped, plus the column-side sums Ecol (read at pos[i]).
-hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, bool packed, hipStream_t s);
+hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 
 // packed K (upper block triangle)
 hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
+// E^T from the chunk partials (each starting at its chunk's first stored
+// column) plus the column-side sums Ecol (read at pos[i]); zpart per
+// kSymRedStripe columns.
+hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,
                               float* out, hipStream_t s);
 hipError_t launch_et_to_e(const IterBufs& b, const int* counts, const int* pos, float* E,

@@ -5,20 +5,21 @@
 //   row side     E^T(cl(r), c) += K(r, c)   (every stored entry), and
 //   column side  E^T(cl(c), r) += K(r, c)   (entries right of r's diagonal tile),
 // so each stored byte is read once and serves two sums.  The rows are taken
-// in cluster-sorted chunks of at most kSymChunk rows (all in one cluster), so
+// in cluster-sorted chunks of at most 64 or 128 rows (all in one cluster), so
 // the row side is a plain column sum over the chunk, as in the full-storage
 // SpMM.  The column side needs, for every row, its entries summed per label
 // of their column: a product with the one-hot matrix of the column labels,
 // which runs on the fp32 matrix cores (v_mfma_f32_16x16x4_f32, 16 labels per
 // block, exact: every product is 0 or the entry itself).
 //
-// Workgroup (chunk q, segment sg): 4 wavefronts, one 16-row group each, over
-// the column tiles of segment sg (kSymSeg tiles) that the chunk's rows store.
+// Workgroup (chunk q, segment sg): NW wavefronts (4 or 8), one 16-row group
+// each, over the column tiles of segment sg (kSymSeg tiles) that the chunk's
+// rows store.
 // Per tile a wavefront
 //  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
 //    contiguous bytes per instruction, two tiles ahead of use;
-//  - adds the rows in registers (row side), combines the four wavefronts in
-//    LDS and writes the chunk's partial P[q] for the tile;
+//  - adds the rows in registers (row side), combines the wavefronts in LDS
+//    and writes the chunk's partial P[q] for the tile;
 //  - stages the block in LDS and reads it back in the MFMA operand layout
 //    (lane = row, k slot = column) for the column side.
 // The column-side sums of a row stay in the accumulators for the whole
@@ -36,11 +37,12 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
-template <int NB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
+// 16 wavefronts per CU: at most 128 VGPRs each, and 4 (NW = 4, ~39 KB of
+// LDS) or 2 (NW = 8, ~76 KB) workgroups.
+template <int NB, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const float* __restrict__ Kp, IterBufs b, const int* __restrict__ cl, bool cl_vec) {
-  constexpr int NW = 4, R = kSymChunk;
-  static_assert(R == 16 * NW, "one 16-row group per wavefront");
+  constexpr int R = 16 * NW, NT = 64 * NW;
   const int nseg = b.nseg;
   const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
   if (q >= *b.nchunks) return;
@@ -54,7 +56,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void s
   __shared__ int64_t roff[R];
   __shared__ unsigned mskl[kSymSeg][NB][4][16];  // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * 32];                // per wavefront: 16 rows x 32 chunks of 16 B
-  __shared__ f4 red[2][NW][32];                   // row-side sums of the four wavefronts
+  __shared__ f4 red[2][NW][32];                   // row-side sums of the wavefronts
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int li = lane & 15, lk = lane >> 4;   // MFMA layout: row li, k slot lk
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void s
   // [tile][nb][lk][li] says whether column 16g + 4lk + e of the tile has
   // label 16nb + li.  Columns at or past n have no label.  The ids are read
   // 16 bytes at a time when their address allows it (cl_vec).
-  for (int t = tid; t < (Je - Js) * NB * 64; t += 256) {
+  for (int t = tid; t < (Je - Js) * NB * 64; t += NT) {
     const int bi = t / (NB * 64), rem = t % (NB * 64);
     const int nb = rem >> 6, kk = (rem >> 4) & 3, lab = 16 * nb + (rem & 15);
     const int64_t c0 = (int64_t)(Js + bi) * kTile + 4 * kk;
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void s
       }
     }
 
-    // row side across the four wavefronts -> P[q], columns of tile J
+    // row side across the wavefronts -> P[q], columns of tile J
     if (h == 0) red[par][w][c32] = rs;
     __syncthreads();
     if (tid < kTile) {
@@ -192,18 +194,82 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void s
       }
 }
 
-// Ecol[j][p] = sum over the segments that hold row p's stored columns, in order.
+// Ecol[j][p] = sum over the segments that hold row p's stored columns, in
+// order; also the chunk's first stored column for the reduction.
 __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
   const int q = blockIdx.x;
   if (q >= *b.nchunks) return;
   const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
-  const int s0 = (b.perm[p0] / kTile) / kSymSeg;
+  const int I0 = b.perm[p0] / kTile;
+  if (threadIdx.x == 0) b.chunk_c0[q] = I0 * kTile;
+  const int s0 = I0 / kSymSeg;
+  const int64_t seg_stride = (int64_t)b.k * b.n;
   for (int t = threadIdx.x; t < b.k * nr; t += 256) {
     const int j = t / nr, u = t % nr;
+    const float* e = b.Ecp + (int64_t)j * b.n + p0 + u;
     float acc = 0.f;
-    for (int sg = s0; sg < b.nseg; ++sg) acc += b.Ecp[((int64_t)sg * b.k + j) * b.n + p0 + u];
+    int sg = s0;
+    for (; sg + 8 <= b.nseg; sg += 8) {  // eight loads in flight, added in order
+      float v[8];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) v[x] = e[(sg + x) * seg_stride];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) acc += v[x];
+    }
+    for (; sg < b.nseg; ++sg) acc += e[sg * seg_stride];
     b.Ecol[(int64_t)j * b.n + p0 + u] = acc;
   }
+}
+
+// Workgroup (stripe of kSymRedStripe columns, cluster j).  Cluster j's many
+// short chunks are split into four fixed quarters, one per wavefront, each
+// summed in chunk order (a chunk's partial starts at its first stored
+// column), and the quarters are added in order.  Then the column-side sums
+// of the stripe's rows, and the stripe's part of sum_{i in L_j} E(i, j).
+__global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const int* __restrict__ cl) {
+  const int ns = b.nzpart;
+  const int stripe = (int)(blockIdx.x % (unsigned)ns), j = (int)(blockIdx.x / (unsigned)ns);
+  const int qa = b.qfirst[j], qb = b.qfirst[j + 1];
+  if (qa == qb) return;  // empty cluster: E^T(j, .) and z_j are never read
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  __shared__ f4 part[4][64];
+  const int64_t ld = b.ld;
+  const int64_t col = (int64_t)stripe * kSymRedStripe + 4 * lane;
+  const int per = (qb - qa + 3) / 4;
+  const int q0 = qa + w * per, q1 = min(qb, q0 + per);
+  f4 e = {0.f, 0.f, 0.f, 0.f};
+  if (col < ld) {
+    int q = q0;
+    for (; q + 4 <= q1; q += 4) {
+      int c0[4];
+      f4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) c0[u] = b.chunk_c0[q + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = col >= c0[u] ? *(const f4*)(b.P + (int64_t)(q + u) * ld + col) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) e += v[u];
+    }
+    for (; q < q1; ++q)
+      if (col >= b.chunk_c0[q]) e += *(const f4*)(b.P + (int64_t)q * ld + col);
+  }
+  part[w][lane] = e;
+  __syncthreads();
+  if (w != 0) return;
+  double zs = 0.0;
+  if (col < ld) {
+    e = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (col + c < b.n) e[c] += b.Ecol[(int64_t)j * b.n + b.pos[col + c]];
+    *(f4*)(b.Et + (int64_t)j * ld + col) = e;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (col + c < b.n && cl[col + c] == j) zs += (double)e[c];
+  }
+  for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off, 64);
+  if (lane == 0) b.zpart[(int64_t)j * ns + stripe] = zs;
 }
 
 // Rows r0 .. r1-1 of the full K from the packed triangle.
@@ -224,18 +290,28 @@ hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hi
   const unsigned grid = (unsigned)((int64_t)b.qmax * b.nseg);
   const int nb = (b.k + 15) / 16;
   const bool v = ((uintptr_t)cl & 15) == 0;
+#define KKM_SYM_LAUNCH(NB, NW) \
+  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW>), dim3(grid), dim3(64 * NW), 0, s, Kp, b, cl, v)
+  if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
+  const bool tall = b.chunk_len == 128;
   switch (nb) {
-    case 1: hipLaunchKernelGGL(spmm_sym_kernel<1>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
-    case 2: hipLaunchKernelGGL(spmm_sym_kernel<2>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
-    case 3: hipLaunchKernelGGL(spmm_sym_kernel<3>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
-    case 4: hipLaunchKernelGGL(spmm_sym_kernel<4>, dim3(grid), dim3(256), 0, s, Kp, b, cl, v); break;
+    case 1: if (tall) KKM_SYM_LAUNCH(1, 8); else KKM_SYM_LAUNCH(1, 4); break;
+    case 2: if (tall) KKM_SYM_LAUNCH(2, 8); else KKM_SYM_LAUNCH(2, 4); break;
+    case 3: if (tall) KKM_SYM_LAUNCH(3, 8); else KKM_SYM_LAUNCH(3, 4); break;
+    case 4: if (tall) KKM_SYM_LAUNCH(4, 8); else KKM_SYM_LAUNCH(4, 4); break;
     default: return hipErrorInvalidValue;  // k > kSymMaxK is rejected before launch
   }
+#undef KKM_SYM_LAUNCH
   return hipGetLastError();
 }
 
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s) {
   hipLaunchKernelGGL(ecol_sum_kernel, dim3((unsigned)b.qmax), dim3(256), 0, s, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t s) {
+  hipLaunchKernelGGL(spmm_reduce_sym_kernel, dim3((unsigned)(b.nzpart * b.k)), dim3(256), 0, s, b, cl);
   return hipGetLastError();
 }
 
