@@ -234,6 +234,11 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
     for (int ww = 0; ww < w; ++ww) r += wc[ww * k + lab];
     b.perm[r] = (int)i;
     b.pos[i] = r;
+    // packed K: the first member of a chunk (members are in index order)
+    // fixes the chunk's first stored column
+    const int rel = r - offs[lab];
+    if (b.chunk_c0 && rel % b.chunk_len == 0)
+      b.chunk_c0[qf[lab] + rel / b.chunk_len] = (int)(i / kTile) * kTile;
   }
 }
 

@@ -71,7 +71,10 @@ int64_t qmax_for(const Sizes& s, int k, int mode) {
   const int64_t c = chunk_len_for(s, mode);
   return (s.n + c - 1) / c + k;
 }
-int nseg_for(const Sizes& s) { return (int)((s.n_pad / kTile + kSymSeg - 1) / kSymSeg); }
+int nseg_for(const Sizes& s, int k) {
+  const int bseg = sym_seg_for(s.n, k);
+  return (int)((s.n_pad / kTile + bseg - 1) / bseg);
+}
 // self-term partials per cluster: one per stripe of the mode's reduction
 int nzpart_for(const Sizes& s, int mode) {
   return mode == KKM_MODE_PACKED ? (int)((s.ld + kSymRedStripe - 1) / kSymRedStripe) : s.nstripes;
@@ -85,7 +88,7 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
     b += (size_t)qmax * s.ld * 4;         // P: chunk partials
   }
   if (mode == KKM_MODE_PACKED) {
-    b += (size_t)nseg_for(s) * k * s.n * 4;  // Ecp: column-side partials per segment
+    b += (size_t)nseg_for(s, k) * k * s.n * 4;  // Ecp: column-side partials per segment
     b += (size_t)k * s.n * 4;                // Ecol
     b += (size_t)qmax * 4;                   // chunk start columns
     b += (size_t)kTile * 4;                  // zero page
@@ -294,7 +297,8 @@ int carve_ws(kkm_ctx* c, int k) {
   }
   if (c->mode == KKM_MODE_PACKED) {
     b.nt = (int)(s.n_pad / kTile);
-    b.nseg = nseg_for(s);
+    b.bseg = sym_seg_for(s.n, k);
+    b.nseg = nseg_for(s, k);
     b.Ecp = (float*)take((size_t)b.nseg * k * s.n * 4);
     b.Ecol = (float*)take((size_t)k * s.n * 4);
     b.chunk_c0 = (int*)take((size_t)qmax * 4);

@@ -24,14 +24,15 @@ constexpr int kBlk = 256;
 
 // Packed (upper block triangle) SpMM: a workgroup of W wavefronts takes a
 // chunk of at most 16 W sorted rows of one cluster (one 16-row MFMA group per
-// wavefront) and a segment of kSymSeg column tiles.  W = 4 up to
-// kSymSmallN points, W = 8 above: taller chunks halve the partial sums and
-// the workgroup prologues, shorter ones give small problems enough
-// workgroups to fill the GPU evenly.  kSymMaxK bounds the one-hot MFMA label
-// blocks (16 labels each) a wavefront carries.
+// wavefront) and a segment of S column tiles.  Up to kSymSmallN points,
+// W = 4 and S = 8: small problems need many workgroups to fill the GPU
+// evenly.  Above, W = 8 and (for k <= 16) S = 16: taller chunks halve the
+// partial sums, and longer segments spread each workgroup's start (row
+// addresses far apart in a K of tens of GB) over more tiles.  kSymMaxK
+// bounds the one-hot MFMA label blocks (16 labels each) a wavefront carries.
 constexpr int64_t kSymSmallN = 40000;
 inline int sym_chunk_for(int64_t n) { return n <= kSymSmallN ? 64 : 128; }
-constexpr int kSymSeg = 8;
+inline int sym_seg_for(int64_t n, int k) { return n > kSymSmallN && k <= 16 ? 16 : 8; }
 constexpr int kSymMaxK = 64;
 constexpr int kSymRedStripe = 256;  // columns per workgroup of the packed reduction
 
@@ -87,10 +88,11 @@ struct IterBufs {
   int* pos;             // n: point -> sorted position
   int* status;          // 1: bit 0 = id out of range
   // packed K only
-  int nt, nseg;         // column tiles (ld / kTile); column segments of kSymSeg tiles
+  int nt, nseg, bseg;   // column tiles (ld / kTile); column segments of bseg tiles
   float* Ecp;           // nseg x k x n: column-side partials per segment, sorted positions
   float* Ecol;          // k x n: column-side sums, sorted positions
-  int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile start)
+  int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
+                        // start), written by the scatter; null when K is not packed
   const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
 };
 

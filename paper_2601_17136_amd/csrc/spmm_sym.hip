@@ -13,7 +13,7 @@
 // block, exact: every product is 0 or the entry itself).
 //
 // Workgroup (chunk q, segment sg): NW wavefronts (4 or 8), one 16-row group
-// each, over the column tiles of segment sg (kSymSeg tiles) that the chunk's
+// each, over the column tiles of segment sg (BSEG tiles) that the chunk's
 // rows store.
 // Per tile a wavefront
 //  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
@@ -39,7 +39,7 @@ namespace {
 
 // 16 wavefronts per CU: at most 128 VGPRs each, and 4 (NW = 4, ~39 KB of
 // LDS) or 2 (NW = 8, ~76 KB) workgroups.
-template <int NB, int NW>
+template <int NB, int NW, int BSEG>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const float* __restrict__ Kp, IterBufs b, const int* __restrict__ cl, bool cl_vec) {
   constexpr int R = 16 * NW, NT = 64 * NW;
@@ -47,14 +47,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
   if (q >= *b.nchunks) return;
   const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
-  const int Js = sg * kSymSeg, Je = min(b.nt, Js + kSymSeg);
+  const int Js = sg * BSEG, Je = min(b.nt, Js + BSEG);
   // Rows are in increasing index order within a chunk, so the first row has
   // the smallest tile; a segment left of it holds nothing of this chunk.
-  if (b.perm[p0] / kTile >= Je) return;
+  if (b.chunk_c0[q] >= Je * kTile) return;
 
   __shared__ int rtile[R];
   __shared__ int64_t roff[R];
-  __shared__ unsigned mskl[kSymSeg][NB][4][16];  // one-hot bits: [tile][label block][k slot][label]
+  __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * 32];                // per wavefront: 16 rows x 32 chunks of 16 B
   __shared__ f4 red[2][NW][32];                   // row-side sums of the wavefronts
 
@@ -194,15 +194,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       }
 }
 
-// Ecol[j][p] = sum over the segments that hold row p's stored columns, in
-// order; also the chunk's first stored column for the reduction.
+// Ecol[j][p] = sum over the segments that hold row p's stored columns, in order.
 __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
   const int q = blockIdx.x;
   if (q >= *b.nchunks) return;
   const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
-  const int I0 = b.perm[p0] / kTile;
-  if (threadIdx.x == 0) b.chunk_c0[q] = I0 * kTile;
-  const int s0 = I0 / kSymSeg;
+  const int s0 = b.chunk_c0[q] / kTile / b.bseg;
   const int64_t seg_stride = (int64_t)b.k * b.n;
   for (int t = threadIdx.x; t < b.k * nr; t += 256) {
     const int j = t / nr, u = t % nr;
@@ -290,15 +287,20 @@ hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hi
   const unsigned grid = (unsigned)((int64_t)b.qmax * b.nseg);
   const int nb = (b.k + 15) / 16;
   const bool v = ((uintptr_t)cl & 15) == 0;
-#define KKM_SYM_LAUNCH(NB, NW) \
-  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW>), dim3(grid), dim3(64 * NW), 0, s, Kp, b, cl, v)
+#define KKM_SYM_LAUNCH(NB, NW, S) \
+  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S>), dim3(grid), dim3(64 * NW), 0, s, Kp, b, cl, v)
   if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
+  if (b.bseg != 8 && !(b.bseg == 16 && nb == 1 && b.chunk_len == 128)) return hipErrorInvalidValue;
   const bool tall = b.chunk_len == 128;
   switch (nb) {
-    case 1: if (tall) KKM_SYM_LAUNCH(1, 8); else KKM_SYM_LAUNCH(1, 4); break;
-    case 2: if (tall) KKM_SYM_LAUNCH(2, 8); else KKM_SYM_LAUNCH(2, 4); break;
-    case 3: if (tall) KKM_SYM_LAUNCH(3, 8); else KKM_SYM_LAUNCH(3, 4); break;
-    case 4: if (tall) KKM_SYM_LAUNCH(4, 8); else KKM_SYM_LAUNCH(4, 4); break;
+    case 1:
+      if (b.bseg == 16) KKM_SYM_LAUNCH(1, 8, 16);
+      else if (tall) KKM_SYM_LAUNCH(1, 8, 8);
+      else KKM_SYM_LAUNCH(1, 4, 8);
+      break;
+    case 2: if (tall) KKM_SYM_LAUNCH(2, 8, 8); else KKM_SYM_LAUNCH(2, 4, 8); break;
+    case 3: if (tall) KKM_SYM_LAUNCH(3, 8, 8); else KKM_SYM_LAUNCH(3, 4, 8); break;
+    case 4: if (tall) KKM_SYM_LAUNCH(4, 8, 8); else KKM_SYM_LAUNCH(4, 4, 8); break;
     default: return hipErrorInvalidValue;  // k > kSymMaxK is rejected before launch
   }
 #undef KKM_SYM_LAUNCH
