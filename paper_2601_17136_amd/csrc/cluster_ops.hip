@@ -49,20 +49,32 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
 
   for (int j = tid; j < k; j += 256) hist[j] = 0;
   if (MODE == 1) {
+    // sum_{i in L_j} E(i, j) from the reduction's nzpart parts: for k <= 256,
+    // 256/k threads per cluster each add a fixed run of parts, and the runs
+    // are added in order (a short latency chain instead of nzpart loads)
+    __shared__ double zrun[256];
+    const int G = k <= 256 ? 256 / k : 1;
+    if (k <= 256) {
+      const int j = tid / G, g = tid % G;
+      double s = 0.0;
+      if (j < k) {
+        const int per = (b.nzpart + G - 1) / G, lo = g * per, hi = min(b.nzpart, lo + per);
+        const double* zp = b.zpart + (int64_t)j * b.nzpart;
+        for (int x = lo; x < hi; ++x) s += zp[x];
+      }
+      zrun[tid] = s;
+      __syncthreads();
+    }
     for (int j = tid; j < k; j += 256) {
       const int c = counts_in[j];
       double zs = 0.0;
       if (c > 0) {
-        const double* zp = b.zpart + (int64_t)j * b.nzpart;
-        int s = 0;
-        for (; s + 8 <= b.nzpart; s += 8) {  // eight loads in flight, added in order
-          double v[8];
-#pragma unroll
-          for (int x = 0; x < 8; ++x) v[x] = zp[s + x];
-#pragma unroll
-          for (int x = 0; x < 8; ++x) zs += v[x];
+        if (k <= 256) {
+          for (int g = 0; g < G; ++g) zs += zrun[j * G + g];
+        } else {
+          const double* zp = b.zpart + (int64_t)j * b.nzpart;
+          for (int s = 0; s < b.nzpart; ++s) zs += zp[s];
         }
-        for (; s < b.nzpart; ++s) zs += zp[s];
       }
       const double z = c > 0 ? zs / ((double)c * (double)c) : 0.0;
       zd[j] = c > 0 ? zs / (double)c : 0.0;  // |L_j| z_j

@@ -194,28 +194,32 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       }
 }
 
-// Ecol[j][p] = sum over the segments that hold row p's stored columns, in order.
+// Ecol[j][p] = sum over the segments that hold row p's stored columns, in
+// order.  One output per thread: (chunk, label, row) over ecol_wgs(b)
+// workgroups per chunk.
+__device__ __host__ inline int ecol_wgs(const IterBufs& b) { return (b.k * b.chunk_len + 255) / 256; }
 __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
-  const int q = blockIdx.x;
+  const int per = ecol_wgs(b);
+  const int q = (int)(blockIdx.x / (unsigned)per), part = (int)(blockIdx.x % (unsigned)per);
   if (q >= *b.nchunks) return;
   const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
+  const int t = part * 256 + (int)threadIdx.x;
+  if (t >= b.k * nr) return;
+  const int j = t / nr, u = t % nr;
   const int s0 = b.chunk_c0[q] / kTile / b.bseg;
   const int64_t seg_stride = (int64_t)b.k * b.n;
-  for (int t = threadIdx.x; t < b.k * nr; t += 256) {
-    const int j = t / nr, u = t % nr;
-    const float* e = b.Ecp + (int64_t)j * b.n + p0 + u;
-    float acc = 0.f;
-    int sg = s0;
-    for (; sg + 8 <= b.nseg; sg += 8) {  // eight loads in flight, added in order
-      float v[8];
+  const float* e = b.Ecp + (int64_t)j * b.n + p0 + u;
+  float acc = 0.f;
+  int sg = s0;
+  for (; sg + 8 <= b.nseg; sg += 8) {  // eight loads in flight, added in order
+    float v[8];
 #pragma unroll
-      for (int x = 0; x < 8; ++x) v[x] = e[(sg + x) * seg_stride];
+    for (int x = 0; x < 8; ++x) v[x] = e[(sg + x) * seg_stride];
 #pragma unroll
-      for (int x = 0; x < 8; ++x) acc += v[x];
-    }
-    for (; sg < b.nseg; ++sg) acc += e[sg * seg_stride];
-    b.Ecol[(int64_t)j * b.n + p0 + u] = acc;
+    for (int x = 0; x < 8; ++x) acc += v[x];
   }
+  for (; sg < b.nseg; ++sg) acc += e[sg * seg_stride];
+  b.Ecol[(int64_t)j * b.n + p0 + u] = acc;
 }
 
 // Workgroup (stripe of kSymRedStripe columns, cluster j).  Cluster j's many
@@ -237,16 +241,16 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
   f4 e = {0.f, 0.f, 0.f, 0.f};
   if (col < ld) {
     int q = q0;
-    for (; q + 4 <= q1; q += 4) {
-      int c0[4];
-      f4 v[4];
+    for (; q + 8 <= q1; q += 8) {  // eight chunks in flight, added in order
+      int c0[8];
+      f4 v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) c0[u] = b.chunk_c0[q + u];
+      for (int u = 0; u < 8; ++u) c0[u] = b.chunk_c0[q + u];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
         v[u] = col >= c0[u] ? *(const f4*)(b.P + (int64_t)(q + u) * ld + col) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int u = 0; u < 4; ++u) e += v[u];
+      for (int u = 0; u < 8; ++u) e += v[u];
     }
     for (; q < q1; ++q)
       if (col >= b.chunk_c0[q]) e += *(const f4*)(b.P + (int64_t)q * ld + col);
@@ -308,7 +312,7 @@ hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hi
 }
 
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s) {
-  hipLaunchKernelGGL(ecol_sum_kernel, dim3((unsigned)b.qmax), dim3(256), 0, s, b);
+  hipLaunchKernelGGL(ecol_sum_kernel, dim3((unsigned)((int64_t)b.qmax * ecol_wgs(b))), dim3(256), 0, s, b);
   return hipGetLastError();
 }
 
