@@ -230,6 +230,8 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
   const int64_t i = (int64_t)blk * kBlk + tid;
   const bool valid = i < b.n;
   const int lab = valid ? clamp_id(cl[i], k) : -1;
+  int* labs = segsum + 256;  // this block's 256 ids (-1 past n), for the packed one-hot masks
+  labs[tid] = lab;
   int rank = 0;
   unsigned long long todo = __ballot(valid);
   while (todo) {
@@ -251,12 +253,31 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
     const int rel = r - offs[lab];
     if (b.chunk_c0 && rel % b.chunk_len == 0)
       b.chunk_c0[qf[lab] + rel / b.chunk_len] = (int)(i / kTile) * kTile;
+    if (b.roffp) b.roffp[r] = packed_row(i, b.ld);
+  }
+  // packed K: the one-hot bits of this block's two column tiles, once per
+  // update (the SpMM reads them instead of the ids)
+  if (b.mskg) {
+    const int per_tile = b.nlb * 64;
+    for (int t = tid; t < 2 * per_tile; t += 256) {
+      const int half = t / per_tile, rem = t % per_tile;
+      const int J = 2 * blk + half;
+      if ((int64_t)J * kTile >= b.n) continue;
+      const int nb = rem >> 6, kk = (rem >> 4) & 3, want = 16 * nb + (rem & 15);
+      const int* lt = labs + half * kTile + 4 * kk;
+      unsigned m = 0;
+#pragma unroll
+      for (int g = 0; g < 8; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m |= (unsigned)(lt[16 * g + e] == want) << (4 * g + e);
+      b.mskg[(int64_t)J * per_tile + rem] = m;
+    }
   }
 }
 
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s) {
-  const size_t sm = (size_t)(7 * b.k + 2 + 256) * sizeof(int);
+  const size_t sm = (size_t)(7 * b.k + 2 + 512) * sizeof(int);
   hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)b.nblk), dim3(256), sm, s, b, cl, counts,
                      zero_counts, zero_changed);
   return hipGetLastError();

@@ -91,6 +91,8 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
     b += (size_t)nseg_for(s, k) * k * s.n * 4;  // Ecp: column-side partials per segment
     b += (size_t)k * s.n * 4;                // Ecol
     b += (size_t)qmax * 4;                   // chunk start columns
+    b += (size_t)s.n * 8;                    // packed row offsets at sorted positions
+    b += (size_t)(s.n_pad / kTile) * ((k + 15) / 16) * 64 * 4;  // one-hot bits per column tile
     b += (size_t)kTile * 4;                  // zero page
   } else if (mode == KKM_MODE_ONTHEFLY) {
     b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
@@ -302,6 +304,9 @@ int carve_ws(kkm_ctx* c, int k) {
     b.Ecp = (float*)take((size_t)b.nseg * k * s.n * 4);
     b.Ecol = (float*)take((size_t)k * s.n * 4);
     b.chunk_c0 = (int*)take((size_t)qmax * 4);
+    b.nlb = (k + 15) / 16;
+    b.roffp = (int64_t*)take((size_t)s.n * 8);
+    b.mskg = (unsigned*)take((size_t)b.nt * b.nlb * 64 * 4);
     float* zero = (float*)take((size_t)kTile * 4);
     b.zero = zero;
     rc = run(c, KKM_PHASE_OTHER, "zero page", [&] { return launch_zero_ints((int*)zero, kTile, c->stream); });
@@ -393,7 +398,7 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
     if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cur, c->stream); })))
       return rc;
   } else if (c->mode == KKM_MODE_PACKED) {
-    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_sym", [&] { return launch_spmm_sym(c->K, b, cur, c->stream); })))
+    if ((rc = run(c, KKM_PHASE_SPMM, "spmm_sym", [&] { return launch_spmm_sym(c->K, b, c->stream); })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "ecol_sum", [&] { return launch_ecol_sum(b, c->stream); })))
       return rc;

@@ -93,6 +93,11 @@ struct IterBufs {
   float* Ecol;          // k x n: column-side sums, sorted positions
   int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
                         // start), written by the scatter; null when K is not packed
+  int64_t* roffp;       // n: packed_row of the point at each sorted position (scatter)
+  unsigned* mskg;       // nt x nlb x 4 x 16 one-hot bits of each column tile (scatter):
+                        // bit 4g+e of [J][nb][kk][li] says column 128J + 16g + 4kk + e
+                        // has label 16nb + li
+  int nlb;              // label blocks of 16, ceil(k / 16)
   const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
 };
 
@@ -128,7 +133,8 @@ hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
 hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 
 // packed K (upper block triangle)
-hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hipStream_t s);
+// needs the scatter's chunk_c0, roffp and mskg for the current ids
+hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s);
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
 // E^T from the chunk partials (each starting at its chunk's first stored
 // column) plus the column-side sums Ecol (read at pos[i]); zpart per

@@ -22,7 +22,9 @@
 //    and writes the chunk's partial P[q] for the tile;
 //  - stages the block in LDS and reads it back in the MFMA operand layout
 //    (lane = row, k slot = column) for the column side.
-// The column-side sums of a row stay in the accumulators for the whole
+// The scatter prepares, once per update, each sorted row's packed offset and
+// each column tile's one-hot bits, so a workgroup's prologue is two parallel
+// loads.  The column-side sums of a row stay in the accumulators for the whole
 // segment and go to Ecp[sg] at sorted positions; ecol_sum_kernel adds the
 // segments and spmm_reduce_kernel adds them into E^T.  Fixed orders
 // throughout, so the result is bitwise reproducible.
@@ -41,7 +43,7 @@ namespace {
 // LDS) or 2 (NW = 8, ~76 KB) workgroups.
 template <int NB, int NW, int BSEG>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
-    const float* __restrict__ Kp, IterBufs b, const int* __restrict__ cl, bool cl_vec) {
+    const float* __restrict__ Kp, IterBufs b) {
   constexpr int R = 16 * NW, NT = 64 * NW;
   const int nseg = b.nseg;
   const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
@@ -63,41 +65,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   const int h = lane >> 5, c32 = lane & 31;   // load layout: row 2g + h, columns 4*c32 .. +3
   const int64_t ld = b.ld, n = b.n;
 
+  // Row tiles and packed row offsets, and the segment's one-hot bits (bit
+  // 4g+e of [tile][nb][lk][li]: column 16g + 4lk + e of the tile has label
+  // 16nb + li), all prepared by the scatter for this update.
   if (tid < R) {
     if (tid < nr) {
-      const int r = b.perm[p0 + tid];
-      rtile[tid] = r / kTile;
-      roff[tid] = packed_row(r, ld);
+      rtile[tid] = b.perm[p0 + tid] / kTile;
+      roff[tid] = b.roffp[p0 + tid];
     } else {
       rtile[tid] = INT_MAX;
       roff[tid] = 0;
     }
   }
-  // One-hot bits for every tile of the segment: bit 4g+e of entry
-  // [tile][nb][lk][li] says whether column 16g + 4lk + e of the tile has
-  // label 16nb + li.  Columns at or past n have no label.  The ids are read
-  // 16 bytes at a time when their address allows it (cl_vec).
-  for (int t = tid; t < (Je - Js) * NB * 64; t += NT) {
-    const int bi = t / (NB * 64), rem = t % (NB * 64);
-    const int nb = rem >> 6, kk = (rem >> 4) & 3, lab = 16 * nb + (rem & 15);
-    const int64_t c0 = (int64_t)(Js + bi) * kTile + 4 * kk;
-    unsigned m = 0;
-    if (cl_vec && (int64_t)(Js + bi + 1) * kTile <= n) {
-#pragma unroll
-      for (int g = 0; g < 8; ++g) {
-        const int4 v = *(const int4*)(cl + c0 + 16 * g);
-        m |= (unsigned)(v.x == lab) << (4 * g) | (unsigned)(v.y == lab) << (4 * g + 1) |
-             (unsigned)(v.z == lab) << (4 * g + 2) | (unsigned)(v.w == lab) << (4 * g + 3);
-      }
-    } else {
-      for (int g = 0; g < 8; ++g)
-        for (int e = 0; e < 4; ++e) {
-          const int64_t c = c0 + 16 * g + e;
-          if (c < n && cl[c] == lab) m |= 1u << (4 * g + e);
-        }
-    }
-    mskl[bi][nb][kk][rem & 15] = m;
-  }
+  for (int t = tid; t < (Je - Js) * NB * 64; t += NT)
+    (&mskl[0][0][0][0])[t] = b.mskg[(int64_t)Js * NB * 64 + t];
   __syncthreads();
 
   const int I0 = rtile[0];
@@ -111,13 +92,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   f4 b0[8], b1[8];
   f4* tw = tile[w];
 
-  // Rows not stored in tile J (their diagonal tile is further right), rows
-  // past the chunk and tiles past the segment read the zero page instead.
+  // Rows not stored in tile J (their diagonal tile is further right) and rows
+  // past the chunk read the zero page instead.
   auto load = [&](f4(&buf)[8], int J) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int u = w * 16 + 2 * g + h;
-      const bool on = rtile[u] <= J && J < J_hi;
+      const bool on = rtile[u] <= J;
       const float* rp = on ? Kp + roff[u] + (int64_t)J * kTile + 4 * c32 : b.zero + 4 * c32;
       buf[g] = __builtin_nontemporal_load((const f4*)rp);
     }
@@ -139,7 +120,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     // the buffer is free again: fetch the tile two ahead into it (kept after
     // the staging stores so that no third buffer is needed)
     __builtin_amdgcn_sched_barrier(0);
-    load(buf, J + 2);
+    if (J + 2 < J_hi) load(buf, J + 2);  // nothing past the segment
     __builtin_amdgcn_sched_barrier(0);
 
     // column side: entries right of the row's own diagonal tile
@@ -177,7 +158,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   };
 
   load(b0, J_lo);
-  load(b1, J_lo + 1);
+  if (J_lo + 1 < J_hi) load(b1, J_lo + 1);
   for (int J = J_lo; J < J_hi; J += 2) {
     step(b0, J, 0);
     if (J + 1 < J_hi) step(b1, J + 1, 1);
@@ -287,12 +268,12 @@ __global__ __launch_bounds__(256) void packed_rows_kernel(const float* __restric
 
 }  // namespace
 
-hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, const int* cl, hipStream_t s) {
+hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s) {
   const unsigned grid = (unsigned)((int64_t)b.qmax * b.nseg);
-  const int nb = (b.k + 15) / 16;
-  const bool v = ((uintptr_t)cl & 15) == 0;
+  const int nb = b.nlb;
+  if (nb != (b.k + 15) / 16) return hipErrorInvalidValue;
 #define KKM_SYM_LAUNCH(NB, NW, S) \
-  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S>), dim3(grid), dim3(64 * NW), 0, s, Kp, b, cl, v)
+  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S>), dim3(grid), dim3(64 * NW), 0, s, Kp, b)
   if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
   if (b.bseg != 8 && !(b.bseg == 16 && nb == 1 && b.chunk_len == 128)) return hipErrorInvalidValue;
   const bool tall = b.chunk_len == 128;
