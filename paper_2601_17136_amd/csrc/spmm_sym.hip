@@ -17,11 +17,14 @@
 // rows store.
 // Per tile a wavefront
 //  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
-//    contiguous bytes per instruction, two tiles ahead of use;
+//    contiguous bytes per instruction, one tile ahead: a single register
+//    buffer, refilled as soon as the block is staged (two buffers and two
+//    tiles in flight measured slower: 180 vs 166 us on 20000 points);
 //  - adds the rows in registers (row side), combines the wavefronts in LDS
 //    and writes the chunk's partial P[q] for the tile;
-//  - stages the block in LDS and reads it back in the MFMA operand layout
-//    (lane = row, k slot = column) for the column side.
+//  - stages the block in LDS in two 64-column halves and reads each back in
+//    the MFMA operand layout (lane = row, k slot = column) for the column
+//    side.
 // The scatter prepares, once per update, each sorted row's packed offset and
 // each column tile's one-hot bits, so a workgroup's prologue is two parallel
 // loads.  The column-side sums of a row stay in the accumulators for the whole
@@ -39,8 +42,9 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
-// 16 wavefronts per CU: at most 128 VGPRs each, and 4 (NW = 4, ~39 KB of
-// LDS) or 2 (NW = 8, ~76 KB) workgroups.
+// 90 VGPRs and ~23 KB (NW = 4) or ~45 KB (NW = 8) of LDS per workgroup:
+// 20 or 16 wavefronts per CU.  Six wavefronts per SIMD (80 VGPRs, spilling)
+// measured slower.
 template <int NB, int NW, int BSEG>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const float* __restrict__ Kp, IterBufs b) {
@@ -57,7 +61,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ int rtile[R];
   __shared__ int64_t roff[R];
   __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
-  __shared__ f4 tile[NW][16 * 32];                // per wavefront: 16 rows x 32 chunks of 16 B
+  __shared__ f4 tile[NW][16 * 16];                // per wavefront: 16 rows x 16 chunks of 16 B (a half tile)
   __shared__ f4 red[2][NW][32];                   // row-side sums of the wavefronts
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -89,7 +93,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   f4 D[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
-  f4 b0[8], b1[8];
+  f4 bb[8];
   f4* tw = tile[w];
 
   // Rows not stored in tile J (their diagonal tile is further right) and rows
@@ -111,17 +115,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     for (int g = 1; g < 8; ++g) rs += buf[g];
 #pragma unroll
     for (int e = 0; e < 4; ++e) rs[e] += __shfl_xor(rs[e], 32, 64);
-    // stage the 16 x 128 block; chunk index xor row keeps both access patterns conflict-free
-#pragma unroll
-    for (int g = 0; g < 8; ++g) {
-      const int r = 2 * g + h;
-      tw[r * 32 + (c32 ^ r)] = buf[g];
-    }
-    // the buffer is free again: fetch the tile two ahead into it (kept after
-    // the staging stores so that no third buffer is needed)
-    __builtin_amdgcn_sched_barrier(0);
-    if (J + 2 < J_hi) load(buf, J + 2);  // nothing past the segment
-    __builtin_amdgcn_sched_barrier(0);
 
     // column side: entries right of the row's own diagonal tile
     const int bi = J - Js;
@@ -130,18 +123,38 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     for (int nb = 0; nb < NB; ++nb) msk[nb] = mskl[bi][nb][lk][li];
     const bool diag = rt_first <= J && J <= rt_last;  // some row of the group sits in tile J
     const bool dz = rt_m >= J;
-    if (rt_first < J || diag) {
+    const bool any = rt_first < J || diag;
+    // the block is staged and multiplied in two 64-column halves (chunk
+    // index xor row keeps both access patterns conflict-free)
 #pragma unroll
-      for (int g = 0; g < 8; ++g) {
-        f4 v = tw[li * 32 + ((4 * g + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
-        if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
+    for (int half = 0; half < 2; ++half) {
+      if ((c32 >> 4) == half) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
+        for (int g = 0; g < 8; ++g) {
+          const int r = 2 * g + h;
+          tw[r * 16 + ((c32 & 15) ^ r)] = buf[g];
+        }
+      }
+      if (half == 1) {
+        // the whole block is staged: fetch the next tile into the buffer
+        __builtin_amdgcn_sched_barrier(0);
+        if (J + 1 < J_hi) load(buf, J + 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (any) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
-          }
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int g = 4 * half + g4;
+          f4 v = tw[li * 16 + ((4 * g4 + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
+          if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
+              D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
+            }
+        }
       }
     }
 
@@ -157,12 +170,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     }
   };
 
-  load(b0, J_lo);
-  if (J_lo + 1 < J_hi) load(b1, J_lo + 1);
-  for (int J = J_lo; J < J_hi; J += 2) {
-    step(b0, J, 0);
-    if (J + 1 < J_hi) step(b1, J + 1, 1);
-  }
+  load(bb, J_lo);
+  for (int J = J_lo; J < J_hi; ++J) step(bb, J, (J - J_lo) & 1);
 
   // D[nb][r]: label 16nb + 4lk + r of row um
   if (um < nr)
