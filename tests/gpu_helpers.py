@@ -18,12 +18,13 @@ def rowscaled_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
     fin = np.isfinite(ref)
     assert np.array_equal(fin, np.isfinite(gpu)), "infinite entries differ"
+    assert np.array_equal(gpu[~fin], ref[~fin]), "infinite entries differ in sign"
     if not fin.any():
         return 0.0
     a = np.where(fin, np.abs(ref), 0.0)
     scale = a.max(axis=1, keepdims=True)
     scale[scale == 0] = 1.0
-    err = np.where(fin, np.abs(gpu - ref), 0.0) / scale
+    err = np.abs(np.where(fin, gpu, 0.0) - np.where(fin, ref, 0.0)) / scale
     return float(err.max())
 
 
