@@ -9,34 +9,64 @@
 
 namespace kkm {
 
-// One wavefront per row; a fixed shuffle tree makes the norm deterministic.
+// Each wavefront stages kStageRows rows at once (their loads in flight
+// together); per row, lane l sums the squares of columns l, l+64, ... in order
+// and a fixed shuffle tree adds the lanes, so the norm is deterministic.
 // maxnrm_bits (zero on entry) receives the largest norm as its IEEE bits
-// (non-negative floats order like their bit patterns).
-__global__ __launch_bounds__(256) void stage_kernel(const float* __restrict__ X, int64_t n, int d,
-                                                    int d_pad, int64_t n_pad,
-                                                    float* __restrict__ Xp,
-                                                    float* __restrict__ nrm,
-                                                    unsigned* __restrict__ maxnrm_bits) {
-  const int lane = threadIdx.x & 63;
-  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (i >= n_pad) return;
-  float s = 0.f;
+// (non-negative floats order like their bit patterns); a workgroup takes the
+// max of its rows in LDS and updates the word only when its max is larger than
+// what the word already holds.  A stale read only costs a redundant atomic.
+constexpr int kStageRows = 4;
+constexpr int kStageWaves = 4;
+
+__global__ __launch_bounds__(64 * kStageWaves) void stage_kernel(const float* __restrict__ X, int64_t n,
+                                                                 int d, int d_pad, int64_t n_pad,
+                                                                 float* __restrict__ Xp,
+                                                                 float* __restrict__ nrm,
+                                                                 unsigned* __restrict__ maxnrm_bits) {
+  __shared__ float wmax[kStageWaves];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t i0 = ((int64_t)blockIdx.x * kStageWaves + w) * kStageRows;
+  float s[kStageRows];
+#pragma unroll
+  for (int r = 0; r < kStageRows; ++r) s[r] = 0.f;
   for (int c = lane; c < d_pad; c += 64) {
-    float v = (i < n && c < d) ? X[i * d + c] : 0.f;
-    Xp[i * d_pad + c] = v;
-    s = fmaf(v, v, s);
+    float v[kStageRows];
+#pragma unroll
+    for (int r = 0; r < kStageRows; ++r) {
+      const int64_t i = i0 + r;
+      v[r] = (i < n && c < d) ? X[i * d + c] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < kStageRows; ++r) {
+      const int64_t i = i0 + r;
+      if (i < n_pad) Xp[i * d_pad + c] = v[r];
+      s[r] = fmaf(v[r], v[r], s[r]);
+    }
   }
-  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (lane == 0) {
-    nrm[i] = s;
-    atomicMax(maxnrm_bits, __float_as_uint(s));
+  float m = 0.f;
+#pragma unroll
+  for (int r = 0; r < kStageRows; ++r) {
+    for (int off = 32; off > 0; off >>= 1) s[r] += __shfl_xor(s[r], off, 64);
+    if (lane == r && i0 + r < n_pad) nrm[i0 + r] = s[r];
+    m = fmaxf(m, s[r]);
+  }
+  if (lane == 0) wmax[w] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < kStageWaves; ++q) m = fmaxf(m, wmax[q]);
+    const unsigned bits = __float_as_uint(m);
+    if (__hip_atomic_load(maxnrm_bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < bits)
+      atomicMax(maxnrm_bits, bits);
   }
 }
 
 hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
                         float* nrm, unsigned* maxnrm_bits, hipStream_t s) {
-  dim3 grid((unsigned)((n_pad + 3) / 4));
-  hipLaunchKernelGGL(stage_kernel, grid, dim3(256), 0, s, X, n, d, d_pad, n_pad, Xp, nrm, maxnrm_bits);
+  const int64_t rows = (int64_t)kStageRows * kStageWaves;
+  dim3 grid((unsigned)((n_pad + rows - 1) / rows));
+  hipLaunchKernelGGL(stage_kernel, grid, dim3(64 * kStageWaves), 0, s, X, n, d, d_pad, n_pad, Xp, nrm,
+                     maxnrm_bits);
   return hipGetLastError();
 }
 
