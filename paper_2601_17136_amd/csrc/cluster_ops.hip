@@ -48,6 +48,19 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
   int* hist = (int*)(sc + k);          // k
 
   for (int j = tid; j < k; j += 256) hist[j] = 0;
+  // Loads that do not wait for z are issued first (clamped to a valid point
+  // so they need no branch).
+  const int64_t i = (int64_t)blockIdx.x * kBlk + tid;
+  const bool valid = i < b.n;
+  const int64_t iv = valid ? i : b.n - 1;
+  const int cl_i = cl_in[iv];
+  float dg = 0.f;
+  int64_t ei = iv;  // column of E^T holding point i
+  if (MODE == 1) {
+    dg = b.diagK[iv];
+    if (pos) ei = pos[iv];
+  }
+  const int cnt0 = (MODE == 1 && tid < k) ? counts_in[tid] : 0;
   if (MODE == 1) {
     // sum_{i in L_j} E(i, j) from the reduction's nzpart parts: for k <= 256,
     // 256/k threads per cluster each add a fixed run of parts, and the runs
@@ -60,13 +73,20 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
       if (j < k) {
         const int per = (b.nzpart + G - 1) / G, lo = g * per, hi = min(b.nzpart, lo + per);
         const double* zp = b.zpart + (int64_t)j * b.nzpart;
-        for (int x = lo; x < hi; ++x) s += zp[x];
+        for (int x = lo; x < hi; x += 4) {  // four loads in flight, added in order
+          double v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = zp[min(x + u, hi - 1)];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (x + u < hi) s += v[u];
+        }
       }
       zrun[tid] = s;
       __syncthreads();
     }
     for (int j = tid; j < k; j += 256) {
-      const int c = counts_in[j];
+      const int c = j == tid ? cnt0 : counts_in[j];
       double zs = 0.0;
       if (c > 0) {
         if (k <= 256) {
@@ -90,35 +110,42 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
     *obj = *b.trK - s;  // J(cl_in) = tr K - sum_j |L_j| z_j
   }
 
-  const int64_t i = (int64_t)blockIdx.x * kBlk + tid;
-  const bool valid = i < b.n;
   int lab = 0, chg = 0;
   if (valid) {
     if (MODE == 0) {
-      lab = cl_in[i];
+      lab = cl_i;
       if (lab < 0 || lab >= k) {
         atomicOr(b.status, 1);
         lab = clamp_id(lab, k);
       }
     } else {
-      const float dg = b.diagK[i];
-      const int64_t ei = pos ? (int64_t)pos[i] : i;  // column of E^T holding point i
       float best = INFINITY;
       int arg = -1;
-      for (int j = 0; j < k; ++j) {
-        const float s = sc[j];
-        float Dv = INFINITY;
-        if (s != 0.f) {
-          Dv = fmaf(s, b.Et[(int64_t)j * b.ld + ei], dg + zf[j]);
-          if (arg < 0 || Dv < best) {
-            best = Dv;
-            arg = j;
+      for (int j0 = 0; j0 < k; j0 += 8) {
+        // eight entries of E in flight (E^T has k rows, so the clamped reads
+        // stay inside it); empty clusters are read but not used
+        float ev[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ev[u] = b.Et[(int64_t)min(j0 + u, k - 1) * b.ld + ei];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u;
+          if (j < k) {
+            const float s = sc[j];
+            float Dv = INFINITY;
+            if (s != 0.f) {
+              Dv = fmaf(s, ev[u], dg + zf[j]);
+              if (arg < 0 || Dv < best) {
+                best = Dv;
+                arg = j;
+              }
+            }
+            if (D_out) D_out[i * k + j] = Dv;
           }
         }
-        if (D_out) D_out[i * k + j] = Dv;
       }
       lab = arg < 0 ? 0 : arg;
-      chg = (lab != clamp_id(cl_in[i], k));
+      chg = (lab != clamp_id(cl_i, k));
       cl_out[i] = lab;
     }
     atomicAdd(&hist[lab], 1);
@@ -169,12 +196,37 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
   int* qf = offs + k + 1;    // k + 1: first chunk of each cluster
   int* basej = qf + k + 1;   // k: sorted position of this block's first member of j
   int* segsum = basej + k;   // 256
+  int* cnt = segsum + 512;   // k: cluster sizes (after labs)
 
+  const int64_t i = (int64_t)blk * kBlk + tid;
+  const bool valid = i < b.n;
+  const int lab = valid ? clamp_id(cl[i], k) : -1;
   for (int q = tid; q < 4 * k; q += 256) wc[q] = 0;
+  for (int j = tid; j < k; j += 256) cnt[j] = counts[j];
+  // members of each cluster in earlier blocks: for k <= 256, 256/k threads
+  // per cluster each add a run of blocks (integers: any order is exact)
+  const int G = k <= 256 ? 256 / k : 1, jg = tid / G, g = tid % G;
+  if (k <= 256) {
+    const int seg = (blk + G - 1) / G, lo = g * seg, hi = (lo + seg < blk) ? lo + seg : blk;
+    int s = 0;
+    if (jg < k) {
+      const int* hj = b.hist + (int64_t)jg * nb;
+      for (int bb = lo; bb < hi; bb += 4) {  // four loads in flight
+        int v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = hj[min(bb + u, hi - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (bb + u < hi) s += v[u];
+      }
+    }
+    segsum[tid] = s;
+  }
+  __syncthreads();
   if (tid == 0) {
     int o = 0, q = 0;
     for (int j = 0; j < k; ++j) {
-      const int c = counts[j];
+      const int c = cnt[j];
       offs[j] = o;
       qf[j] = q;
       o += c;
@@ -185,17 +237,10 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
   }
   __syncthreads();
   if (k <= 256) {
-    const int G = 256 / k, j = tid / G, g = tid % G;
-    const int seg = (blk + G - 1) / G, lo = g * seg, hi = (lo + seg < blk) ? lo + seg : blk;
-    int s = 0;
-    if (j < k)
-      for (int bb = lo; bb < hi; ++bb) s += b.hist[(int64_t)j * nb + bb];
-    segsum[tid] = s;
-    __syncthreads();
-    if (j < k && g == 0) {
-      int run = offs[j];
-      for (int gg = 0; gg < G; ++gg) run += segsum[j * G + gg];
-      basej[j] = run;
+    if (jg < k && g == 0) {
+      int run = offs[jg];
+      for (int gg = 0; gg < G; ++gg) run += segsum[jg * G + gg];
+      basej[jg] = run;
     }
   } else {
     for (int j = tid; j < k; j += 256) {
@@ -227,9 +272,6 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
     }
   }
 
-  const int64_t i = (int64_t)blk * kBlk + tid;
-  const bool valid = i < b.n;
-  const int lab = valid ? clamp_id(cl[i], k) : -1;
   int* labs = segsum + 256;  // this block's 256 ids (-1 past n), for the packed one-hot masks
   labs[tid] = lab;
   int rank = 0;
@@ -277,7 +319,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
 
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s) {
-  const size_t sm = (size_t)(7 * b.k + 2 + 512) * sizeof(int);
+  const size_t sm = (size_t)(8 * b.k + 2 + 512) * sizeof(int);
   hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)b.nblk), dim3(256), sm, s, b, cl, counts,
                      zero_counts, zero_changed);
   return hipGetLastError();

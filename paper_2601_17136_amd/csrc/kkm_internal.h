@@ -90,7 +90,7 @@ struct IterBufs {
   // packed K only
   int nt, nseg, bseg;   // column tiles (ld / kTile); column segments of bseg tiles
   float* Ecp;           // nseg x k x n: column-side partials per segment, sorted positions
-  float* Ecol;          // k x n: column-side sums, sorted positions
+  float* Ecol;          // k x n: column-side sums, by point index
   int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
                         // start), written by the scatter; null when K is not packed
   int64_t* roffp;       // n: packed_row of the point at each sorted position (scatter)
@@ -137,7 +137,7 @@ hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s);
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
 // E^T from the chunk partials (each starting at its chunk's first stored
-// column) plus the column-side sums Ecol (read at pos[i]); zpart per
+// column) plus the column-side sums Ecol (by point index); zpart per
 // kSymRedStripe columns.
 hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,

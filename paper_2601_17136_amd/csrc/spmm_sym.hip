@@ -29,7 +29,8 @@
 // each column tile's one-hot bits, so a workgroup's prologue is two parallel
 // loads.  The column-side sums of a row stay in the accumulators for the whole
 // segment and go to Ecp[sg] at sorted positions; ecol_sum_kernel adds the
-// segments and spmm_reduce_kernel adds them into E^T.  Fixed orders
+// segments into Ecol at each row's point index, and spmm_reduce_sym_kernel
+// adds them into E^T.  Fixed orders
 // throughout, so the result is bitwise reproducible.
 #include "kkm_internal.h"
 
@@ -51,12 +52,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   constexpr int R = 16 * NW, NT = 64 * NW;
   const int nseg = b.nseg;
   const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
-  if (q >= *b.nchunks) return;
-  const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
+  // q < qmax, so the chunk table is read before the count says whether q is
+  // in use (one round trip instead of two)
+  const int nq = *b.nchunks, p0 = b.chunk_p0[q], p1 = b.chunk_p1[q], c0 = b.chunk_c0[q];
   const int Js = sg * BSEG, Je = min(b.nt, Js + BSEG);
   // Rows are in increasing index order within a chunk, so the first row has
   // the smallest tile; a segment left of it holds nothing of this chunk.
-  if (b.chunk_c0[q] >= Je * kTile) return;
+  if (q >= nq || c0 >= Je * kTile) return;
+  const int nr = p1 - p0;
 
   __shared__ int rtile[R];
   __shared__ int64_t roff[R];
@@ -184,32 +187,34 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       }
 }
 
-// Ecol[j][p] = sum over the segments that hold row p's stored columns, in
-// order.  One output per thread: (chunk, label, row) over ecol_wgs(b)
-// workgroups per chunk.
+// Ecol[j][perm[p]] = sum over the segments that hold the stored columns of
+// the row at sorted position p, in order (stored at the point's own index, so
+// the reduction reads it in step with E^T).  One output per thread: (chunk,
+// label, row) over ecol_wgs(b) workgroups per chunk.
 __device__ __host__ inline int ecol_wgs(const IterBufs& b) { return (b.k * b.chunk_len + 255) / 256; }
 __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
   const int per = ecol_wgs(b);
   const int q = (int)(blockIdx.x / (unsigned)per), part = (int)(blockIdx.x % (unsigned)per);
-  if (q >= *b.nchunks) return;
-  const int p0 = b.chunk_p0[q], nr = b.chunk_p1[q] - p0;
+  const int nq = *b.nchunks, p0 = b.chunk_p0[q], p1 = b.chunk_p1[q], c0 = b.chunk_c0[q];
+  if (q >= nq) return;
+  const int nr = p1 - p0;
   const int t = part * 256 + (int)threadIdx.x;
   if (t >= b.k * nr) return;
   const int j = t / nr, u = t % nr;
-  const int s0 = b.chunk_c0[q] / kTile / b.bseg;
+  const int row = b.perm[p0 + u];
+  const int s0 = c0 / kTile / b.bseg, last = b.nseg - 1;
   const int64_t seg_stride = (int64_t)b.k * b.n;
   const float* e = b.Ecp + (int64_t)j * b.n + p0 + u;
   float acc = 0.f;
-  int sg = s0;
-  for (; sg + 8 <= b.nseg; sg += 8) {  // eight loads in flight, added in order
+  for (int sg = s0; sg <= last; sg += 8) {  // eight loads in flight, added in order
     float v[8];
 #pragma unroll
-    for (int x = 0; x < 8; ++x) v[x] = e[(sg + x) * seg_stride];
+    for (int x = 0; x < 8; ++x) v[x] = e[min(sg + x, last) * seg_stride];
 #pragma unroll
-    for (int x = 0; x < 8; ++x) acc += v[x];
+    for (int x = 0; x < 8; ++x)
+      if (sg + x <= last) acc += v[x];
   }
-  for (; sg < b.nseg; ++sg) acc += e[sg * seg_stride];
-  b.Ecol[(int64_t)j * b.n + p0 + u] = acc;
+  b.Ecol[(int64_t)j * b.n + row] = acc;
 }
 
 // Workgroup (stripe of kSymRedStripe columns, cluster j).  Cluster j's many
@@ -224,26 +229,39 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
   if (qa == qb) return;  // empty cluster: E^T(j, .) and z_j are never read
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   __shared__ f4 part[4][64];
-  const int64_t ld = b.ld;
+  const int64_t ld = b.ld, n = b.n;
   const int64_t col = (int64_t)stripe * kSymRedStripe + 4 * lane;
+  // the column-side sums and ids of the stripe's points, for wavefront 0's
+  // epilogue, are loaded before the chunk loop
+  float ec[4];
+  int cc[4];
+  if (w == 0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t x = min(col + c, n - 1);
+      ec[c] = b.Ecol[(int64_t)j * n + x];
+      cc[c] = cl[x];
+    }
+  }
   const int per = (qb - qa + 3) / 4;
   const int q0 = qa + w * per, q1 = min(qb, q0 + per);
   f4 e = {0.f, 0.f, 0.f, 0.f};
   if (col < ld) {
-    int q = q0;
-    for (; q + 8 <= q1; q += 8) {  // eight chunks in flight, added in order
+    // a chunk's partial starts at its first stored column; entries left of
+    // it are stale and are read but not added
+    for (int q = q0; q < q1; q += 8) {  // eight chunks in flight, added in order
       int c0[8];
       f4 v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) c0[u] = b.chunk_c0[q + u];
+      for (int u = 0; u < 8; ++u) {
+        const int qq = min(q + u, q1 - 1);
+        c0[u] = b.chunk_c0[qq];
+        v[u] = *(const f4*)(b.P + (int64_t)qq * ld + col);
+      }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        v[u] = col >= c0[u] ? *(const f4*)(b.P + (int64_t)(q + u) * ld + col) : f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int u = 0; u < 8; ++u) e += v[u];
+        if (q + u < q1 && col >= c0[u]) e += v[u];
     }
-    for (; q < q1; ++q)
-      if (col >= b.chunk_c0[q]) e += *(const f4*)(b.P + (int64_t)q * ld + col);
   }
   part[w][lane] = e;
   __syncthreads();
@@ -253,11 +271,11 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
     e = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-      if (col + c < b.n) e[c] += b.Ecol[(int64_t)j * b.n + b.pos[col + c]];
+      if (col + c < n) e[c] += ec[c];
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-      if (col + c < b.n && cl[col + c] == j) zs += (double)e[c];
+      if (col + c < n && cc[c] == j) zs += (double)e[c];
   }
   for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off, 64);
   if (lane == 0) b.zpart[(int64_t)j * ns + stripe] = zs;
