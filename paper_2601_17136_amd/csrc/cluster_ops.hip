@@ -270,6 +270,15 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
       b.chunk_p0[q] = p0;
       b.chunk_p1[q] = (p0 + b.chunk_len < end) ? p0 + b.chunk_len : end;
     }
+    // packed K: the chunk-major member table ends each cluster's last chunk
+    // and starts each unused chunk with -1 (the members are written below)
+    if (b.crow) {
+      const int cl = b.chunk_len;
+      for (int j = 0; j < k; ++j)
+        for (int64_t x = (int64_t)qf[j] * cl + (offs[j + 1] - offs[j]) + tid; x < (int64_t)qf[j + 1] * cl; x += 256)
+          b.crow[x] = -1;
+      for (int q = qf[k] + tid; q < b.qmax; q += 256) b.crow[(int64_t)q * cl] = -1;
+    }
   }
 
   int* labs = segsum + 256;  // this block's 256 ids (-1 past n), for the packed one-hot masks
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(IterBufs b, const int* __r
     const int rel = r - offs[lab];
     if (b.chunk_c0 && rel % b.chunk_len == 0)
       b.chunk_c0[qf[lab] + rel / b.chunk_len] = (int)(i / kTile) * kTile;
-    if (b.roffp) b.roffp[r] = packed_row(i, b.ld);
+    if (b.crow) b.crow[(int64_t)qf[lab] * b.chunk_len + rel] = (int)i;
   }
   // packed K: the one-hot bits of this block's two column tiles, once per
   // update (the SpMM reads them instead of the ids)

@@ -88,10 +88,10 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
     b += (size_t)qmax * s.ld * 4;         // P: chunk partials
   }
   if (mode == KKM_MODE_PACKED) {
-    b += (size_t)nseg_for(s, k) * k * s.n * 4;  // Ecp: column-side partials per segment
+    b += (size_t)nseg_for(s, k) * k * qmax * chunk_len_for(s, mode) * 4;  // Ecp: column-side partials
     b += (size_t)k * s.n * 4;                // Ecol
     b += (size_t)qmax * 4;                   // chunk start columns
-    b += (size_t)s.n * 8;                    // packed row offsets at sorted positions
+    b += (size_t)qmax * chunk_len_for(s, mode) * 4;  // chunk-major member table
     b += (size_t)(s.n_pad / kTile) * ((k + 15) / 16) * 64 * 4;  // one-hot bits per column tile
     b += (size_t)kTile * 4;                  // zero page
   } else if (mode == KKM_MODE_ONTHEFLY) {
@@ -301,11 +301,11 @@ int carve_ws(kkm_ctx* c, int k) {
     b.nt = (int)(s.n_pad / kTile);
     b.bseg = sym_seg_for(s.n, k);
     b.nseg = nseg_for(s, k);
-    b.Ecp = (float*)take((size_t)b.nseg * k * s.n * 4);
+    b.Ecp = (float*)take((size_t)b.nseg * k * qmax * b.chunk_len * 4);
     b.Ecol = (float*)take((size_t)k * s.n * 4);
     b.chunk_c0 = (int*)take((size_t)qmax * 4);
     b.nlb = (k + 15) / 16;
-    b.roffp = (int64_t*)take((size_t)s.n * 8);
+    b.crow = (int*)take((size_t)qmax * b.chunk_len * 4);
     b.mskg = (unsigned*)take((size_t)b.nt * b.nlb * 64 * 4);
     float* zero = (float*)take((size_t)kTile * 4);
     b.zero = zero;

@@ -89,11 +89,14 @@ struct IterBufs {
   int* status;          // 1: bit 0 = id out of range
   // packed K only
   int nt, nseg, bseg;   // column tiles (ld / kTile); column segments of bseg tiles
-  float* Ecp;           // nseg x k x n: column-side partials per segment, sorted positions
+  float* Ecp;           // nseg x k x (qmax * chunk_len): column-side partials per segment,
+                        // at chunk-major positions (member t of chunk q at q * chunk_len + t)
   float* Ecol;          // k x n: column-side sums, by point index
   int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
                         // start), written by the scatter; null when K is not packed
-  int64_t* roffp;       // n: packed_row of the point at each sorted position (scatter)
+  int* crow;            // qmax x chunk_len: point index of member t of chunk q at
+                        // q * chunk_len + t (scatter); -1 past a chunk's end and at the
+                        // start of an unused chunk
   unsigned* mskg;       // nt x nlb x 4 x 16 one-hot bits of each column tile (scatter):
                         // bit 4g+e of [J][nb][kk][li] says column 128J + 16g + 4kk + e
                         // has label 16nb + li
@@ -133,7 +136,7 @@ hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
 hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 
 // packed K (upper block triangle)
-// needs the scatter's chunk_c0, roffp and mskg for the current ids
+// needs the scatter's crow and mskg for the current ids
 hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s);
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
 // E^T from the chunk partials (each starting at its chunk's first stored

@@ -17,21 +17,21 @@
 // rows store.
 // Per tile a wavefront
 //  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
-//    contiguous bytes per instruction, one tile ahead: a single register
-//    buffer, refilled as soon as the block is staged (two buffers and two
-//    tiles in flight measured slower: 180 vs 166 us on 20000 points);
+//    contiguous bytes per instruction, one tile ahead in a single register
+//    buffer (a second buffer costs more occupancy than it gains);
 //  - adds the rows in registers (row side), combines the wavefronts in LDS
 //    and writes the chunk's partial P[q] for the tile;
-//  - stages the block in LDS in two 64-column halves and reads each back in
-//    the MFMA operand layout (lane = row, k slot = column) for the column
-//    side.
-// The scatter prepares, once per update, each sorted row's packed offset and
-// each column tile's one-hot bits, so a workgroup's prologue is two parallel
-// loads.  The column-side sums of a row stay in the accumulators for the whole
-// segment and go to Ecp[sg] at sorted positions; ecol_sum_kernel adds the
-// segments into Ecol at each row's point index, and spmm_reduce_sym_kernel
-// adds them into E^T.  Fixed orders
-// throughout, so the result is bitwise reproducible.
+//  - stages the block in LDS and reads it back in the MFMA operand layout
+//    (lane = row, k slot = column) for the column side.  With one label
+//    block the whole block is staged and the next tile's loads are issued
+//    right after, so they are in flight during the multiply.
+// The scatter writes, once per update, the chunks' members in chunk-major
+// order and each column tile's one-hot bits, so a workgroup's prologue is a
+// single round trip of independent loads.  The column-side sums of a row stay
+// in the accumulators for the whole segment and go to Ecp[sg] at the row's
+// chunk-major position; ecol_sum_kernel adds the segments into Ecol at each
+// row's point index, and spmm_reduce_sym_kernel adds them into E^T.  Fixed
+// orders throughout, so the result is bitwise reproducible.
 #include "kkm_internal.h"
 
 #include <algorithm>
@@ -50,66 +50,102 @@ template <int NB, int NW, int BSEG>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const float* __restrict__ Kp, IterBufs b) {
   constexpr int R = 16 * NW, NT = 64 * NW;
+  // With one label block the whole 16 x 128 block is staged at once; with
+  // more, the MFMA work per tile is larger and the block goes in two halves,
+  // which keeps the LDS per workgroup (and so the occupancy) down.
+  constexpr bool kFull = NB == 1;
+  constexpr int kCh = kFull ? 32 : 16;                   // 16-byte chunks per staged row
+  constexpr int kMw = BSEG * NB * 64;                    // one-hot words of a segment
+  constexpr int kMpt = (kMw + NT - 1) / NT;              // ... per thread
   const int nseg = b.nseg;
   const int q = (int)(blockIdx.x / (unsigned)nseg), sg = (int)(blockIdx.x % (unsigned)nseg);
-  // q < qmax, so the chunk table is read before the count says whether q is
-  // in use (one round trip instead of two)
-  const int nq = *b.nchunks, p0 = b.chunk_p0[q], p1 = b.chunk_p1[q], c0 = b.chunk_c0[q];
-  const int Js = sg * BSEG, Je = min(b.nt, Js + BSEG);
-  // Rows are in increasing index order within a chunk, so the first row has
-  // the smallest tile; a segment left of it holds nothing of this chunk.
-  if (q >= nq || c0 >= Je * kTile) return;
-  const int nr = p1 - p0;
-
-  __shared__ int rtile[R];
-  __shared__ int64_t roff[R];
-  __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
-  __shared__ f4 tile[NW][16 * 16];                // per wavefront: 16 rows x 16 chunks of 16 B (a half tile)
-  __shared__ f4 red[2][NW][32];                   // row-side sums of the wavefronts
-
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int li = lane & 15, lk = lane >> 4;   // MFMA layout: row li, k slot lk
   const int h = lane >> 5, c32 = lane & 31;   // load layout: row 2g + h, columns 4*c32 .. +3
-  const int64_t ld = b.ld, n = b.n;
+  const int64_t ld = b.ld;
+  const int Js = sg * BSEG, Je = min(b.nt, Js + BSEG);
 
-  // Row tiles and packed row offsets, and the segment's one-hot bits (bit
-  // 4g+e of [tile][nb][lk][li]: column 16g + 4lk + e of the tile has label
-  // 16nb + li), all prepared by the scatter for this update.
-  if (tid < R) {
-    if (tid < nr) {
-      rtile[tid] = b.perm[p0 + tid] / kTile;
-      roff[tid] = b.roffp[p0 + tid];
-    } else {
-      rtile[tid] = INT_MAX;
-      roff[tid] = 0;
-    }
-  }
-  for (int t = tid; t < (Je - Js) * NB * 64; t += NT)
-    (&mskl[0][0][0][0])[t] = b.mskg[(int64_t)Js * NB * 64 + t];
-  __syncthreads();
-
-  const int I0 = rtile[0];
-  const int J_lo = max(Js, I0), J_hi = Je;
+  // Everything the workgroup needs is read in one round trip: the chunk's
+  // rows by point index from the scatter's chunk-major table (-1 past the
+  // chunk's end and at the start of an unused chunk), and the segment's
+  // one-hot bits (bit 4g+e of [tile][nb][lk][li]: column 16g + 4lk + e of the
+  // tile has label 16nb + li).
+  const int* cr = b.crow + (int64_t)q * R;
+  const int i0 = cr[0];
   const int um = w * 16 + li;  // this lane's row in the MFMA layout
-  const int rt_m = rtile[um];
-  const int rt_first = rtile[w * 16], rt_last = rtile[min(w * 16 + 15, nr - 1)];
-  f4 D[NB];
+  const int im = cr[um];
+  int iu[8];
+  if (kFull) {
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
-  f4 bb[8];
-  f4* tw = tile[w];
+    for (int g = 0; g < 8; ++g) iu[g] = cr[w * 16 + 2 * g + h];
+  }
+  const int64_t mbase = (int64_t)Js * NB * 64, mlast = (int64_t)b.nt * NB * 64 - 1;
+  unsigned mv[kMpt];
+#pragma unroll
+  for (int m = 0; m < kMpt; ++m) mv[m] = b.mskg[min(mbase + tid + m * NT, mlast)];
+  // Rows are in increasing index order within a chunk, so the first row has
+  // the smallest tile; a segment left of it holds nothing of this chunk.
+  if (i0 < 0 || i0 / kTile >= Je) return;
 
-  // Rows not stored in tile J (their diagonal tile is further right) and rows
-  // past the chunk read the zero page instead.
+  __shared__ int rtile[kFull ? 1 : R];
+  __shared__ int64_t roff[kFull ? 1 : R];
+  __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
+  __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
+  __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
+
+  const int I0 = i0 / kTile;
+  const int J_lo = max(Js, I0), J_hi = Je;
+  const int rt_m = im >= 0 ? im / kTile : INT_MAX;
+  // first and last diagonal tile among the wavefront's 16 rows (rows increase
+  // with their position in the chunk; lane 0 holds the first)
+  const int rt_first = __shfl(rt_m, 0, 64);
+  int rt_last = im >= 0 ? rt_m : -1;
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) rt_last = max(rt_last, __shfl_xor(rt_last, off, 16));
+
+  // This lane's 8 rows (2g + h of its wavefront's group).  Rows not stored
+  // in tile J (their diagonal tile is further right), rows past the chunk and
+  // tiles past the segment read the zero page instead, so the loads need no
+  // branch.  With one label block the rows' packed bases (at this lane's 4
+  // columns of tile 0) and diagonal tiles are held in registers, so issuing
+  // a tile's loads needs no LDS round trip; with more label blocks the
+  // registers go to the accumulators and the rows are read from LDS.
+  const float* rbase[8];
+  int rt[8];
+  if (kFull) {
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      rt[g] = iu[g] >= 0 ? iu[g] / kTile : INT_MAX;
+      rbase[g] = Kp + packed_row(iu[g] >= 0 ? iu[g] : 0, ld) + 4 * c32;
+    }
+  } else if (tid < R) {
+    const int iv = cr[tid];
+    rtile[tid] = iv >= 0 ? iv / kTile : INT_MAX;
+    roff[tid] = iv >= 0 ? packed_row(iv, ld) : 0;
+  }
+  const float* zp = b.zero + 4 * c32;
   auto load = [&](f4(&buf)[8], int J) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int u = w * 16 + 2 * g + h;
-      const bool on = rtile[u] <= J;
-      const float* rp = on ? Kp + roff[u] + (int64_t)J * kTile + 4 * c32 : b.zero + 4 * c32;
-      buf[g] = __builtin_nontemporal_load((const f4*)rp);
+      const bool on = (kFull ? rt[g] : rtile[u]) <= J && J < J_hi;
+      const float* rp = kFull ? rbase[g] + (int64_t)J * kTile : Kp + roff[u] + (int64_t)J * kTile + 4 * c32;
+      buf[g] = __builtin_nontemporal_load((const f4*)(on ? rp : zp));
     }
   };
+
+  f4 bb[8];
+  if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
+#pragma unroll
+  for (int m = 0; m < kMpt; ++m)
+    if (tid + m * NT < kMw) (&mskl[0][0][0][0])[tid + m * NT] = mv[m];
+  __syncthreads();
+  if (!kFull) load(bb, J_lo);
+
+  f4 D[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
+  f4* tw = tile[w];
 
   auto step = [&](f4(&buf)[8], int J, int par) {
     // row side: this lane's 4 columns over its 8 rows, then the other half-wave's 8
@@ -127,37 +163,51 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     const bool diag = rt_first <= J && J <= rt_last;  // some row of the group sits in tile J
     const bool dz = rt_m >= J;
     const bool any = rt_first < J || diag;
-    // the block is staged and multiplied in two 64-column halves (chunk
-    // index xor row keeps both access patterns conflict-free)
+    // The block is staged in LDS (chunk index xor row keeps both the row-wise
+    // writes and the MFMA-layout reads conflict-free) and read back in the
+    // MFMA operand layout.  The next tile's loads are issued as soon as the
+    // whole block is staged, so they are in flight while it is multiplied.
+    auto mma = [&](int g0, int ng, int cb) {
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      if ((c32 >> 4) == half) {
+      for (int gg = 0; gg < ng; ++gg) {
+        const int g = g0 + gg;
+        f4 v = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
+        if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int g = 0; g < 8; ++g) {
-          const int r = 2 * g + h;
-          tw[r * 16 + ((c32 & 15) ^ r)] = buf[g];
-        }
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
+          }
       }
-      if (half == 1) {
-        // the whole block is staged: fetch the next tile into the buffer
-        __builtin_amdgcn_sched_barrier(0);
-        if (J + 1 < J_hi) load(buf, J + 1);
-        __builtin_amdgcn_sched_barrier(0);
+    };
+    if (kFull) {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        const int r = 2 * g + h;
+        tw[r * 32 + (c32 ^ r)] = buf[g];
       }
-      if (any) {
+      __builtin_amdgcn_sched_barrier(0);
+      load(buf, J + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (any) mma(0, 8, 0);
+    } else {
 #pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int g = 4 * half + g4;
-          f4 v = tw[li * 16 + ((4 * g4 + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
-          if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
+      for (int half = 0; half < 2; ++half) {
+        if ((c32 >> 4) == half) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-              const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
-              D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
-            }
+          for (int g = 0; g < 8; ++g) {
+            const int r = 2 * g + h;
+            tw[r * 16 + ((c32 & 15) ^ r)] = buf[g];
+          }
         }
+        if (half == 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          load(buf, J + 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (any) mma(4 * half, 4, 4 * half);
       }
     }
 
@@ -173,38 +223,35 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     }
   };
 
-  load(bb, J_lo);
   for (int J = J_lo; J < J_hi; ++J) step(bb, J, (J - J_lo) & 1);
 
-  // D[nb][r]: label 16nb + 4lk + r of row um
-  if (um < nr)
+  // D[nb][r]: label 16nb + 4lk + r of row um, at its chunk-major position
+  const int64_t ecs = (int64_t)b.qmax * R;
+  if (im >= 0)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int lab = 16 * nb + 4 * lk + r;
-        if (lab < b.k) b.Ecp[((int64_t)sg * b.k + lab) * n + p0 + um] = D[nb][r];
+        if (lab < b.k) b.Ecp[((int64_t)sg * b.k + lab) * ecs + (int64_t)q * R + um] = D[nb][r];
       }
 }
 
-// Ecol[j][perm[p]] = sum over the segments that hold the stored columns of
-// the row at sorted position p, in order (stored at the point's own index, so
-// the reduction reads it in step with E^T).  One output per thread: (chunk,
-// label, row) over ecol_wgs(b) workgroups per chunk.
+// Ecol[j][i] = the column-side sums of point i (member u of chunk q) over
+// the segments that hold its row's stored columns, in order.  One output per
+// thread: (chunk, label, member) over ecol_wgs(b) workgroups per chunk.
 __device__ __host__ inline int ecol_wgs(const IterBufs& b) { return (b.k * b.chunk_len + 255) / 256; }
 __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
-  const int per = ecol_wgs(b);
+  const int per = ecol_wgs(b), cl = b.chunk_len;
   const int q = (int)(blockIdx.x / (unsigned)per), part = (int)(blockIdx.x % (unsigned)per);
-  const int nq = *b.nchunks, p0 = b.chunk_p0[q], p1 = b.chunk_p1[q], c0 = b.chunk_c0[q];
-  if (q >= nq) return;
-  const int nr = p1 - p0;
   const int t = part * 256 + (int)threadIdx.x;
-  if (t >= b.k * nr) return;
-  const int j = t / nr, u = t % nr;
-  const int row = b.perm[p0 + u];
-  const int s0 = c0 / kTile / b.bseg, last = b.nseg - 1;
-  const int64_t seg_stride = (int64_t)b.k * b.n;
-  const float* e = b.Ecp + (int64_t)j * b.n + p0 + u;
+  const int j = t / cl, u = t % cl;
+  const int* cr = b.crow + (int64_t)q * cl;
+  const int i0 = cr[0], row = cr[u];
+  if (i0 < 0 || j >= b.k || row < 0) return;
+  const int s0 = i0 / kTile / b.bseg, last = b.nseg - 1;
+  const int64_t ecs = (int64_t)b.qmax * cl, seg_stride = (int64_t)b.k * ecs;
+  const float* e = b.Ecp + (int64_t)j * ecs + (int64_t)q * cl + u;
   float acc = 0.f;
   for (int sg = s0; sg <= last; sg += 8) {  // eight loads in flight, added in order
     float v[8];
