@@ -294,20 +294,20 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
   const int q0 = qa + w * per, q1 = min(qb, q0 + per);
   f4 e = {0.f, 0.f, 0.f, 0.f};
   if (col < ld) {
-    // a chunk's partial starts at its first stored column; entries left of
-    // it are stale and are read but not added
+    // a chunk's partial starts at its first stored column: entries left of
+    // it are stale and are not read
     for (int q = q0; q < q1; q += 8) {  // eight chunks in flight, added in order
       int c0[8];
       f4 v[8];
 #pragma unroll
+      for (int u = 0; u < 8; ++u) c0[u] = b.chunk_c0[min(q + u, q1 - 1)];
+#pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int qq = min(q + u, q1 - 1);
-        c0[u] = b.chunk_c0[qq];
-        v[u] = *(const f4*)(b.P + (int64_t)qq * ld + col);
+        v[u] = f4{0.f, 0.f, 0.f, 0.f};
+        if (q + u < q1 && col >= c0[u]) v[u] = *(const f4*)(b.P + (int64_t)(q + u) * ld + col);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (q + u < q1 && col >= c0[u]) e += v[u];
+      for (int u = 0; u < 8; ++u) e += v[u];
     }
   }
   part[w][lane] = e;
