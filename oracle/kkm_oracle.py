@@ -29,7 +29,8 @@ Readings where the paper is silent (each is listed in the design doc):
     update that changed no assignment; tol > 0 also stops once
     J(cl_{t-1}) - J(cl_t) <= tol * |J(cl_{t-1})|.
 
-Functions with no independent pin: none (see tests/test_oracle_pins.py).
+Functions with no independent pin: none (see tests/test_oracle_pins.py and
+tests/test_oracle_seed_pins.py).
 """
 from __future__ import annotations
 
@@ -277,3 +278,61 @@ def step_rows(kern: Kernel, X: np.ndarray, cl: np.ndarray, k: int, rows, z=None)
     D = distances(diag_all[rows], E, z, counts)
     return dict(E=E, z=z, D=D, cl=assign(D), counts=counts,
                 J=objective(float(diag_all.sum()), z, counts), K_rows=K_rows)
+
+
+# ----------------------------------------------------------------- seeding
+
+def feature_sq_dist(kern: Kernel, X: np.ndarray, c: int, diagK: np.ndarray) -> np.ndarray:
+    """||phi(x_m) - phi(x_c)||^2 = K(m,m) - 2 K(m,c) + K(c,c) for every m, fp64,
+    clamped at 0 (the kernel trick of Section II-B applied to one center)."""
+    Kc = kern.block(X, rows=np.array([c]))[0]
+    return np.maximum(diagK - 2.0 * Kc + diagK[c], 0.0)
+
+
+def draw_index(D: np.ndarray, ut: float, chosen) -> int:
+    """The index a uniform ut in [0, 1) draws from the weights D (one step of
+    D^2 sampling): the first i, in index order, with P(i) > ut * S, where
+    P(i) = sum_{m <= i} D(m) and S = P(n - 1), so that i is drawn with
+    probability D(i) / S.  If S = 0, the lowest index not in ``chosen``."""
+    P = np.cumsum(D)
+    S = P[-1]
+    if S > 0.0:
+        target = ut * S
+        i = 0
+        while P[i] <= target:
+            i += 1
+        return i
+    chosen = set(int(c) for c in chosen)
+    return next(m for m in range(D.size) if m not in chosen)
+
+
+def kmeanspp(kern: Kernel, X: np.ndarray, k: int, u) -> tuple[np.ndarray, np.ndarray]:
+    """K-means++ seeding in the kernel's feature space, driven by the caller's
+    uniforms: the initialization the paper cites for its convergence
+    properties (Section II-B) and leaves to future work (Section V), i.e. the
+    D^2 sampling of Arthur and Vassilvitskii, with the centers drawn from the
+    points themselves.
+
+    * u[0] in [0, 1) picks the first center, floor(u[0] * n) (uniform);
+    * D(m) = min over the chosen centers c of ||phi(x_m) - phi(x_c)||^2;
+    * center t >= 1 is ``draw_index(D, u[t], centers)``.
+    The initial ids are each point's nearest center, by position in the list,
+    lowest position among equal distances; the comparison is made on the
+    distances rounded to single precision, as in ``assign``.
+
+    Returns (centers int64[k], cl int32[n]).
+    """
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    n = X.shape[0]
+    u = np.asarray(u, dtype=np.float64)
+    assert 1 <= k <= n and u.shape == (k,)
+    diagK = kern.diag(X)
+    centers = [min(int(np.floor(u[0] * n)), n - 1)]
+    dist = [feature_sq_dist(kern, X, centers[0], diagK)]
+    D = dist[0].copy()
+    for t in range(1, k):
+        centers.append(draw_index(D, u[t], centers))
+        dist.append(feature_sq_dist(kern, X, centers[-1], diagK))
+        D = np.minimum(D, dist[-1])
+    cl = assign(np.stack(dist, axis=1))
+    return np.asarray(centers, dtype=np.int64), cl
