@@ -55,6 +55,31 @@ def counted_traffic(kernel, cfg, mode):
     return round((fetch_kib * FETCH_SCALE + write_kib * WRITE_SCALE) * 1024 / 1e9, 4)
 
 
+def time_seeding(kkm, ctx, n, k, d_pad, reps=5):
+    """K-means++ seeding on the built context (not part of the timed steps):
+    events on the context's stream around whole calls, so no launch inside is
+    bracketed.  Each of its k distance passes reads the staged points once
+    (n * d_pad * 4 bytes), the algorithmic bytes of the roofline figure."""
+    import numpy as np
+    import torch
+    u = np.random.default_rng(4242).random(k)
+    V = torch.empty(n, dtype=torch.int32, device="cuda")
+    kkm.kkm_init_kmeanspp(ctx, k, u, V)  # first call allocates the scratch
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ms = []
+    for _ in range(reps):
+        a.record()
+        kkm.kkm_init_kmeanspp(ctx, k, u, V)
+        b.record()
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    t = min(ms)
+    gbs = k * n * d_pad * 4 / (t * 1e-3) / 1e9
+    return {"ms": round(t, 4), "k": k, "launches": 2 * k - 1, "bound": "hbm", "achieved": round(gbs, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "work": "k passes over the staged points, n * d_pad * 4 bytes each"}
+
+
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -245,6 +270,8 @@ def main():
                                       "traffic": counted_traffic("gemm_kappa", args.config, args.mode),
                                       "traffic_unit": "GB per launch", "avg_launch_ms": round(gemm_ms, 5),
                                       "gauss_fixups": info["fixups"]}
+    if not args.no_timing:
+        out["kmeanspp"] = time_seeding(kkm, ctx, n, k, info["d_pad"])
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline_sized(w, X, cl0, args.cpu_seconds)

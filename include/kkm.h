@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 1
+#define KKM_ABI_VERSION 2
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -100,7 +100,8 @@ enum {
   KKM_PHASE_ONTHEFLY = 7,/* recomputed K tiles folded into E */
   KKM_PHASE_REDUCE = 8,  /* per-cluster sums of the SpMM's chunk partials, self-term parts */
   KKM_PHASE_OTHER = 9,   /* gathers, copies, trace */
-  KKM_NPHASE = 10
+  KKM_PHASE_SEED = 10,   /* K-means++ seeding: distance passes and draws */
+  KKM_NPHASE = 11
 };
 typedef struct kkm_timing {
   double ms[KKM_NPHASE];       /* summed kernel time per phase, milliseconds */
@@ -201,6 +202,31 @@ int kkm_objective(kkm_ctx *ctx, const int32_t *V, int32_t k, double *J);
  * Errors as kkm_iterate. */
 int kkm_step(kkm_ctx *ctx, const int32_t *cl_in, int32_t k, float *E, float *z, float *D,
              int32_t *cl_out, int32_t *counts_out, double *J);
+
+/* K-means++ seeding in the kernel's feature space (the initialization the
+ * paper cites for its convergence properties in Section II-B and leaves to
+ * future work in Section V): D^2 sampling of k centers among the points,
+ * then each point's nearest center as its initial id.
+ *   u[0]      picks the first center, floor(u[0] * n);
+ *   D(i)      = min over chosen centers c of K(i,i) - 2 K(i,c) + K(c,c);
+ *   center t  = the first index i with sum_{m <= i} D(m) > u[t] * sum_m D(m),
+ *               i.e. i with probability D(i) / sum D; if the sum is 0 (every
+ *               point coincides with a chosen center), the lowest index not
+ *               yet chosen.
+ * The entries of K are computed from the staged points of the last build,
+ * in every storage mode (the Gaussian from the coordinate differences).
+ * u:           host, k doubles in [0, 1), the caller's uniforms (the draws
+ *              are reproducible from them).
+ * centers_out: host, may be NULL, k int32: the chosen point indices in order.
+ * V:           device int32[n], written with the position (0 .. k-1) in the
+ *              center list of each point's nearest center, lowest position
+ *              among equal distances: ready for kkm_iterate.
+ * Sums run in a fixed order in fp64 over fp32 distances, so results are
+ * reproducible.  The context allocates O(n) scratch on first use.
+ * Synchronises before returning.
+ * Errors: KKM_ERR_ARG (k outside 1..min(n, KKM_MAX_K), u NULL or outside
+ * [0, 1), V NULL), KKM_ERR_STATE (no build), KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_init_kmeanspp(kkm_ctx *ctx, int32_t k, const double *u, int32_t *centers_out, int32_t *V);
 
 /* Rows r0 .. r1-1 of K into out (device, (r1-r0) x n fp32 row-major).  In
  * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses;

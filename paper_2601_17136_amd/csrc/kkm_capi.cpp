@@ -145,6 +145,13 @@ struct kkm_ctx {
   double* obj = nullptr;
   std::vector<Alloc> hist_allocs;
 
+  // K-means++ seeding scratch (first use after a build): n floats kd, D,
+  // best, n ints bestc, per-block fp64 sums, KKM_MAX_K center indices
+  std::vector<Alloc> seed_allocs;
+  float *sd_kd = nullptr, *sd_D = nullptr, *sd_best = nullptr;
+  int *sd_bestc = nullptr, *sd_centers = nullptr;
+  double* sd_bsum = nullptr;
+
   int32_t timing = 0;  // mask of timed phases
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> pool;
@@ -256,9 +263,17 @@ void free_hist(kkm_ctx* c) {
   c->obj = nullptr;
 }
 
+void free_seed(kkm_ctx* c) {
+  release(c, c->seed_allocs);
+  c->sd_kd = c->sd_D = c->sd_best = nullptr;
+  c->sd_bestc = c->sd_centers = nullptr;
+  c->sd_bsum = nullptr;
+}
+
 void free_build(kkm_ctx* c) {
   free_ws(c);
   free_hist(c);
+  free_seed(c);
   release(c, c->build_allocs);
   c->Xp = c->nrm = c->diagK = c->K = nullptr;
   c->trK = nullptr;
@@ -693,6 +708,56 @@ int kkm_step(kkm_ctx* c, const int32_t* cl_in, int32_t k, float* E, float* z, fl
 int kkm_objective(kkm_ctx* c, const int32_t* V, int32_t k, double* J) {
   if (!J) return fail(c, KKM_ERR_ARG, "J is NULL");
   return kkm_step(c, V, k, nullptr, nullptr, nullptr, nullptr, nullptr, J);
+}
+
+int kkm_init_kmeanspp(kkm_ctx* c, int32_t k, const double* u, int32_t* centers_out, int32_t* V) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  const int64_t n = c->sz.n;
+  if (k < 1 || k > KKM_MAX_K || (int64_t)k > n)
+    return fail(c, KKM_ERR_ARG, "k=%d must be in [1, min(n=%lld, %d)]", k, (long long)n, KKM_MAX_K);
+  if (!u) return fail(c, KKM_ERR_ARG, "u is NULL");
+  if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
+  for (int t = 0; t < k; ++t)
+    if (!(u[t] >= 0.0 && u[t] < 1.0)) return fail(c, KKM_ERR_ARG, "u[%d]=%g is outside [0, 1)", t, u[t]);
+  if (!c->sd_kd) {
+    const size_t nb = (size_t)seed_blocks(n);
+    const size_t bytes = 4 * (((size_t)n * 4 + 255) / 256 * 256) + (nb * 8 + 255) / 256 * 256 + KKM_MAX_K * 4;
+    void* base = nullptr;
+    int rc = dalloc(c, &base, bytes, c->seed_allocs, "seeding scratch");
+    if (rc) return rc;
+    char* p = (char*)base;
+    auto take = [&](size_t b) {
+      char* r = p;
+      p += (b + 255) / 256 * 256;
+      return (void*)r;
+    };
+    c->sd_kd = (float*)take((size_t)n * 4);
+    c->sd_D = (float*)take((size_t)n * 4);
+    c->sd_best = (float*)take((size_t)n * 4);
+    c->sd_bestc = (int*)take((size_t)n * 4);
+    c->sd_bsum = (double*)take(nb * 8);
+    c->sd_centers = (int*)take((size_t)KKM_MAX_K * 4);
+  }
+  const int c_first = (int)std::min<int64_t>((int64_t)std::floor(u[0] * (double)n), n - 1);
+  for (int t = 0; t < k; ++t) {
+    if (t > 0) {
+      int rc = run(c, KKM_PHASE_SEED, "kpp_select", [&] {
+        return launch_kpp_select(c->sd_D, c->sd_bsum, n, u[t], c->sd_centers, t, c->stream);
+      });
+      if (rc) return rc;
+    }
+    int rc = run(c, KKM_PHASE_SEED, "kpp_dist", [&] {
+      return launch_kpp_dist(c->Xp, n, c->sz.d_pad, c->kp, c->sd_centers, t, c_first, c->sd_kd, c->sd_D,
+                             c->sd_best, c->sd_bestc, c->sd_bsum, t == k - 1 ? V : nullptr, c->stream);
+    });
+    if (rc) return rc;
+  }
+  if (centers_out)
+    HIP_TRY(c, hipMemcpyAsync(centers_out, c->sd_centers, (size_t)k * 4, hipMemcpyDeviceToHost, c->stream),
+            "copy centers");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
 }
 
 int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {

@@ -120,6 +120,15 @@ hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int 
                               const unsigned long long* fix_count, long long seg_cap, float* K,
                               hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
+// K-means++ seeding (seed.hip): one distance pass per center, one draw per
+// center after the first; buffers of n (kd, D, best, bestc) and
+// seed_blocks(n) (bsum) entries.
+int seed_blocks(int64_t n);
+hipError_t launch_kpp_dist(const float* Xp, int64_t n, int d_pad, const KappaParams& kp, int* centers, int t,
+                           int c_first, float* kd, float* D, float* best, int* bestc, double* bsum, int* V,
+                           hipStream_t s);
+hipError_t launch_kpp_select(const float* D, const double* bsum, int64_t n, double ut, int* centers, int t,
+                             hipStream_t s);
 hipError_t launch_fill_diag(float* diagK, int64_t n, float v, hipStream_t s);
 
 hipError_t launch_zero_ints(int* p, int64_t count, hipStream_t s);

@@ -20,7 +20,8 @@ KKM_LINEAR, KKM_POLY, KKM_GAUSS = 0, 1, 2
 KKM_MODE_AUTO, KKM_MODE_RESIDENT, KKM_MODE_ONTHEFLY, KKM_MODE_PACKED = 0, 1, 2, 3
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
-PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other")
+PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
+          "seed")
 KINDS = {"linear": KKM_LINEAR, "poly": KKM_POLY, "gauss": KKM_GAUSS}
 MODES = {"auto": KKM_MODE_AUTO, "resident": KKM_MODE_RESIDENT, "onthefly": KKM_MODE_ONTHEFLY,
          "packed": KKM_MODE_PACKED}
@@ -62,6 +63,7 @@ _SIGS = {
     "kkm_iterate": ([_vp, _vp, _i32, _i32, _f64, ctypes.POINTER(_i32), _vp], _i32),
     "kkm_objective": ([_vp, _vp, _i32, ctypes.POINTER(_f64)], _i32),
     "kkm_step": ([_vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(_f64)], _i32),
+    "kkm_init_kmeanspp": ([_vp, _i32, _vp, _vp, _vp], _i32),
     "kkm_copy_kernel_rows": ([_vp, _i64, _i64, _vp], _i32),
     "kkm_copy_diag": ([_vp, _vp], _i32),
     "kkm_set_timing": ([_vp, _i32], _i32),
@@ -187,6 +189,19 @@ def kkm_step(ctx, cl_in, k: int, E=None, z=None, D=None, cl_out=None, counts_out
                           _dev_ptr(D, torch.float32, "D"), _dev_ptr(cl_out, torch.int32, "cl_out"),
                           _dev_ptr(counts_out, torch.int32, "counts_out", int(k)), ctypes.byref(J)), ctx)
     return J.value
+
+
+def kkm_init_kmeanspp(ctx, k: int, u, V) -> np.ndarray:
+    """K-means++ seeding from the uniforms u (k floats in [0, 1)); writes the
+    initial ids into V (device int32[n]) and returns the chosen centers."""
+    import torch
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    if u.shape != (int(k),):
+        raise KKMError(KKM_ERR_ARG, f"u must hold k={k} uniforms, got shape {u.shape}")
+    centers = np.zeros(int(k), dtype=np.int32)
+    _check(lib().kkm_init_kmeanspp(ctx, int(k), u.ctypes.data, centers.ctypes.data,
+                                   _dev_ptr(V, torch.int32, "V")), ctx)
+    return centers
 
 
 def kkm_copy_kernel_rows(ctx, r0: int, r1: int, out) -> None:

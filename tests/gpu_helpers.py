@@ -99,6 +99,13 @@ class Engine:
         it, hist = self.kkm.kkm_iterate(self.ctx, V, k, max_iter, tol)
         return V.cpu().numpy(), it, hist
 
+    def seed(self, k: int, u):
+        """K-means++ seeding: (centers, initial ids) as numpy arrays."""
+        import torch
+        V = torch.full((self.n,), -1, dtype=torch.int32, device="cuda")
+        centers = self.kkm.kkm_init_kmeanspp(self.ctx, k, u, V)
+        return centers, V.cpu().numpy()
+
     def info(self):
         return self.kkm.kkm_get_info(self.ctx)
 

@@ -35,9 +35,10 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 1
+    assert kkm.kkm_abi_version() == 2
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 1" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 2" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
 def test_library_is_built_for_gfx950_only(L):
