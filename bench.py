@@ -88,6 +88,9 @@ def parse():
     ap.add_argument("--config", type=int, default=2, help="workload 1-5 (default 2: n=20000, d=784)")
     ap.add_argument("--mode", choices=["packed", "resident", "onthefly"], default=None,
                     help="K storage (default: packed when k <= 16, else resident)")
+    ap.add_argument("--storage", choices=["f32", "f16"], default="f32",
+                    help="number format of the stored K (f16: binary16 with fp32 sums, a mixed-precision "
+                         "option with its own error bound; the default keeps fp32)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="oracle sample sized for about this much host time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -180,7 +183,7 @@ def main():
     V0 = torch.from_numpy(cl0).cuda()
     Vs = [V0.clone() for _ in range(args.steps + args.warmup)]
     ctx = kkm.kkm_create(kkm.current_stream_handle())
-    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.MODES[args.mode])
+    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.MODES[args.mode], kkm.STORAGES[args.storage])
     kind = kkm.KINDS[w.kind]
 
     def job(V):
@@ -217,12 +220,15 @@ def main():
 
     ms_per_step = 1e3 * (t1 - t0) / args.steps
     value = w.iters / (ms_per_step / 1e3)
+    f16 = args.storage == "f16"
+    traffic_tag = "-f16" if f16 else ""   # counted traffic is kept per storage format
     out = {"metric": METRIC, "value": round(value, 3), "unit": "iters/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
            "data": "synthetic",
-           "config": {"workload": w.describe() + f", K {args.mode}", "n": n, "d": d, "k": k,
-                      "iters": w.iters, "kernel": w.kind, "mode": args.mode, "parallelism": "1 GPU"}}
+           "config": {"workload": w.describe() + f", K {args.mode}" + (", binary16 K" if f16 else ""),
+                      "n": n, "d": d, "k": k, "iters": w.iters, "kernel": w.kind, "mode": args.mode,
+                      "storage": args.storage, "parallelism": "1 GPU"}}
 
     def avg(ph):
         ms, cnt = phases[ph]
@@ -245,11 +251,12 @@ def main():
             # n(n+1)/2 (what symmetry leaves to read; the stored diagonal
             # tiles and column padding count against the kernel)
             kname = "spmm_onehot" if args.mode == "resident" else "spmm_sym"
-            bytes_per = 4.0 * n * n if args.mode == "resident" else 2.0 * n * (n + 1)
+            esize = 2.0 if f16 else 4.0   # bytes per stored entry
+            bytes_per = esize * n * n if args.mode == "resident" else esize * n * (n + 1) / 2
             gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
             out["roofline"] = {"kernel": kname, "bound": "hbm", "achieved": round(gbs, 1),
                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                               "traffic": counted_traffic(kname, args.config, args.mode),
+                               "traffic": counted_traffic(kname, args.config, args.mode + traffic_tag),
                                "traffic_unit": "GB per launch (algorithmic %.4f)" % (bytes_per / 1e9),
                                "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt,
                                "stored_K_bytes": info["bytes_K"]}
@@ -267,7 +274,7 @@ def main():
             out["roofline_kbuild"] = {"kernel": "gemm_kappa", "bound": "mfma", "achieved": tf,
                                       "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
                                       "frac": round(tf / FP32_MFMA_PEAK_TF, 4) if tf else None,
-                                      "traffic": counted_traffic("gemm_kappa", args.config, args.mode),
+                                      "traffic": counted_traffic("gemm_kappa", args.config, args.mode + traffic_tag),
                                       "traffic_unit": "GB per launch", "avg_launch_ms": round(gemm_ms, 5),
                                       "gauss_fixups": info["fixups"]}
     if not args.no_timing:

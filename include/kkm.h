@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 2
+#define KKM_ABI_VERSION 3
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -78,11 +78,27 @@ typedef enum kkm_mode {
 } kkm_mode;
 #define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
 
+/* Number format of a stored K (RESIDENT or PACKED; ONTHEFLY stores nothing
+ * and ignores it).  F32 keeps the fp32 entries.  F16 keeps them in IEEE
+ * binary16, half the bytes to stream per iteration (mixed precision is the
+ * paper's future work, Section VII): entry K(i,j) is stored as
+ * fp16(K(i,j) / w_i), where w_i bounds row i (Cauchy-Schwarz:
+ * |x_i . x_j| <= |x_i| max_m |x_m|; linear w_i = that bound, polynomial
+ * w_i = (|gamma| * bound + |coef0|)^degree, Gaussian w_i = 1 since
+ * 0 < K <= 1), so every stored value lies in [-1, 1] and keeps binary16's
+ * 11 significant bits; reads multiply by w_i again and every sum runs in
+ * fp32.  Each entry then carries a relative error of at most 2^-11, and
+ * E(i,j) an error of at most 2^-11 sum_{m in L_j} |K(i,m)| plus the fp32
+ * accumulation error; diag K, tr K, z's fp64 parts and the distances'
+ * arithmetic stay fp32/fp64. */
+typedef enum kkm_storage { KKM_STORE_F32 = 0, KKM_STORE_F16 = 1 } kkm_storage;
+
 typedef struct kkm_params {
   float gamma;    /* POLY: scale of x.y; GAUSS: > 0.  Ignored for LINEAR. */
   float coef0;    /* POLY: additive constant c.  Ignored otherwise. */
   int32_t degree; /* POLY: integer exponent, 1..16.  Ignored otherwise. */
   int32_t mode;   /* kkm_mode */
+  int32_t storage;/* kkm_storage of a stored K (ignored ONTHEFLY) */
 } kkm_params;
 
 typedef struct kkm_ctx kkm_ctx; /* opaque; owns K, the staged points and all scratch */
@@ -113,6 +129,7 @@ typedef struct kkm_info {
   int64_t n;
   int32_t d, d_pad;       /* feature count and its zero-padded width */
   int32_t kind, mode;     /* kkm_kind, resolved kkm_mode (never AUTO) */
+  int32_t storage;        /* kkm_storage of K (F32 when ONTHEFLY) */
   int64_t ld;             /* RESIDENT: row stride of K in floats; PACKED: the
                              padded row length (row block I holds ld - 128*I
                              columns); ONTHEFLY: row stride of E^T */
@@ -141,10 +158,11 @@ const char *kkm_last_error(const kkm_ctx *ctx);
 /* Pure host planning, no HIP call.  Picks the mode for a problem and the
  * device bytes it needs (K, staged points, per-iteration scratch for k
  * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget.
- * Errors: KKM_ERR_ARG (bad sizes, or PACKED with k > KKM_PACKED_MAX_K),
- * KKM_ERR_OOM (even the on-the-fly mode does not fit, or the requested
- * storing mode does not). */
-int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode,
+ * storage: kkm_storage of K (sizes K and the row scales).
+ * Errors: KKM_ERR_ARG (bad sizes or storage, or PACKED with
+ * k > KKM_PACKED_MAX_K), KKM_ERR_OOM (even the on-the-fly mode does not fit,
+ * or the requested storing mode does not). */
+int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode, int32_t storage,
              int32_t *mode_out, size_t *bytes_out);
 
 /* Host-only argument checks that the entry points apply first; exported so
@@ -156,7 +174,7 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  * X:      device, n x d fp32 row-major.  The engine copies it (zero-padded to
  *         d_pad columns); the caller may free X once this call has returned.
  * n:      points, 1 .. 2^31-1.   d: features, 1 .. 65536.
- * kind:   kkm_kind.   params: host pointer (gamma, coef0, degree, mode).
+ * kind:   kkm_kind.   params: host pointer (gamma, coef0, degree, mode, storage).
  * RESIDENT: stores K (n rows, stride ld) in device memory; diag K is exact
  *   (Gaussian: exactly 1).  Gaussian entries whose expansion
  *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are
@@ -164,6 +182,8 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  * PACKED: as RESIDENT, but only the tiles I <= J of the 128 x 128 tiling
  *   are stored (row i keeps columns 128*floor(i/128) .. ld-1).
  * ONTHEFLY: stages X and row norms only.
+ * storage F16 (RESIDENT, PACKED): K in binary16 with row scales, see
+ *   kkm_storage; diag K stays fp32.
  * Replaces any earlier build on ctx; a build of the same n, d, kind and mode
  * reuses the device buffers of the previous one.  Asynchronous.
  * Errors: KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP. */

@@ -17,9 +17,12 @@
 // waits on another workgroup: every hand-off is a kernel boundary.
 #include "kkm_internal.h"
 
+#include <algorithm>
+
 namespace kkm {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 
 __device__ inline int clamp_id(int c, int k) { return c < 0 ? 0 : (c >= k ? k - 1 : c); }
 
@@ -343,7 +346,11 @@ hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, i
 // to P[q].  A second kernel adds the chunks of each cluster in chunk order;
 // the kernel boundary makes the partial sums visible across XCDs without a
 // device-scope fence per workgroup, which costs more than half the bandwidth.
-__global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restrict__ K, IterBufs b) {
+// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
+// binary16 rows are read 4 entries (8 bytes) per lane, widened and scaled.
+template <typename KT>
+__global__ __launch_bounds__(256) void spmm_onehot_kernel(const KT* __restrict__ K, IterBufs b) {
+  constexpr bool kHalf = sizeof(KT) == 2;
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int q = (int)(blockIdx.x / (unsigned)ns);
@@ -351,7 +358,12 @@ __global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restric
   const int p0 = b.chunk_p0[q], p1 = b.chunk_p1[q];
   const int tid = threadIdx.x;
   __shared__ int rows[kChunk];
-  for (int p = p0 + tid; p < p1; p += 256) rows[p - p0] = b.perm[p];
+  __shared__ float rw[kHalf ? kChunk : 1];
+  for (int p = p0 + tid; p < p1; p += 256) {
+    const int r = b.perm[p];
+    rows[p - p0] = r;
+    if (kHalf) rw[p - p0] = b.kw ? b.kw[r] : 1.f;
+  }
   __syncthreads();
 
   const int64_t ld = b.ld;
@@ -359,17 +371,24 @@ __global__ __launch_bounds__(256) void spmm_onehot_kernel(const float* __restric
   if (col >= ld) return;
   f4 acc = {0.f, 0.f, 0.f, 0.f};
   const int nr = p1 - p0;
-  const float* base = K + col;
+  const KT* base = K + col;
+  auto row = [&](int r) {  // row r of the chunk at this lane's 4 columns
+    if (kHalf) {
+      const h4 v = __builtin_nontemporal_load((const h4*)(base + (int64_t)rows[r] * ld));
+      return __builtin_convertvector(v, f4) * rw[r];
+    } else {
+      return (f4)__builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r] * ld));
+    }
+  };
   int r = 0;
   for (; r + 8 <= nr; r += 8) {
     f4 v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      v[u] = __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r + u] * ld));
+    for (int u = 0; u < 8; ++u) v[u] = row(r + u);
 #pragma unroll
     for (int u = 0; u < 8; ++u) acc += v[u];
   }
-  for (; r < nr; ++r) acc += __builtin_nontemporal_load((const f4*)(base + (int64_t)rows[r] * ld));
+  for (; r < nr; ++r) acc += row(r);
   *(f4*)(b.P + (int64_t)q * ld + col) = acc;
 }
 
@@ -400,9 +419,30 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int*
   if (tid == 0) b.zpart[(int64_t)j * ns + stripe] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s) {
+hipError_t launch_spmm_onehot(const void* K, const IterBufs& b, hipStream_t s) {
   const long long grid = (long long)b.nstripes * b.qmax;
-  hipLaunchKernelGGL(spmm_onehot_kernel, dim3((unsigned)grid), dim3(256), 0, s, K, b);
+  if (b.kf16)
+    hipLaunchKernelGGL(spmm_onehot_kernel<half_t>, dim3((unsigned)grid), dim3(256), 0, s, (const half_t*)K, b);
+  else
+    hipLaunchKernelGGL(spmm_onehot_kernel<float>, dim3((unsigned)grid), dim3(256), 0, s, (const float*)K, b);
+  return hipGetLastError();
+}
+
+// Rows r0 .. r1-1 of a full binary16 K, widened and scaled back to fp32.
+__global__ __launch_bounds__(256) void rows_f16_kernel(const half_t* __restrict__ K, const float* __restrict__ kw,
+                                                       int64_t n, int64_t ld, int64_t r0, int64_t r1,
+                                                       float* __restrict__ out) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= n) return;
+  for (int64_t r = r0 + blockIdx.y; r < r1; r += gridDim.y)
+    out[(r - r0) * n + c] = (float)K[r * ld + c] * (kw ? kw[r] : 1.f);
+}
+
+hipError_t launch_rows_f16(const half_t* K, const float* kw, int64_t n, int64_t ld, int64_t r0, int64_t r1,
+                           float* out, hipStream_t s) {
+  const unsigned gy = (unsigned)std::min<int64_t>(r1 - r0, 65535);
+  hipLaunchKernelGGL(rows_f16_kernel, dim3((unsigned)((n + 255) / 256), gy), dim3(256), 0, s, K, kw, n, ld, r0,
+                     r1, out);
   return hipGetLastError();
 }
 

@@ -37,14 +37,40 @@ __device__ inline void triangle_tile(int64_t t, int64_t nt, int64_t& I, int64_t&
   J = nt - 1 - o;
 }
 
+// Row scales of binary16 storage: |x_i . x_j| <= |x_i| max_m |x_m|
+// (Cauchy-Schwarz), so kw[i] bounds every |K(i, j)|; 1 for a zero row.
+__global__ void row_scales_kernel(const float* __restrict__ nrm, const unsigned* __restrict__ maxnrm_bits,
+                                  int64_t n, KappaParams kp, float* __restrict__ kw) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float dot = sqrtf(nrm[i] * __uint_as_float(*maxnrm_bits));
+  float w = dot;
+  if (kp.kind == POLY) {
+    const float t = fmaf(fabsf(kp.gamma), dot, fabsf(kp.coef0));
+    w = 1.f;
+    for (int e = 0; e < kp.degree; ++e) w *= t;
+  }
+  kw[i] = w > 0.f ? w : 1.f;
+}
+
+hipError_t launch_row_scales(const float* nrm, const unsigned* maxnrm_bits, int64_t n, const KappaParams& kp,
+                             float* kw, hipStream_t s) {
+  hipLaunchKernelGGL(row_scales_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, nrm, maxnrm_bits, n,
+                     kp, kw);
+  return hipGetLastError();
+}
+
 // Four workgroups per CU (40 KB of LDS each): while some run their store
-// epilogue, others keep the matrix cores busy.
-template <int KIND>
+// epilogue, others keep the matrix cores busy.  KT is the storage type of K
+// (float, or binary16 with entry (i, j) divided by kw[i]).
+template <int KIND, typename KT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemm_kappa_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm,
     const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, bool packed,
-    int64_t nt, int64_t T, KappaParams kp, float* __restrict__ K, float* __restrict__ diagK,
-    int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long seg_cap) {
+    int64_t nt, int64_t T, KappaParams kp, KT* __restrict__ K, const float* __restrict__ kw,
+    float* __restrict__ diagK, int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count,
+    long long seg_cap) {
+  constexpr bool kHalf = sizeof(KT) == 2;
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
   // No Gaussian entry can need the fix-up unless the largest norms allow it.
   const bool may_fix = KIND == GAUSS && gauss_needs_fix(1.f, __uint_as_float(*maxnrm_bits),
@@ -110,8 +136,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     }
   }
 
-  // ---- stores, staged through LDS so each instruction writes 256 contiguous
-  //      bytes; non-temporal, since K is not read again by this kernel
+  // ---- stores, staged through LDS so each instruction writes one row's
+  //      contiguous run (256 bytes in fp32, 128 in binary16); non-temporal,
+  //      since K is not read again by this kernel
+  auto put = [&](int64_t gi, float v, KT* dst) {
+    if (kHalf) {
+      const float inv = kw ? 1.f / kw[gi] : 1.f;
+      __builtin_nontemporal_store((KT)(v * inv), dst);
+    } else {
+      __builtin_nontemporal_store((KT)v, dst);
+    }
+  };
   float* Tw = lds + wave * (32 * 65);
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {  // tile (I, J): rows i, columns j
@@ -125,7 +160,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     for (int rr = 0; rr < 32; ++rr) {
       const int64_t gi = row0 + wm * 64 + bi * 32 + rr;
       const int64_t rowp = packed ? packed_row(gi, ld) : gi * ld;
-      if (gi < n && gj < ld) __builtin_nontemporal_store((gj < n) ? Tw[rr * 65 + lane] : 0.f, K + rowp + gj);
+      if (gi < n && gj < ld) put(gi, (gj < n) ? Tw[rr * 65 + lane] : 0.f, K + rowp + gj);
     }
     __syncthreads();
   }
@@ -141,7 +176,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       const int64_t gj = row0 + wm * 64 + lane;  // I < J, so gj < n
       for (int rr = 0; rr < 32; ++rr) {
         const int64_t gi = col0 + wn * 64 + bj * 32 + rr;
-        if (gi < n) __builtin_nontemporal_store(Tw[rr * 65 + lane], K + gi * ld + gj);
+        if (gi < n) put(gi, Tw[rr * 65 + lane], K + gi * ld + gj);
       }
       __syncthreads();
     }
@@ -149,26 +184,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 }
 
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                             int64_t n, int d_pad, int64_t ld, bool packed, const KappaParams& kp,
-                             float* K, float* diagK, int2* fix_list, unsigned long long* fix_count,
-                             long long seg_cap, hipStream_t s) {
+                             int64_t n, int d_pad, int64_t ld, bool packed, bool f16, const float* kw,
+                             const KappaParams& kp, void* K, float* diagK, int2* fix_list,
+                             unsigned long long* fix_count, long long seg_cap, hipStream_t s) {
   const int64_t nt = (n + kTile - 1) / kTile;
   const int64_t T = nt * (nt + 1) / 2;
   dim3 grid((unsigned)T), block(256);
+#define KKM_GEMM_LAUNCH(KIND, TY)                                                                       \
+  hipLaunchKernelGGL((gemm_kappa_kernel<KIND, TY>), grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld, \
+                     packed, nt, T, kp, (TY*)K, kw, diagK, fix_list, fix_count, seg_cap)
   switch (kp.kind) {
     case LINEAR:
-      hipLaunchKernelGGL(gemm_kappa_kernel<LINEAR>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+      if (f16) KKM_GEMM_LAUNCH(LINEAR, half_t);
+      else KKM_GEMM_LAUNCH(LINEAR, float);
       break;
     case POLY:
-      hipLaunchKernelGGL(gemm_kappa_kernel<POLY>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+      if (f16) KKM_GEMM_LAUNCH(POLY, half_t);
+      else KKM_GEMM_LAUNCH(POLY, float);
       break;
     default:
-      hipLaunchKernelGGL(gemm_kappa_kernel<GAUSS>, grid, block, 0, s, Xp, nrm, maxnrm_bits, n, d_pad, ld,
-                         packed, nt, T, kp, K, diagK, fix_list, fix_count, seg_cap);
+      if (f16) KKM_GEMM_LAUNCH(GAUSS, half_t);
+      else KKM_GEMM_LAUNCH(GAUSS, float);
       break;
   }
+#undef KKM_GEMM_LAUNCH
   return hipGetLastError();
 }
 
@@ -180,13 +219,14 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
 // every entry of the upper triangle is re-tested from the stored K with the
 // epilogue's estimate.  The counts are read on the device, so the build needs
 // no host round trip.
+template <typename T>
 __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp,
                                                           const float* __restrict__ nrm, int64_t n,
                                                           int d_pad, int64_t ld, bool packed,
                                                           KappaParams kp,
                                                           const int2* __restrict__ list,
                                                           const unsigned long long* __restrict__ counts,
-                                                          long long seg_cap, float* __restrict__ K) {
+                                                          long long seg_cap, T* __restrict__ K) {
   __shared__ int overflow;
   if (threadIdx.x == 0) overflow = 0;
   __syncthreads();
@@ -220,7 +260,7 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
     s += __shfl_xor(s, 2, 16);
     s += __shfl_xor(s, 1, 16);
     if (gl == 0) {  // listed pairs have i < j: (i, j) is stored in both layouts
-      const float v = __builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
+      const T v = (T)__builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
       if (packed) {
         K[packed_row(ij.x, ld) + ij.y] = v;
         if (ij.x / kTile == ij.y / kTile) K[packed_row(ij.y, ld) + ij.x] = v;
@@ -236,9 +276,9 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
     const float ni = nrm[i];
     const int64_t ri = packed ? packed_row(i, ld) : i * ld;
     for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
-      const float v = K[ri + j];
+      const float v = (float)K[ri + j];
       if (gauss_needs_fix(v, ni, nrm[j], kp)) {
-        const float w = gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
+        const T w = (T)gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
         K[ri + j] = w;
         if (!packed) K[j * ld + i] = w;
         else if (i / kTile == j / kTile) K[packed_row(j, ld) + i] = w;
@@ -248,11 +288,15 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
 }
 
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                              bool packed, const KappaParams& kp, const int2* fix_list,
-                              const unsigned long long* fix_count, long long seg_cap, float* K,
+                              bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
+                              const unsigned long long* fix_count, long long seg_cap, void* K,
                               hipStream_t s) {
-  hipLaunchKernelGGL(gauss_fixup_kernel, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                     ld, packed, kp, fix_list, fix_count, seg_cap, K);
+  if (f16)
+    hipLaunchKernelGGL(gauss_fixup_kernel<half_t>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
+                       ld, packed, kp, fix_list, fix_count, seg_cap, (half_t*)K);
+  else
+    hipLaunchKernelGGL(gauss_fixup_kernel<float>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
+                       ld, packed, kp, fix_list, fix_count, seg_cap, (float*)K);
   return hipGetLastError();
 }
 

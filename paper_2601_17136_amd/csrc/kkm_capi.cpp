@@ -62,9 +62,15 @@ Sizes sizes_for(int64_t n, int32_t d, int mode) {
 size_t staged_bytes(const Sizes& s) {
   return (size_t)s.n_pad * s.d_pad * 4 + (size_t)s.n_pad * 4 + (size_t)s.n * 4 + 64;
 }
-size_t k_bytes(const Sizes& s, int mode) {
-  if (mode == KKM_MODE_PACKED) return (size_t)packed_floats(s.n, s.ld) * 4;
-  return mode == KKM_MODE_RESIDENT ? (size_t)s.n * (size_t)s.ld * 4 : 0;
+// bytes of one stored entry of K
+size_t k_elem(int storage) { return storage == KKM_STORE_F16 ? 2 : 4; }
+size_t k_bytes(const Sizes& s, int mode, int storage) {
+  if (mode == KKM_MODE_PACKED) return (size_t)packed_floats(s.n, s.ld) * k_elem(storage);
+  return mode == KKM_MODE_RESIDENT ? (size_t)s.n * (size_t)s.ld * k_elem(storage) : 0;
+}
+// binary16 storage of the linear and polynomial kernels keeps a scale per row
+bool row_scaled(int mode, int storage, int kind) {
+  return storage == KKM_STORE_F16 && (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) && kind != KKM_GAUSS;
 }
 int chunk_len_for(const Sizes& s, int mode) { return mode == KKM_MODE_PACKED ? sym_chunk_for(s.n) : kChunk; }
 int64_t qmax_for(const Sizes& s, int k, int mode) {
@@ -123,7 +129,10 @@ struct kkm_ctx {
   int d = 0, kind = 0, mode = 0;
   kkm_params params{};
   KappaParams kp{};
-  float *Xp = nullptr, *nrm = nullptr, *diagK = nullptr, *K = nullptr;
+  float *Xp = nullptr, *nrm = nullptr, *diagK = nullptr;
+  void* K = nullptr;          // fp32 or binary16 entries (storage)
+  int storage = KKM_STORE_F32;
+  float* kw = nullptr;        // binary16 row scales (linear, polynomial), else null
   double* trK = nullptr;
   unsigned* maxnrm = nullptr;  // bits of the largest squared norm (next to tr K)
   int2* fix_list = nullptr;
@@ -275,7 +284,9 @@ void free_build(kkm_ctx* c) {
   free_hist(c);
   free_seed(c);
   release(c, c->build_allocs);
-  c->Xp = c->nrm = c->diagK = c->K = nullptr;
+  c->Xp = c->nrm = c->diagK = nullptr;
+  c->K = nullptr;
+  c->kw = nullptr;
   c->trK = nullptr;
   c->fix_list = nullptr;
   c->fix_count = nullptr;
@@ -308,6 +319,8 @@ int carve_ws(kkm_ctx* c, int k) {
   b.chunk_len = chunk_len_for(s, c->mode);
   b.diagK = c->diagK;
   b.trK = c->trK;
+  b.kf16 = c->storage == KKM_STORE_F16;
+  b.kw = c->kw;
   b.Et = (float*)take((size_t)k * s.ld * 4);
   if (c->mode == KKM_MODE_RESIDENT || c->mode == KKM_MODE_PACKED) {
     b.P = (float*)take((size_t)qmax * s.ld * 4);
@@ -468,6 +481,8 @@ int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params* p
   if (!p) return fail(nullptr, KKM_ERR_ARG, "params is NULL");
   if (p->mode < KKM_MODE_AUTO || p->mode > KKM_MODE_PACKED)
     return fail(nullptr, KKM_ERR_ARG, "mode=%d is not AUTO(0), RESIDENT(1), ONTHEFLY(2) or PACKED(3)", p->mode);
+  if (p->storage != KKM_STORE_F32 && p->storage != KKM_STORE_F16)
+    return fail(nullptr, KKM_ERR_ARG, "storage=%d is not F32(0) or F16(1)", p->storage);
   if (kind == KKM_POLY) {
     if (!(std::isfinite(p->gamma) && std::isfinite(p->coef0)))
       return fail(nullptr, KKM_ERR_ARG, "polynomial gamma and coef0 must be finite");
@@ -486,7 +501,7 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter) {
   return KKM_OK;
 }
 
-int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode,
+int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode, int32_t storage,
              int32_t* mode_out, size_t* bytes_out) {
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
     return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
@@ -495,9 +510,11 @@ int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t request
     return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
   if (requested_mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
     return fail(nullptr, KKM_ERR_ARG, "packed storage handles k <= %d, not %d", KKM_PACKED_MAX_K, k);
+  if (storage != KKM_STORE_F32 && storage != KKM_STORE_F16) return fail(nullptr, KKM_ERR_ARG, "bad storage=%d", storage);
   auto need_for = [&](int m) {
     const Sizes s = sizes_for(n, d, m);
-    return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m);
+    const size_t scales = row_scaled(m, storage, KKM_POLY) ? (size_t)n * 4 + 256 : 0;
+    return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m, storage) + scales;
   };
   int mode = requested_mode;
   if (mode == KKM_MODE_AUTO)
@@ -553,19 +570,22 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   for (const Alloc& a : c->ws_allocs) held_by_build += a.bytes;
   for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
   const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
-  if (kkm_plan(n, d, 1, budget_left, params->mode, &mode, &need) != KKM_OK)
+  if (kkm_plan(n, d, 1, budget_left, params->mode, params->storage, &mode, &need) != KKM_OK)
     return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
   collect_timing(c);
   // A rebuild of the same shape keeps every buffer (K alone can be 160 GB,
   // and allocating it costs far more than building it).
-  const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind;
+  const int storage = (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) ? params->storage : KKM_STORE_F32;
+  const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind &&
+                     c->storage == storage;
   if (!reuse) free_build(c);
 
   c->sz = sizes_for(n, d, mode);
   c->d = d;
   c->kind = kind;
   c->mode = mode;
+  c->storage = storage;
   c->params = *params;
   KappaParams& kp = c->kp;
   kp.kind = kind;
@@ -589,8 +609,12 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
     c->maxnrm = (unsigned*)((char*)p + 8);
     const bool stores_k = mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED;
     if (stores_k) {
-      if ((rc = dalloc(c, &p, k_bytes(s, mode), c->build_allocs, "kernel matrix K"))) return rc;
-      c->K = (float*)p;
+      if ((rc = dalloc(c, &p, k_bytes(s, mode, storage), c->build_allocs, "kernel matrix K"))) return rc;
+      c->K = p;
+    }
+    if (row_scaled(mode, storage, kind)) {
+      if ((rc = dalloc(c, &p, (size_t)n * 4, c->build_allocs, "row scales"))) return rc;
+      c->kw = (float*)p;
     }
     if (kind == KKM_GAUSS && stores_k) {
       const long long upper = (long long)(n * (n - 1) / 2);
@@ -623,15 +647,20 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
       return rc;
     return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
   }
+  const bool f16 = storage == KKM_STORE_F16;
+  if (c->kw && (rc = run(c, KKM_PHASE_STAGE, "row_scales", [&] {
+        return launch_row_scales(c->nrm, c->maxnrm, n, kp, c->kw, c->stream);
+      })))
+    return rc;
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
-         return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, kp,
-                                  c->K, c->diagK, c->fix_list, c->fix_count, c->fix_cap / kFixSegs,
-                                  c->stream);
+         return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16,
+                                  c->kw, kp, c->K, c->diagK, c->fix_list, c->fix_count,
+                                  c->fix_cap / kFixSegs, c->stream);
        })))
     return rc;
   if (kind == KKM_GAUSS &&
       (rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
-         return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, kp,
+         return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16, kp,
                                    c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream);
        })))
     return rc;
@@ -775,15 +804,24 @@ int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
   }
   if (c->mode == KKM_MODE_PACKED) {
     int rc = run(c, KKM_PHASE_OTHER, "packed_rows", [&] {
-      return launch_packed_rows(c->K, c->sz.n, c->sz.ld, r0, r1, out, c->stream);
+      return launch_packed_rows(c->K, c->storage == KKM_STORE_F16, c->kw, c->sz.n, c->sz.ld, r0, r1, out,
+                                c->stream);
+    });
+    if (rc) return rc;
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    return KKM_OK;
+  }
+  if (c->storage == KKM_STORE_F16) {
+    int rc = run(c, KKM_PHASE_OTHER, "rows_f16", [&] {
+      return launch_rows_f16((const half_t*)c->K, c->kw, c->sz.n, c->sz.ld, r0, r1, out, c->stream);
     });
     if (rc) return rc;
     HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
     return KKM_OK;
   }
   const size_t row = (size_t)c->sz.n * 4;
-  HIP_TRY(c, hipMemcpy2DAsync(out, row, c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, row, (size_t)(r1 - r0),
-                              hipMemcpyDeviceToDevice, c->stream), "copy rows");
+  HIP_TRY(c, hipMemcpy2DAsync(out, row, (const float*)c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, row,
+                              (size_t)(r1 - r0), hipMemcpyDeviceToDevice, c->stream), "copy rows");
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
   return KKM_OK;
 }
@@ -822,7 +860,8 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   out->kind = c->kind;
   out->mode = c->mode;
   out->ld = c->sz.ld;
-  out->bytes_K = k_bytes(c->sz, c->mode);
+  out->storage = c->storage;
+  out->bytes_K = k_bytes(c->sz, c->mode, c->storage);
   out->bytes_total = c->held;
   if (c->fixups < 0) {
     unsigned long long cnt[kFixSegs] = {0};

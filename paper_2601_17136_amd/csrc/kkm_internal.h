@@ -102,22 +102,33 @@ struct IterBufs {
                         // has label 16nb + li
   int nlb;              // label blocks of 16, ceil(k / 16)
   const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
+  // stored K in binary16: entry (i, j) holds K(i,j) / kw[i] (kw null: 1)
+  int kf16;
+  const float* kw;
 };
+
+// binary16 storage of K
+typedef _Float16 half_t;
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_stage(const float* X, int64_t n, int d, int d_pad, int64_t n_pad, float* Xp,
                         float* nrm, unsigned* maxnrm_bits, hipStream_t s);
+// Row scales of binary16 storage: kw[i] bounds |K(i, j)| for every j
+// (from the row norms and the largest one; linear and polynomial kernels).
+hipError_t launch_row_scales(const float* nrm, const unsigned* maxnrm_bits, int64_t n, const KappaParams& kp,
+                             float* kw, hipStream_t s);
 // packed: store only tiles I <= J, at packed_row(i) + j (no mirror).
+// f16: K is binary16, entry (i, j) stored as K(i,j) / kw[i] (kw null: 1).
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                             int64_t n, int d_pad, int64_t ld, bool packed, const KappaParams& kp,
-                             float* K, float* diagK, int2* fix_list, unsigned long long* fix_count,
-                             long long seg_cap, hipStream_t s);
+                             int64_t n, int d_pad, int64_t ld, bool packed, bool f16, const float* kw,
+                             const KappaParams& kp, void* K, float* diagK, int2* fix_list,
+                             unsigned long long* fix_count, long long seg_cap, hipStream_t s);
 // Recomputes the listed Gaussian entries (counts read on the device); if a
 // segment received more entries than it holds, re-tests the whole triangle.
 // fix_list holds kFixSegs segments of seg_cap entries; fix_count kFixSegs counters.
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
-                              bool packed, const KappaParams& kp, const int2* fix_list,
-                              const unsigned long long* fix_count, long long seg_cap, float* K,
+                              bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
+                              const unsigned long long* fix_count, long long seg_cap, void* K,
                               hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
 // K-means++ seeding (seed.hip): one distance pass per center, one draw per
@@ -141,19 +152,22 @@ hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, cons
                          float* z_out, float* D_out, hipStream_t s);
 hipError_t launch_scatter(const IterBufs& b, const int* cl, const int* counts, int* zero_counts,
                           int* zero_changed, hipStream_t s);
-hipError_t launch_spmm_onehot(const float* K, const IterBufs& b, hipStream_t s);
+hipError_t launch_spmm_onehot(const void* K, const IterBufs& b, hipStream_t s);
+// rows r0 .. r1-1 of a full binary16 K as fp32 (out: (r1-r0) x n)
+hipError_t launch_rows_f16(const half_t* K, const float* kw, int64_t n, int64_t ld, int64_t r0, int64_t r1,
+                           float* out, hipStream_t s);
 hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 
 // packed K (upper block triangle)
 // needs the scatter's crow and mskg for the current ids
-hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s);
+hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s);
 hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
 // E^T from the chunk partials (each starting at its chunk's first stored
 // column) plus the column-side sums Ecol (by point index); zpart per
 // kSymRedStripe columns.
 hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t s);
-hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,
-                              float* out, hipStream_t s);
+hipError_t launch_packed_rows(const void* Kp, bool f16, const float* kw, int64_t n, int64_t ld, int64_t r0,
+                              int64_t r1, float* out, hipStream_t s);
 hipError_t launch_et_to_e(const IterBufs& b, const int* counts, const int* pos, float* E,
                           hipStream_t s);
 

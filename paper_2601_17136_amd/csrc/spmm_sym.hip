@@ -36,19 +36,26 @@
 
 #include <algorithm>
 #include <climits>
+#include <type_traits>
 
 namespace kkm {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
 // 90 VGPRs and ~23 KB (NW = 4) or ~45 KB (NW = 8) of LDS per workgroup:
 // 20 or 16 wavefronts per CU.  Six wavefronts per SIMD (80 VGPRs, spilling)
 // measured slower.
-template <int NB, int NW, int BSEG>
+// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
+// binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
+// when a tile is consumed, so everything after the loads is the same.
+template <int NB, int NW, int BSEG, typename KT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
-    const float* __restrict__ Kp, IterBufs b) {
+    const KT* __restrict__ Kp, IterBufs b) {
+  constexpr bool kHalf = sizeof(KT) == 2;
+  using BufT = typename std::conditional<kHalf, h4, f4>::type;
   constexpr int R = 16 * NW, NT = 64 * NW;
   // With one label block the whole 16 x 128 block is staged at once; with
   // more, the MFMA work per tile is larger and the block goes in two halves,
@@ -89,6 +96,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   __shared__ int rtile[kFull ? 1 : R];
   __shared__ int64_t roff[kFull ? 1 : R];
+  __shared__ float rwl[kHalf && !kFull ? R : 1];  // row scales (binary16, more label blocks)
   __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
   __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
@@ -110,31 +118,34 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   // columns of tile 0) and diagonal tiles are held in registers, so issuing
   // a tile's loads needs no LDS round trip; with more label blocks the
   // registers go to the accumulators and the rows are read from LDS.
-  const float* rbase[8];
+  const KT* rbase[8];
   int rt[8];
+  float rwt[8];
   if (kFull) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       rt[g] = iu[g] >= 0 ? iu[g] / kTile : INT_MAX;
       rbase[g] = Kp + packed_row(iu[g] >= 0 ? iu[g] : 0, ld) + 4 * c32;
+      if (kHalf) rwt[g] = (iu[g] >= 0 && b.kw) ? b.kw[iu[g]] : 1.f;
     }
   } else if (tid < R) {
     const int iv = cr[tid];
     rtile[tid] = iv >= 0 ? iv / kTile : INT_MAX;
     roff[tid] = iv >= 0 ? packed_row(iv, ld) : 0;
+    if (kHalf) rwl[tid] = (iv >= 0 && b.kw) ? b.kw[iv] : 1.f;
   }
-  const float* zp = b.zero + 4 * c32;
-  auto load = [&](f4(&buf)[8], int J) {
+  const KT* zp = (const KT*)b.zero + 4 * c32;
+  auto load = [&](BufT(&buf)[8], int J) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int u = w * 16 + 2 * g + h;
       const bool on = (kFull ? rt[g] : rtile[u]) <= J && J < J_hi;
-      const float* rp = kFull ? rbase[g] + (int64_t)J * kTile : Kp + roff[u] + (int64_t)J * kTile + 4 * c32;
-      buf[g] = __builtin_nontemporal_load((const f4*)(on ? rp : zp));
+      const KT* rp = kFull ? rbase[g] + (int64_t)J * kTile : Kp + roff[u] + (int64_t)J * kTile + 4 * c32;
+      buf[g] = __builtin_nontemporal_load((const BufT*)(on ? rp : zp));
     }
   };
 
-  f4 bb[8];
+  BufT bb[8];
   if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
 #pragma unroll
   for (int m = 0; m < kMpt; ++m)
@@ -147,7 +158,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
   f4* tw = tile[w];
 
-  auto step = [&](f4(&buf)[8], int J, int par) {
+  auto step = [&](BufT(&raw)[8], int J, int par) {
+    f4 buf[8];  // the tile's entries in fp32 (binary16: widened and scaled)
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      if constexpr (kHalf)
+        buf[g] = __builtin_convertvector(raw[g], f4) * (kFull ? rwt[g] : rwl[w * 16 + 2 * g + h]);
+      else
+        buf[g] = raw[g];
+    }
     // row side: this lane's 4 columns over its 8 rows, then the other half-wave's 8
     f4 rs = buf[0];
 #pragma unroll
@@ -189,7 +208,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
         tw[r * 32 + (c32 ^ r)] = buf[g];
       }
       __builtin_amdgcn_sched_barrier(0);
-      load(buf, J + 1);
+      load(raw, J + 1);
       __builtin_amdgcn_sched_barrier(0);
       if (any) mma(0, 8, 0);
     } else {
@@ -204,7 +223,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
         }
         if (half == 1) {
           __builtin_amdgcn_sched_barrier(0);
-          load(buf, J + 1);
+          load(raw, J + 1);
           __builtin_amdgcn_sched_barrier(0);
         }
         if (any) mma(4 * half, 4, 4 * half);
@@ -329,25 +348,36 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
 }
 
 // Rows r0 .. r1-1 of the full K from the packed triangle.
-__global__ __launch_bounds__(256) void packed_rows_kernel(const float* __restrict__ Kp, int64_t n,
-                                                          int64_t ld, int64_t r0, int64_t r1,
+// (binary16: widened and scaled by the row that stores the entry)
+template <typename KT>
+__global__ __launch_bounds__(256) void packed_rows_kernel(const KT* __restrict__ Kp, const float* __restrict__ kw,
+                                                          int64_t n, int64_t ld, int64_t r0, int64_t r1,
                                                           float* __restrict__ out) {
   const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (c >= n) return;
   for (int64_t r = r0 + blockIdx.y; r < r1; r += gridDim.y) {
     const int64_t c0 = (r / kTile) * kTile;
-    out[(r - r0) * n + c] = c >= c0 ? Kp[packed_row(r, ld) + c] : Kp[packed_row(c, ld) + r];
+    const int64_t sr = c >= c0 ? r : c;  // the row that stores K(r, c)
+    const float v = (float)Kp[packed_row(sr, ld) + (c >= c0 ? c : r)];
+    out[(r - r0) * n + c] = kw ? v * kw[sr] : v;
   }
 }
 
 }  // namespace
 
-hipError_t launch_spmm_sym(const float* Kp, const IterBufs& b, hipStream_t s) {
+hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
   const unsigned grid = (unsigned)((int64_t)b.qmax * b.nseg);
   const int nb = b.nlb;
   if (nb != (b.k + 15) / 16) return hipErrorInvalidValue;
-#define KKM_SYM_LAUNCH(NB, NW, S) \
-  hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S>), dim3(grid), dim3(64 * NW), 0, s, Kp, b)
+#define KKM_SYM_LAUNCH(NB, NW, S)                                                                        \
+  do {                                                                                                   \
+    if (b.kf16)                                                                                          \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, half_t>), dim3(grid), dim3(64 * NW), 0, s,            \
+                         (const half_t*)Kp, b);                                                          \
+    else                                                                                                 \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float>), dim3(grid), dim3(64 * NW), 0, s,             \
+                         (const float*)Kp, b);                                                           \
+  } while (0)
   if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
   if (b.bseg != 8 && !(b.bseg == 16 && nb == 1 && b.chunk_len == 128)) return hipErrorInvalidValue;
   const bool tall = b.chunk_len == 128;
@@ -376,12 +406,15 @@ hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t launch_packed_rows(const float* Kp, int64_t n, int64_t ld, int64_t r0, int64_t r1,
-                              float* out, hipStream_t s) {
+hipError_t launch_packed_rows(const void* Kp, bool f16, const float* kw, int64_t n, int64_t ld, int64_t r0,
+                              int64_t r1, float* out, hipStream_t s) {
   const unsigned gy = (unsigned)std::min<int64_t>(r1 - r0, 65535);
-  hipLaunchKernelGGL(packed_rows_kernel, dim3((unsigned)((n + 255) / 256), gy), dim3(256), 0, s, Kp,
-                     n, ld, r0, r1, out);
+  const dim3 grid((unsigned)((n + 255) / 256), gy);
+  if (f16)
+    hipLaunchKernelGGL(packed_rows_kernel<half_t>, grid, dim3(256), 0, s, (const half_t*)Kp, kw, n, ld, r0, r1, out);
+  else
+    hipLaunchKernelGGL(packed_rows_kernel<float>, grid, dim3(256), 0, s, (const float*)Kp, nullptr, n, ld, r0, r1,
+                       out);
   return hipGetLastError();
 }
-
 }  // namespace kkm

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkkm.so")
 KKM_OK, KKM_ERR_ARG, KKM_ERR_OOM, KKM_ERR_HIP, KKM_ERR_STATE, KKM_ERR_DEVICE_DATA = 0, -1, -2, -3, -4, -5
 KKM_LINEAR, KKM_POLY, KKM_GAUSS = 0, 1, 2
 KKM_MODE_AUTO, KKM_MODE_RESIDENT, KKM_MODE_ONTHEFLY, KKM_MODE_PACKED = 0, 1, 2, 3
+KKM_STORE_F32, KKM_STORE_F16 = 0, 1
+STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
@@ -35,7 +37,7 @@ class KKMError(RuntimeError):
 
 class kkm_params(ctypes.Structure):
     _fields_ = [("gamma", ctypes.c_float), ("coef0", ctypes.c_float),
-                ("degree", ctypes.c_int32), ("mode", ctypes.c_int32)]
+                ("degree", ctypes.c_int32), ("mode", ctypes.c_int32), ("storage", ctypes.c_int32)]
 
 
 class kkm_timing(ctypes.Structure):
@@ -44,7 +46,8 @@ class kkm_timing(ctypes.Structure):
 
 class kkm_info(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int32), ("d_pad", ctypes.c_int32),
-                ("kind", ctypes.c_int32), ("mode", ctypes.c_int32), ("ld", ctypes.c_int64),
+                ("kind", ctypes.c_int32), ("mode", ctypes.c_int32), ("storage", ctypes.c_int32),
+                ("ld", ctypes.c_int64),
                 ("bytes_K", ctypes.c_size_t), ("bytes_total", ctypes.c_size_t),
                 ("fixups", ctypes.c_int64), ("fixup_capacity", ctypes.c_int64)]
 
@@ -56,7 +59,7 @@ _SIGS = {
     "kkm_last_error": ([_vp], ctypes.c_char_p),
     "kkm_create": ([ctypes.POINTER(_vp), _vp, _sz], _i32),
     "kkm_destroy": ([_vp], _i32),
-    "kkm_plan": ([_i64, _i32, _i32, _sz, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
+    "kkm_plan": ([_i64, _i32, _i32, _sz, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
     "kkm_check_build_args": ([_i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
     "kkm_check_iterate_args": ([_i64, _i32, _i32], _i32),
     "kkm_build_kernel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
@@ -138,15 +141,16 @@ def kkm_destroy(ctx) -> None:
     _check(lib().kkm_destroy(ctx))
 
 
-def kkm_plan(n: int, d: int, k: int, mem_budget: int, mode: int = KKM_MODE_AUTO):
+def kkm_plan(n: int, d: int, k: int, mem_budget: int, mode: int = KKM_MODE_AUTO, storage: int = KKM_STORE_F32):
     """(resolved mode, device bytes); raises KKMError(KKM_ERR_OOM) if it cannot fit."""
     m, b = _i32(), _sz()
-    _check(lib().kkm_plan(int(n), int(d), int(k), int(mem_budget), int(mode), ctypes.byref(m), ctypes.byref(b)))
+    _check(lib().kkm_plan(int(n), int(d), int(k), int(mem_budget), int(mode), int(storage), ctypes.byref(m),
+                          ctypes.byref(b)))
     return m.value, b.value
 
 
-def make_params(gamma=1.0, coef0=0.0, degree=1, mode=KKM_MODE_AUTO) -> kkm_params:
-    return kkm_params(float(gamma), float(coef0), int(degree), int(mode))
+def make_params(gamma=1.0, coef0=0.0, degree=1, mode=KKM_MODE_AUTO, storage=KKM_STORE_F32) -> kkm_params:
+    return kkm_params(float(gamma), float(coef0), int(degree), int(mode), int(storage))
 
 
 def kkm_check_build_args(n, d, kind, params: kkm_params) -> int:

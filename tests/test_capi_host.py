@@ -35,9 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 2
+    assert kkm.kkm_abi_version() == 3
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 2" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 3" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
@@ -64,6 +64,10 @@ def test_library_is_built_for_gfx950_only(L):
     (1000, 16, kkm.KKM_GAUSS, (-1.0, 0.0, 1, 0), False),
     (1000, 16, kkm.KKM_GAUSS, (float("inf"), 0.0, 1, 0), False),
     (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 5), False),
+    (1000, 16, kkm.KKM_GAUSS, (0.5, 0.0, 1, 1, kkm.KKM_STORE_F16), True),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 3, kkm.KKM_STORE_F16), True),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 1, 2), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 1, -1), False),
 ])
 def test_build_argument_checks(L, n, d, kind, params, ok):
     rc = kkm.kkm_check_build_args(n, d, kind, kkm.make_params(*params))
@@ -122,6 +126,24 @@ def test_plan_packed_holds_half_of_k(L):
     assert e.value.code == kkm.KKM_ERR_ARG
     mode, _ = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO)   # AUTO never picks packed
     assert mode == kkm.KKM_MODE_ONTHEFLY
+
+
+def test_plan_binary16_storage_halves_k(L):
+    """Binary16 storage: 2 bytes per stored entry plus one fp32 row scale per
+    point, so the 200000-point problem fits RESIDENT in 100 GB (80 GB of K)
+    and PACKED in half of that."""
+    n, d, k = 200000, 54, 7
+    mode, need16 = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
+    _, need32 = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F32)
+    assert mode == kkm.KKM_MODE_RESIDENT
+    assert 2 * n * n <= need16 <= 0.51 * need32
+    mode, needp = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
+    assert mode == kkm.KKM_MODE_RESIDENT and needp == need16
+    _, needpk = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_PACKED, kkm.KKM_STORE_F16)
+    assert needpk < 0.53 * need16
+    with pytest.raises(kkm.KKMError) as e:
+        kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, 7)
+    assert e.value.code == kkm.KKM_ERR_ARG
 
 
 def test_plan_reports_oom(L):
