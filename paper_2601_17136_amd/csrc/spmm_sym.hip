@@ -100,7 +100,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
   __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
-  __shared__ h4 onehot[kFull && kHalf ? 16 : 1];  // the 4 bits of a nibble as binary16 0 / 1
+  __shared__ h4 onehot[kHalf ? 16 : 1];  // the 4 bits of a nibble as binary16 0 / 1
 
   const int I0 = i0 / kTile;
   const int J_lo = max(Js, I0), J_hi = Je;
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   BufT bb[8];
   if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
-  if (kFull && kHalf && tid < 16)
+  if (kHalf && tid < 16)
     onehot[tid] = h4{(_Float16)(tid & 1), (_Float16)((tid >> 1) & 1), (_Float16)((tid >> 2) & 1),
                      (_Float16)((tid >> 3) & 1)};
 #pragma unroll
@@ -205,13 +205,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
           }
       }
     };
-    if constexpr (kFull && kHalf) {
-      // binary16, one label block: the raw halves are staged (8-byte chunk c
-      // of row r at c ^ 2r, conflict-free for the row-wise writes and for the
-      // operand reads, which LDS serves 32 lanes at a time) and the column
-      // side runs on v_mfma_f32_16x16x16_f16: 16 columns per instruction, the
-      // one-hot operand from a table of the 16 nibbles; the products are
-      // exact and the sums fp32, and the row's scale is applied at the end.
+    if constexpr (kHalf) {
+      // binary16: the raw halves of the whole block are staged (4 KB per
+      // wavefront; 8-byte chunk c of row r at c ^ 2r, conflict-free for the
+      // row-wise writes and for the operand reads, which LDS serves 32 lanes
+      // at a time) and the column side runs on v_mfma_f32_16x16x16_f16: 16
+      // columns per instruction and label block, the one-hot operand from a
+      // table of the 16 nibbles; the products are exact and the sums fp32,
+      // and the row's scale is applied at the end.
       h4* th = (h4*)tw;
 #pragma unroll
       for (int g = 0; g < 8; ++g) {
@@ -226,8 +227,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
         for (int g = 0; g < 8; ++g) {
           h4 v = th[li * 32 + ((4 * g + lk) ^ (2 * li))];  // row li, columns 16g + 4lk .. +3
           if (diag && dz) v = h4{0, 0, 0, 0};
-          const h4 a = onehot[(msk[0] >> (4 * g)) & 15u];
-          D[0] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, v, D[0], 0, 0, 0);
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const h4 a = onehot[(msk[nb] >> (4 * g)) & 15u];
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, v, D[nb], 0, 0, 0);
+          }
         }
       }
     } else if (kFull) {
@@ -275,9 +279,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   // D[nb][r]: label 16nb + 4lk + r of row um, at its chunk-major position
   // (binary16 on the matrix path: sums of the stored values, times the row's scale)
-  if constexpr (kFull && kHalf) {
+  if constexpr (kHalf) {
     const float wm = (im >= 0 && b.kw) ? b.kw[im] : 1.f;
-    D[0] *= wm;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) D[nb] *= wm;
   }
   const int64_t ecs = (int64_t)b.qmax * R;
   if (im >= 0)

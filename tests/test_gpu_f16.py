@@ -138,7 +138,7 @@ def test_f16_halves_the_stored_bytes():
         assert e.info()["storage"] == 0 and e.info()["bytes_K"] == 0
 
 
-@pytest.mark.parametrize("cfg,mode", [(2, "packed"), (2, "resident"), (3, "packed"), (5, "packed")])
+@pytest.mark.parametrize("cfg,mode", [(2, "packed"), (2, "resident"), (3, "packed"), (4, "packed"), (5, "packed")])
 def test_f16_workload_step(oracle, cfg, mode):
     w_, X, cl = datagen.workload(cfg)
     n, k = w_.n, w_.k
