@@ -41,6 +41,10 @@ CASES = {
     "kmax1024-n3000": (lambda: datagen.make_points(5, n=3000, d=8)[0], 1024, "gauss", 0.125, 0.0, 1, 20),
     # a wide point (d_pad = 2512, 157 k chunks)
     "d2500-n300": (lambda: datagen.make_points(2, n=300, d=2500)[0], 6, "poly", 1.0 / 2500, 1.0, 3, 21),
+    # two and three 16-label blocks in the packed SpMM's column side
+    "k20-n1500-gauss": (lambda: datagen.make_points(2, n=1500, d=24)[0], 20, "gauss", 1.0 / 24, 0.0, 1, 22),
+    "k40-n1800-poly": (lambda: datagen.separated_blobs(1800, 6, 40, seed=6, spread=2.5, sigma=1.0)[0],
+                       40, "poly", 0.2, 1.0, 2, 23),
 }
 
 
