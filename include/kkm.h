@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 3
+#define KKM_ABI_VERSION 4
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -247,6 +247,51 @@ int kkm_step(kkm_ctx *ctx, const int32_t *cl_in, int32_t k, float *E, float *z, 
  * Errors: KKM_ERR_ARG (k outside 1..min(n, KKM_MAX_K), u NULL or outside
  * [0, 1), V NULL), KKM_ERR_STATE (no build), KKM_ERR_OOM, KKM_ERR_HIP. */
 int kkm_init_kmeanspp(kkm_ctx *ctx, int32_t k, const double *u, int32_t *centers_out, int32_t *V);
+
+/* One GPU's share of the 1D split (the paper's 1D algorithm, Section IV-A,
+ * Algorithm 1, with K's symmetry used to hold rows as columns).  GPU g of G
+ * owns the points [c0, c1) and holds the column panel K[:, c0:c1], all n
+ * rows, which by symmetry is its rows of K transposed.  Per update:
+ *   kkm_panel_spmm    E(i, j) = sum_{m: cl(m)=j} K(i, m) for its points i
+ *                     (kept in the context) and its part of the self-terms,
+ *                     zpart_j = sum_{i in [c0,c1), cl(i)=j} E(i, j);
+ *   (exchange)        the caller sums zpart over the G GPUs (an all-reduce of
+ *                     k doubles) and forms z_j = sum_g zpart_j / |L_j|^2;
+ *   kkm_panel_assign  D(i, j) = K(i,i) - 2 E(i,j)/|L_j| + z_j and the new ids
+ *                     of its points (lowest index on ties, +inf for empty j);
+ *   (exchange)        the caller gathers the new ids of all points (an
+ *                     all-gather of 4n bytes) for the next update.
+ * The exchanges are not part of the library.
+ *
+ * kkm_build_panel: as kkm_build_kernel (params->mode is ignored; storage must
+ * be KKM_STORE_F32) for the panel of points [c0, c1): 0 <= c0 < c1 <= n, c0
+ * a multiple of 128.  The panel takes n x round_up(c1 - c0, 128) floats; its
+ * tiles are computed whole (no symmetry saving), the Gaussian diagonal is 1
+ * and flagged Gaussian entries are recomputed from the differences, as in
+ * the full build.  Only the panel's points get diag K.  After it,
+ * kkm_copy_kernel_rows copies rows of the panel ((r1-r0) x (c1-c0)), and
+ * kkm_iterate, kkm_step and kkm_objective return KKM_ERR_STATE.
+ * Errors: KKM_ERR_ARG (as kkm_build_kernel, a bad range, fp16 storage),
+ * KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_build_panel(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t kind,
+                    const kkm_params *params, int64_t c0, int64_t c1);
+
+/* cl: device int32[n], the ids of all points.  zpart: host, k doubles (the
+ * sum over the SpMM's column stripes in order).  counts: host, may be NULL, k
+ * int32: |L_j| over all n points.  Synchronises before returning.
+ * Errors: KKM_ERR_ARG, KKM_ERR_STATE (no panel built), KKM_ERR_DEVICE_DATA
+ * (an id outside [0, k)), KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_panel_spmm(kkm_ctx *ctx, const int32_t *cl, int32_t k, double *zpart, int32_t *counts);
+
+/* z: host, k doubles, the global self-terms (converted to fp32 as the full
+ * step uses them).  cl_out: device int32[c1 - c0], the new ids of the points
+ * c0 .. c1-1.  E_out: device, may be NULL, (c1 - c0) x k fp32 row-major, the
+ * panel's rows of E.  counts_out: host, may be NULL, k int32: how many of the
+ * panel's points took each id.  Uses the sizes and E of the last
+ * kkm_panel_spmm, which must have had the same k.  Synchronises before
+ * returning.  Errors: KKM_ERR_ARG, KKM_ERR_STATE, KKM_ERR_HIP. */
+int kkm_panel_assign(kkm_ctx *ctx, int32_t k, const double *z, int32_t *cl_out, float *E_out,
+                     int32_t *counts_out);
 
 /* Rows r0 .. r1-1 of K into out (device, (r1-r0) x n fp32 row-major).  In
  * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses;

@@ -164,6 +164,60 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
 
 static size_t assign_smem(int k) { return (size_t)k * 20 + 64; }
 
+// Panel points, one per thread: D(i,j) = K(i,i) - 2 E(i,j)/|L_j| + z_j for
+// nonempty j (the full-step assign's formula, with z given), lowest-index
+// argmin; the new sizes are counted per workgroup in LDS.
+__global__ __launch_bounds__(256) void panel_assign_kernel(IterBufs b, const float* __restrict__ z,
+                                                           const int* __restrict__ counts,
+                                                           int* __restrict__ cl_out,
+                                                           int* __restrict__ counts_out,
+                                                           float* __restrict__ E_out) {
+  extern __shared__ float psm[];
+  const int k = b.k, tid = threadIdx.x;
+  float* zf = psm;                // k
+  float* sc = zf + k;             // k
+  int* hist = (int*)(sc + k);     // k
+  for (int j = tid; j < k; j += 256) {
+    const int c = counts[j];
+    zf[j] = z[j];
+    sc[j] = c > 0 ? -2.0f / (float)c : 0.f;
+    hist[j] = 0;
+  }
+  __syncthreads();
+  const int64_t u = (int64_t)blockIdx.x * 256 + tid;  // the panel's point col0 + u
+  if (u < b.ncol) {
+    const float dg = b.diagK[b.col0 + u];
+    float best = INFINITY;
+    int arg = -1;
+    for (int j = 0; j < k; ++j) {
+      const float e = b.Et[(int64_t)j * b.ld + u];
+      if (E_out) E_out[u * k + j] = e;
+      const float s = sc[j];
+      if (s != 0.f) {
+        const float Dv = fmaf(s, e, dg + zf[j]);
+        if (arg < 0 || Dv < best) {
+          best = Dv;
+          arg = j;
+        }
+      }
+    }
+    const int lab = arg < 0 ? 0 : arg;
+    cl_out[u] = lab;
+    atomicAdd(&hist[lab], 1);
+  }
+  __syncthreads();
+  for (int j = tid; j < k; j += 256)
+    if (hist[j]) atomicAdd(&counts_out[j], hist[j]);
+}
+
+hipError_t launch_panel_assign(const IterBufs& b, const float* z, const int* counts, int* cl_out,
+                               int* counts_out, float* E_out, hipStream_t s) {
+  const unsigned grid = (unsigned)((b.ncol + 255) / 256);
+  hipLaunchKernelGGL(panel_assign_kernel, dim3(grid), dim3(256), (size_t)b.k * 12, s, b, z, counts, cl_out,
+                     counts_out, E_out);
+  return hipGetLastError();
+}
+
 hipError_t launch_assign(int mode, const IterBufs& b, const int* counts_in, const int* cl_in,
                          const int* pos, int* cl_out, int* counts_out, int* changed, double* obj,
                          float* z_out, float* D_out, hipStream_t s) {
@@ -411,7 +465,7 @@ __global__ __launch_bounds__(256) void spmm_reduce_kernel(IterBufs b, const int*
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-      if (col + c < b.n && cl[col + c] == j) zs += (double)e[c];
+      if (col + c < b.ncol && cl[b.col0 + col + c] == j) zs += (double)e[c];
   }
   for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off, 64);
   if ((tid & 63) == 0) red[tid >> 6] = zs;

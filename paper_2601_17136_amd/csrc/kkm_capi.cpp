@@ -125,6 +125,8 @@ struct kkm_ctx {
   std::string err;
 
   bool built = false;
+  int64_t pc0 = 0, pc1 = 0;  // a panel (one GPU's share): its points [pc0, pc1); pc1 = 0 otherwise
+  bool panel_e = false;       // the panel's E^T and sizes are current (kkm_panel_spmm ran)
   Sizes sz{};
   int d = 0, kind = 0, mode = 0;
   kkm_params params{};
@@ -292,6 +294,8 @@ void free_build(kkm_ctx* c) {
   c->fix_count = nullptr;
   c->fix_cap = 0;
   c->built = false;
+  c->pc0 = c->pc1 = 0;
+  c->panel_e = false;
 }
 
 // Allocate one block and carve it (keeps the accounting to one number).
@@ -318,6 +322,8 @@ int carve_ws(kkm_ctx* c, int k) {
   b.qmax = (int)qmax;
   b.chunk_len = chunk_len_for(s, c->mode);
   b.diagK = c->diagK;
+  b.col0 = c->pc1 > 0 ? c->pc0 : 0;
+  b.ncol = c->pc1 > 0 ? c->pc1 - c->pc0 : s.n;
   b.trK = c->trK;
   b.kf16 = c->storage == KKM_STORE_F16;
   b.kw = c->kw;
@@ -458,6 +464,7 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
 int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
+  if (c->pc1 > 0) return fail(c, KKM_ERR_STATE, "the context holds a panel of K; use kkm_panel_spmm / kkm_panel_assign");
   if (kkm_check_iterate_args(c->sz.n, k, max_iter) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
   if (c->mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
     return fail(c, KKM_ERR_ARG, "k=%d exceeds %d, the most the packed storage handles; build RESIDENT or ONTHEFLY",
@@ -558,30 +565,49 @@ int kkm_destroy(kkm_ctx* c) {
   return KKM_OK;
 }
 
-int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params) {
+}  // extern "C"
+
+namespace {
+
+// The build of the full K (pc1 = 0) or of the column panel K[:, pc0 : pc1)
+// of one GPU's share (resident, fp32).
+int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
+               int64_t pc0, int64_t pc1) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (kkm_check_build_args(n, d, kind, params) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
   if (!X) return fail(c, KKM_ERR_ARG, "X is NULL");
-  int32_t mode = 0;
+  const bool panel = pc1 > 0;
+  int32_t mode = KKM_MODE_RESIDENT;
   size_t need = 0;
-  // plan with k = 1: the k-dependent scratch is sized when kkm_iterate is called
-  size_t held_by_build = 0;
-  for (const Alloc& a : c->build_allocs) held_by_build += a.bytes;
-  for (const Alloc& a : c->ws_allocs) held_by_build += a.bytes;
-  for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
-  const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
-  if (kkm_plan(n, d, 1, budget_left, params->mode, params->storage, &mode, &need) != KKM_OK)
-    return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
+  if (panel) {
+    if (params->storage != KKM_STORE_F32) return fail(c, KKM_ERR_ARG, "a panel is stored in fp32");
+  } else {
+    // plan with k = 1: the k-dependent scratch is sized when kkm_iterate is called
+    size_t held_by_build = 0;
+    for (const Alloc& a : c->build_allocs) held_by_build += a.bytes;
+    for (const Alloc& a : c->ws_allocs) held_by_build += a.bytes;
+    for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
+    const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
+    if (kkm_plan(n, d, 1, budget_left, params->mode, params->storage, &mode, &need) != KKM_OK)
+      return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
+  }
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
   collect_timing(c);
   // A rebuild of the same shape keeps every buffer (K alone can be 160 GB,
   // and allocating it costs far more than building it).
   const int storage = (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) ? params->storage : KKM_STORE_F32;
   const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind &&
-                     c->storage == storage;
+                     c->storage == storage && c->pc0 == pc0 && c->pc1 == pc1;
   if (!reuse) free_build(c);
 
   c->sz = sizes_for(n, d, mode);
+  if (panel) {  // the panel's columns: a multiple of kTile, so its tiles store whole
+    c->sz.ld = round_up(pc1 - pc0, kTile);
+    c->sz.nstripes = (int)((c->sz.ld + kStripe - 1) / kStripe);
+  }
+  c->pc0 = pc0;
+  c->pc1 = pc1;
+  c->panel_e = false;
   c->d = d;
   c->kind = kind;
   c->mode = mode;
@@ -617,7 +643,7 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
       c->kw = (float*)p;
     }
     if (kind == KKM_GAUSS && stores_k) {
-      const long long upper = (long long)(n * (n - 1) / 2);
+      const long long upper = panel ? (long long)(n * (pc1 - pc0)) : (long long)(n * (n - 1) / 2);
       long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
       const size_t room = c->budget > c->held ? c->budget - c->held : 0;
       cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
@@ -653,6 +679,10 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
       })))
     return rc;
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
+         if (panel)
+           return launch_gemm_kappa_panel(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, pc0, pc1, s.ld, kp,
+                                          (float*)c->K, c->diagK, c->fix_list, c->fix_count,
+                                          c->fix_cap / kFixSegs, c->stream);
          return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16,
                                   c->kw, kp, c->K, c->diagK, c->fix_list, c->fix_count,
                                   c->fix_cap / kFixSegs, c->stream);
@@ -661,10 +691,89 @@ int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t k
   if (kind == KKM_GAUSS &&
       (rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
          return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16, kp,
-                                   c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream);
+                                   c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream, pc0, pc1);
        })))
     return rc;
+  if (panel) return KKM_OK;  // diag K is set for the panel's points only; no trace
   return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
+}
+
+}  // namespace
+
+extern "C" {
+
+int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params) {
+  return build_impl(c, X, n, d, kind, params, 0, 0);
+}
+
+int kkm_build_panel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
+                    int64_t c0, int64_t c1) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (c0 < 0 || c0 % kTile || c1 <= c0 || c1 > n)
+    return fail(c, KKM_ERR_ARG, "bad panel [%lld, %lld): needs 0 <= c0 < c1 <= n=%lld, c0 a multiple of %d",
+                (long long)c0, (long long)c1, (long long)n, kTile);
+  return build_impl(c, X, n, d, kind, params, c0, c1);
+}
+
+int kkm_panel_spmm(kkm_ctx* c, const int32_t* cl, int32_t k, double* zpart, int32_t* counts) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no panel built on this context");
+  if (kkm_check_iterate_args(c->sz.n, k, 1) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  if (!cl || !zpart) return fail(c, KKM_ERR_ARG, "cl or zpart is NULL");
+  int rc;
+  c->panel_e = false;
+  if ((rc = ensure_ws(c, k, 1))) return rc;
+  if ((rc = label_pass(c, cl))) return rc;  // sizes of cl in counts[0], per-block histograms
+  IterBufs& b = c->ib;
+  if ((rc = run(c, KKM_PHASE_SCATTER, "scatter", [&] {
+         return launch_scatter(b, cl, c->counts[0], c->counts[1], c->changed, c->stream);
+       })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce", [&] { return launch_spmm_reduce(b, cl, c->stream); })))
+    return rc;
+  std::vector<double> parts((size_t)k * b.nzpart);
+  int status = 0;
+  HIP_TRY(c, hipMemcpyAsync(parts.data(), b.zpart, parts.size() * sizeof(double), hipMemcpyDeviceToHost, c->stream),
+          "read z parts");
+  if (counts)
+    HIP_TRY(c, hipMemcpyAsync(counts, c->counts[0], (size_t)k * 4, hipMemcpyDeviceToHost, c->stream), "read sizes");
+  HIP_TRY(c, hipMemcpyAsync(&status, b.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if ((rc = status_error(c, status))) return rc;
+  for (int j = 0; j < k; ++j) {  // the stripes in order
+    double zs = 0.0;
+    for (int x = 0; x < b.nzpart; ++x) zs += parts[(size_t)j * b.nzpart + x];
+    zpart[j] = zs;
+  }
+  c->panel_e = true;
+  return KKM_OK;
+}
+
+int kkm_panel_assign(kkm_ctx* c, int32_t k, const double* z, int32_t* cl_out, float* E_out, int32_t* counts_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no panel built on this context");
+  if (!c->panel_e || c->ib.k != k) return fail(c, KKM_ERR_STATE, "kkm_panel_spmm with this k must come first");
+  if (!z || !cl_out) return fail(c, KKM_ERR_ARG, "z or cl_out is NULL");
+  IterBufs& b = c->ib;
+  // z goes to the device through the (now read) reduction parts: k floats
+  std::vector<float> zf((size_t)k);
+  for (int j = 0; j < k; ++j) zf[j] = (float)z[j];
+  float* zd = (float*)b.zpart;
+  int rc;
+  HIP_TRY(c, hipMemcpyAsync(zd, zf.data(), (size_t)k * 4, hipMemcpyHostToDevice, c->stream), "write z");
+  if ((rc = run(c, KKM_PHASE_ASSIGN, "zero", [&] { return launch_zero_ints(c->counts[1], k, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_ASSIGN, "panel_assign", [&] {
+         return launch_panel_assign(b, zd, c->counts[0], cl_out, c->counts[1], E_out, c->stream);
+       })))
+    return rc;
+  if (counts_out)
+    HIP_TRY(c, hipMemcpyAsync(counts_out, c->counts[1], (size_t)k * 4, hipMemcpyDeviceToHost, c->stream),
+            "read sizes");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
 }
 
 int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
@@ -794,6 +903,13 @@ int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
   if (!out || r0 < 0 || r1 > c->sz.n || r0 > r1) return fail(c, KKM_ERR_ARG, "bad row range [%lld, %lld)", (long long)r0, (long long)r1);
   if (r1 == r0) return KKM_OK;
+  if (c->pc1 > 0) {  // a panel: its c1 - c0 columns of each row
+    const size_t w = (size_t)(c->pc1 - c->pc0) * 4;
+    HIP_TRY(c, hipMemcpy2DAsync(out, w, (const float*)c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, w,
+                                (size_t)(r1 - r0), hipMemcpyDeviceToDevice, c->stream), "copy panel rows");
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    return KKM_OK;
+  }
   if (c->mode == KKM_MODE_ONTHEFLY) {
     int rc = run(c, KKM_PHASE_OTHER, "kernel_rows", [&] {
       return launch_kernel_rows(c->Xp, c->nrm, c->maxnrm, c->sz.n, c->sz.d_pad, c->kp, r0, r1, out, c->stream);

@@ -70,6 +70,8 @@ struct IterBufs {
   int64_t n, ld;
   int k, nblk, nstripes, qmax;
   int chunk_len;        // rows per SpMM chunk: kChunk, or sym_chunk_for(n) when K is packed
+  int64_t col0, ncol;   // the points whose columns E^T covers: [col0, col0 + ncol)
+                        // (all n from 0, except on a panel: one GPU's share)
   const float* diagK;   // n
   const double* trK;    // 1
   float* Et;            // k x ld: E transposed, E(i,j) at Et[j*ld + i]
@@ -129,7 +131,20 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
                               bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, void* K,
-                              hipStream_t s);
+                              hipStream_t s, int64_t c0 = 0, int64_t c1 = 0);
+// One GPU's share of the 1D split: the column panel K[:, c0 : c0 + ld) (c0 a
+// multiple of kTile, c1 <= n, columns from c1 on stored as 0), fp32, row
+// stride ld; diagK of the panel's points; Gaussian entries to fix listed as
+// (i, j) with j the global column (launch_gauss_fixup with the same c0, c1).
+hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
+                                   int64_t n, int d_pad, int64_t c0, int64_t c1, int64_t ld,
+                                   const KappaParams& kp, float* K, float* diagK, int2* fix_list,
+                                   unsigned long long* fix_count, long long seg_cap, hipStream_t s);
+// D and lowest-index argmin for the panel's points (columns [b.col0, b.col0 + b.ncol))
+// from E^T (k x ld, column = point - col0), the global z and the cluster sizes;
+// counts_out gets the panel's share of the new sizes (added; zeroed by the caller).
+hipError_t launch_panel_assign(const IterBufs& b, const float* z, const int* counts, int* cl_out,
+                               int* counts_out, float* E_out, hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
 // K-means++ seeding (seed.hip): one distance pass per center, one draw per
 // center after the first; buffers of n (kd, D, best, bestc) and

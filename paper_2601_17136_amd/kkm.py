@@ -67,6 +67,9 @@ _SIGS = {
     "kkm_objective": ([_vp, _vp, _i32, ctypes.POINTER(_f64)], _i32),
     "kkm_step": ([_vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(_f64)], _i32),
     "kkm_init_kmeanspp": ([_vp, _i32, _vp, _vp, _vp], _i32),
+    "kkm_build_panel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params), _i64, _i64], _i32),
+    "kkm_panel_spmm": ([_vp, _vp, _i32, _vp, _vp], _i32),
+    "kkm_panel_assign": ([_vp, _i32, _vp, _vp, _vp, _vp], _i32),
     "kkm_copy_kernel_rows": ([_vp, _i64, _i64, _vp], _i32),
     "kkm_copy_diag": ([_vp, _vp], _i32),
     "kkm_set_timing": ([_vp, _i32], _i32),
@@ -193,6 +196,36 @@ def kkm_step(ctx, cl_in, k: int, E=None, z=None, D=None, cl_out=None, counts_out
                           _dev_ptr(D, torch.float32, "D"), _dev_ptr(cl_out, torch.int32, "cl_out"),
                           _dev_ptr(counts_out, torch.int32, "counts_out", int(k)), ctypes.byref(J)), ctx)
     return J.value
+
+
+def kkm_build_panel(ctx, X, n: int, d: int, kind: int, params: kkm_params, c0: int, c1: int) -> None:
+    """One GPU's share: the column panel K[:, c0:c1] (c0 a multiple of 128)."""
+    import torch
+    _check(lib().kkm_build_panel(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
+                                 int(kind), ctypes.byref(params), int(c0), int(c1)), ctx)
+
+
+def kkm_panel_spmm(ctx, cl, k: int):
+    """E for the panel's points (kept); returns (zpart as numpy fp64[k], sizes as numpy int32[k])."""
+    import torch
+    zpart = np.zeros(int(k), dtype=np.float64)
+    counts = np.zeros(int(k), dtype=np.int32)
+    _check(lib().kkm_panel_spmm(ctx, _dev_ptr(cl, torch.int32, "cl"), int(k), zpart.ctypes.data,
+                                counts.ctypes.data), ctx)
+    return zpart, counts
+
+
+def kkm_panel_assign(ctx, k: int, z, cl_out, E_out=None) -> np.ndarray:
+    """New ids of the panel's points into cl_out from the global z; returns
+    how many of them took each id (numpy int32[k])."""
+    import torch
+    z = np.ascontiguousarray(z, dtype=np.float64)
+    if z.shape != (int(k),):
+        raise KKMError(KKM_ERR_ARG, f"z must hold k={k} values, got shape {z.shape}")
+    counts = np.zeros(int(k), dtype=np.int32)
+    _check(lib().kkm_panel_assign(ctx, int(k), z.ctypes.data, _dev_ptr(cl_out, torch.int32, "cl_out"),
+                                  _dev_ptr(E_out, torch.float32, "E_out"), counts.ctypes.data), ctx)
+    return counts
 
 
 def kkm_init_kmeanspp(ctx, k: int, u, V) -> np.ndarray:

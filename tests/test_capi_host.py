@@ -35,9 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 3
+    assert kkm.kkm_abi_version() == 4
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 3" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 4" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
