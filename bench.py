@@ -98,6 +98,9 @@ def parse():
                     help="oracle sample sized for about this much host time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not record per-kernel events")
+    ap.add_argument("--panel", type=int, default=0, metavar="G",
+                    help="measure one GPU's share of a G-GPU 1D split instead: GPU 0's column panel "
+                         "of K (n x n/G), its build and its updates, without the exchanges")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB (a known-size "
                          "reference for memory-traffic counters)")
@@ -182,6 +185,9 @@ def main():
         print(f"bench: calibration copy of {args.copy_calibration} MiB done", file=sys.stderr, flush=True)
         del src, dst
         torch.cuda.empty_cache()
+    if args.panel:
+        panel_main(args, w, X, cl0, kkm, torch)
+        return
     Xd = torch.from_numpy(X).cuda()
     V0 = torch.from_numpy(cl0).cuda()
     Vs = [V0.clone() for _ in range(args.steps + args.warmup)]
@@ -286,6 +292,80 @@ def main():
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline_sized(w, X, cl0, args.cpu_seconds)
     kkm.kkm_destroy(ctx)
+    print(json.dumps(out), flush=True)
+
+
+def panel_main(args, w, X, cl0, kkm, torch):
+    """One GPU's share of a G-GPU 1D split at its real shape: GPU 0's points
+    [0, c1) (the first of G ranges cut at multiples of 128), the column panel
+    K[:, 0:c1] built and updated on this GPU.  The exchanges a multi-GPU run
+    adds (an all-reduce of k doubles, an all-gather of 4n bytes) are replaced
+    by their local stand-ins: this GPU's z parts alone, and its new ids copied
+    into the id vector."""
+    import numpy as np
+    n, d, k, G = w.n, w.d, w.k, args.panel
+    c1 = n if G == 1 else max(128, (n // G) // 128 * 128)
+    Xd = torch.from_numpy(X).cuda()
+    V = torch.from_numpy(cl0).cuda()
+    cl_out = torch.empty(c1, dtype=torch.int32, device="cuda")
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.KKM_MODE_RESIDENT)
+    kind = kkm.KINDS[w.kind]
+
+    def build():
+        kkm.kkm_build_panel(ctx, Xd, n, d, kind, params, 0, c1)
+
+    def update():
+        zpart, counts = kkm.kkm_panel_spmm(ctx, V, k)
+        c = counts.astype(np.float64)
+        z = np.where(counts > 0, zpart / np.where(counts > 0, c * c, 1.0), 0.0)
+        kkm.kkm_panel_assign(ctx, k, z, cl_out)
+        V[:c1].copy_(cl_out)
+
+    for _ in range(args.warmup):
+        build()
+        update()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        build()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(args.steps * w.iters):
+        update()
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    kkm.kkm_set_timing(ctx, kkm.phase_mask("gemm", "spmm"))
+    build()
+    for _ in range(w.iters):
+        update()
+    ph = kkm.kkm_get_timing(ctx)
+    kkm.kkm_set_timing(ctx, 0)
+    kkm.kkm_destroy(ctx)
+    upd_ms = 1e3 * (t2 - t1) / (args.steps * w.iters)
+    build_ms = 1e3 * (t1 - t0) / args.steps
+    spmm_ms = ph["spmm"][0] / max(ph["spmm"][1], 1)
+    gemm_ms = ph["gemm"][0] / max(ph["gemm"][1], 1)
+    nbytes = 4.0 * n * c1                      # the panel, read once per update
+    flops = 2.0 * n * c1 * d                   # every tile of the panel (no symmetry inside it)
+    gbs = nbytes / (spmm_ms * 1e-3) / 1e9
+    tf = flops / (gemm_ms * 1e-3) / 1e12
+    out = {"metric": "one GPU's share of a %d-GPU 1D split: updates/s of its panel" % G,
+           "value": round(1e3 / upd_ms, 3), "unit": "updates/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(upd_ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": w.describe() + f", GPU 0 of {G}: column panel K[:, 0:{c1}]",
+                      "n": n, "d": d, "k": k, "panel_points": c1, "panel_bytes": int(nbytes),
+                      "parallelism": f"1 GPU's share of {G} (exchanges not included)"},
+           "panel_build_ms": round(build_ms, 4),
+           "roofline": {"kernel": "spmm_onehot (panel)", "bound": "hbm", "achieved": round(gbs, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "traffic": None, "traffic_unit": "GB per launch (algorithmic %.3f)" % (nbytes / 1e9),
+                        "avg_launch_ms": round(spmm_ms, 5), "launches": ph["spmm"][1]},
+           "roofline_kbuild": {"kernel": "gemm_kappa (panel)", "bound": "mfma", "achieved": round(tf, 2),
+                               "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
+                               "frac": round(tf / FP32_MFMA_PEAK_TF, 4), "avg_launch_ms": round(gemm_ms, 5),
+                               "work": "2 n c1 d flop (the panel's tiles)"}}
     print(json.dumps(out), flush=True)
 
 
