@@ -249,9 +249,9 @@ int kkm_step(kkm_ctx *ctx, const int32_t *cl_in, int32_t k, float *E, float *z, 
 int kkm_init_kmeanspp(kkm_ctx *ctx, int32_t k, const double *u, int32_t *centers_out, int32_t *V);
 
 /* One GPU's share of the 1D split (the paper's 1D algorithm, Section IV-A,
- * Algorithm 1, with K's symmetry used to hold rows as columns).  GPU g of G
- * owns the points [c0, c1) and holds the column panel K[:, c0:c1], all n
- * rows, which by symmetry is its rows of K transposed.  Per update:
+ * Algorithm 1: each process holds the column block of K for its points and
+ * the ids of all points).  GPU g of G owns the points [c0, c1) and holds the
+ * column panel K[:, c0:c1], all n rows.  Per update:
  *   kkm_panel_spmm    E(i, j) = sum_{m: cl(m)=j} K(i, m) for its points i
  *                     (kept in the context) and its part of the self-terms,
  *                     zpart_j = sum_{i in [c0,c1), cl(i)=j} E(i, j);
