@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 4
+#define KKM_ABI_VERSION 5
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -138,6 +138,9 @@ typedef struct kkm_info {
   int64_t fixups;         /* Gaussian entries flagged for recomputation at build */
   int64_t fixup_capacity; /* entries the fix-up list holds; beyond it the whole
                              triangle is re-tested instead */
+  int64_t r0, r1, c0, c1; /* the stored rows [r0, r1) and columns [c0, c1) of K:
+                             a panel or block (kkm_build_panel, kkm_build_block),
+                             else 0, n, 0, n */
 } kkm_info;
 
 /* Create a context on the current HIP device.
@@ -292,6 +295,71 @@ int kkm_panel_spmm(kkm_ctx *ctx, const int32_t *cl, int32_t k, double *zpart, in
  * returning.  Errors: KKM_ERR_ARG, KKM_ERR_STATE, KKM_ERR_HIP. */
 int kkm_panel_assign(kkm_ctx *ctx, int32_t k, const double *z, int32_t *cl_out, float *E_out,
                      int32_t *counts_out);
+
+/* One GPU's share of the 1.5D split (the paper's 1.5D algorithm, Section
+ * IV-C, Algorithm 2: K is computed by SUMMA and stays 2D-partitioned over a
+ * sqrt(P) x sqrt(P) process grid; V stays 1D-partitioned).  The points are
+ * cut into sqrt(P) contiguous blocks, and each block into sqrt(P) pieces
+ * (the 1D partition, P pieces in all).  Process (i, j) holds the block
+ * K[rows of block i, columns of block j] and owns piece l = i of column
+ * block j.  Per update:
+ *   (exchange)        the caller gathers the ids of row block i on each
+ *                     process of grid row i (an all-gather along the row);
+ *   kkm_block_spmm    the partial E(u, j') = sum over the block's rows r with
+ *                     cl(r) = j' of K(r, u), for its columns u;
+ *   (exchange)        the caller sums the partials of grid column j and
+ *                     splits them by columns (a reduce-scatter along the
+ *                     column): each process gets E of its own piece;
+ *   kkm_block_zpart   its piece's part of the self-terms and its sizes;
+ *   (exchange)        the caller sums both over all processes (an
+ *                     all-reduce of k doubles and k ints) and forms
+ *                     z_j = sum zpart_j / |L_j|^2;
+ *   kkm_block_assign  D(u, j) = K(u,u) - 2 E(u,j)/|L_j| + z_j and the new ids
+ *                     of its piece (lowest index on ties, +inf for empty j).
+ * The ids of a piece are the process's own part of V; the exchanges are not
+ * part of the library.  The 1D split's panel is the block of all rows
+ * (kkm_build_panel); these calls also run on it.
+ *
+ * kkm_build_block: as kkm_build_panel for the block rows [r0, r1) x columns
+ * [c0, c1): 0 <= r0 < r1 <= n and 0 <= c0 < c1 <= n, r0 and c0 multiples of
+ * 128.  The block takes (r1 - r0) x round_up(c1 - c0, 128) floats.  diag K is
+ * set for every point, from the staged norms (Gaussian: 1).  A rebuild with
+ * blocks of the same size keeps the buffers.  After it, kkm_copy_kernel_rows
+ * copies rows r0 <= r < r1 of the block ((r1-r0) x (c1-c0)); the full-K and
+ * panel calls return KKM_ERR_STATE.
+ * Errors: KKM_ERR_ARG (as kkm_build_kernel, a bad range, fp16 storage),
+ * KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_build_block(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t kind,
+                    const kkm_params *params, int64_t r0, int64_t r1, int64_t c0, int64_t c1);
+
+/* cl: device int32[r1 - r0], the ids of the block's rows r0 .. r1-1.  E_out:
+ * device, (c1 - c0) x k fp32 row-major (point-major, so that the columns of a
+ * piece are contiguous for the reduce-scatter): E_out[u*k + j] = sum over
+ * r in [r0, r1) with cl[r - r0] = j of K(r, c0 + u), 0 for an id no row
+ * holds; summed in a fixed order.  Synchronises before returning.
+ * Errors: KKM_ERR_ARG, KKM_ERR_STATE (no block built), KKM_ERR_DEVICE_DATA
+ * (an id outside [0, k)), KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_block_spmm(kkm_ctx *ctx, const int32_t *cl, int32_t k, float *E_out);
+
+/* The piece [a0, a1) of the block's columns (c0 <= a0 < a1 <= c1).  E:
+ * device, (a1 - a0) x k fp32 row-major, the piece's rows of E (the summed
+ * partials); cl: device int32[a1 - a0], the piece's ids.  zpart: host, k
+ * doubles, zpart_j = sum_{u in piece, cl(u)=j} E(u, j) (fp64, fixed order).
+ * counts: host, k int32, the piece's cluster sizes.  Synchronises before
+ * returning.  Errors: KKM_ERR_ARG (range, NULL), KKM_ERR_STATE,
+ * KKM_ERR_DEVICE_DATA (an id outside [0, k)), KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_block_zpart(kkm_ctx *ctx, const float *E, const int32_t *cl, int64_t a0, int64_t a1, int32_t k,
+                    double *zpart, int32_t *counts);
+
+/* The piece [a0, a1) as in kkm_block_zpart, E as there.  z: host, k doubles,
+ * the global self-terms (converted to fp32 as the full step uses them);
+ * counts: host, k int32, the global sizes |L_j| (>= 0).  cl_out: device
+ * int32[a1 - a0], the piece's new ids.  counts_out: host, may be NULL, k
+ * int32: how many of the piece's points took each id.  Synchronises before
+ * returning.  Errors: KKM_ERR_ARG (range, NULL, a negative size),
+ * KKM_ERR_STATE, KKM_ERR_OOM, KKM_ERR_HIP. */
+int kkm_block_assign(kkm_ctx *ctx, const float *E, int64_t a0, int64_t a1, int32_t k, const double *z,
+                     const int32_t *counts, int32_t *cl_out, int32_t *counts_out);
 
 /* Rows r0 .. r1-1 of K into out (device, (r1-r0) x n fp32 row-major).  In
  * ONTHEFLY mode the rows are computed by the same tile kernel the loop uses;

@@ -164,16 +164,20 @@ __global__ __launch_bounds__(256) void assign_kernel(IterBufs b, const int* __re
 
 static size_t assign_smem(int k) { return (size_t)k * 20 + 64; }
 
-// Panel points, one per thread: D(i,j) = K(i,i) - 2 E(i,j)/|L_j| + z_j for
-// nonempty j (the full-step assign's formula, with z given), lowest-index
-// argmin; the new sizes are counted per workgroup in LDS.
-__global__ __launch_bounds__(256) void panel_assign_kernel(IterBufs b, const float* __restrict__ z,
-                                                           const int* __restrict__ counts,
-                                                           int* __restrict__ cl_out,
-                                                           int* __restrict__ counts_out,
-                                                           float* __restrict__ E_out) {
+// Points u < m, one per thread: D(u,j) = diag(u) - 2 E(u,j)/|L_j| + z_j for
+// nonempty j (the full-step assign's formula, with z and the sizes given),
+// lowest-index argmin; the new sizes are counted per workgroup in LDS.
+// E(u, j) is read at E[u * s_pt + j * s_cl]: a panel's E^T in place
+// (s_pt = 1, s_cl = ld) or a caller's E, point-major (s_pt = k, s_cl = 1).
+__global__ __launch_bounds__(256) void cols_assign_kernel(const float* __restrict__ E, int64_t s_pt, int64_t s_cl,
+                                                          const float* __restrict__ diag, int64_t m, int k,
+                                                          const float* __restrict__ z,
+                                                          const int* __restrict__ counts,
+                                                          int* __restrict__ cl_out,
+                                                          int* __restrict__ counts_out,
+                                                          float* __restrict__ E_out) {
   extern __shared__ float psm[];
-  const int k = b.k, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   float* zf = psm;                // k
   float* sc = zf + k;             // k
   int* hist = (int*)(sc + k);     // k
@@ -184,13 +188,13 @@ __global__ __launch_bounds__(256) void panel_assign_kernel(IterBufs b, const flo
     hist[j] = 0;
   }
   __syncthreads();
-  const int64_t u = (int64_t)blockIdx.x * 256 + tid;  // the panel's point col0 + u
-  if (u < b.ncol) {
-    const float dg = b.diagK[b.col0 + u];
+  const int64_t u = (int64_t)blockIdx.x * 256 + tid;
+  if (u < m) {
+    const float dg = diag[u];
     float best = INFINITY;
     int arg = -1;
     for (int j = 0; j < k; ++j) {
-      const float e = b.Et[(int64_t)j * b.ld + u];
+      const float e = E[u * s_pt + (int64_t)j * s_cl];
       if (E_out) E_out[u * k + j] = e;
       const float s = sc[j];
       if (s != 0.f) {
@@ -210,11 +214,72 @@ __global__ __launch_bounds__(256) void panel_assign_kernel(IterBufs b, const flo
     if (hist[j]) atomicAdd(&counts_out[j], hist[j]);
 }
 
+hipError_t launch_cols_assign(const float* E, int64_t s_pt, int64_t s_cl, const float* diag, int64_t m, int k,
+                              const float* z, const int* counts, int* cl_out, int* counts_out, float* E_out,
+                              hipStream_t s) {
+  const unsigned grid = (unsigned)((m + 255) / 256);
+  hipLaunchKernelGGL(cols_assign_kernel, dim3(grid), dim3(256), (size_t)k * 12, s, E, s_pt, s_cl, diag, m, k, z,
+                     counts, cl_out, counts_out, E_out);
+  return hipGetLastError();
+}
+
 hipError_t launch_panel_assign(const IterBufs& b, const float* z, const int* counts, int* cl_out,
                                int* counts_out, float* E_out, hipStream_t s) {
-  const unsigned grid = (unsigned)((b.ncol + 255) / 256);
-  hipLaunchKernelGGL(panel_assign_kernel, dim3(grid), dim3(256), (size_t)b.k * 12, s, b, z, counts, cl_out,
-                     counts_out, E_out);
+  return launch_cols_assign(b.Et, 1, b.ld, b.diagK + b.col0, b.ncol, b.k, z, counts, cl_out, counts_out, E_out, s);
+}
+
+// Workgroup g: points u in [1024 g, 1024 g + 1024) of a piece of m points
+// (E point-major, m x k; ids cl): the piece's share of sum_{u in L_j} E(u, j)
+// for each cluster j, in fp64 and a fixed order, at zpart[j * nz + g]; its
+// cluster sizes added to counts; an id outside [0, k) sets bit 0 of status.
+__global__ __launch_bounds__(256) void cols_zpart_kernel(const float* __restrict__ E, const int* __restrict__ cl,
+                                                         int64_t m, int k, double* __restrict__ zpart, int nz,
+                                                         int* __restrict__ counts, int* __restrict__ status) {
+  extern __shared__ int zhist[];  // k
+  __shared__ double red[4];
+  const int tid = threadIdx.x;
+  for (int j = tid; j < k; j += 256) zhist[j] = 0;
+  __syncthreads();
+  int jid[4];
+  float ev[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int64_t u = (int64_t)blockIdx.x * 1024 + c * 256 + tid;
+    jid[c] = -1;
+    ev[c] = 0.f;
+    if (u < m) {
+      const int j = cl[u];
+      if (j < 0 || j >= k) {
+        atomicOr(status, 1);
+      } else {
+        jid[c] = j;
+        ev[c] = E[u * k + j];
+        atomicAdd(&zhist[j], 1);
+      }
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < k; j += 256)
+    if (zhist[j]) atomicAdd(&counts[j], zhist[j]);
+  for (int j = 0; j < k; ++j) {
+    double v = 0.0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (jid[c] == j) v += (double)ev[c];
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if ((tid & 63) == 0) red[tid >> 6] = v;
+    __syncthreads();
+    if (tid == 0) zpart[(int64_t)j * nz + blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+    __syncthreads();
+  }
+}
+
+hipError_t launch_cols_zpart(const float* E, const int* cl, int64_t m, int k, double* zpart, int nz, int* counts,
+                             int* status, hipStream_t s) {
+  const int64_t grid = (m + 1023) / 1024;
+  if (m < 1 || grid > nz) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(cols_zpart_kernel, dim3((unsigned)grid), dim3(256), (size_t)k * 4, s, E, cl, m, k, zpart, nz,
+                     counts, status);
   return hipGetLastError();
 }
 
@@ -502,6 +567,30 @@ hipError_t launch_rows_f16(const half_t* K, const float* kw, int64_t n, int64_t 
 
 hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s) {
   hipLaunchKernelGGL(spmm_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, cl);
+  return hipGetLastError();
+}
+
+// Workgroup (stripe, j): a block's partial E(u, j), the sum over its rows in
+// cluster j of K(row, c0 + u) (cluster j's chunk partials added in chunk
+// order; 0 where none of the block's rows is in cluster j), stored
+// point-major at E_out[u * k + j] for u < ncol.
+__global__ __launch_bounds__(256) void block_out_kernel(IterBufs b, float* __restrict__ E_out) {
+  const int ns = b.nstripes;
+  const int stripe = (int)(blockIdx.x % (unsigned)ns);
+  const int j = (int)(blockIdx.x / (unsigned)ns);
+  const int qa = b.qfirst[j], qb = b.qfirst[j + 1];
+  const int64_t ld = b.ld;
+  const int64_t col = (int64_t)stripe * kStripe + threadIdx.x * 4;
+  if (col >= b.ncol) return;
+  f4 e = {0.f, 0.f, 0.f, 0.f};
+  for (int q = qa; q < qb; ++q) e += *(const f4*)(b.P + (int64_t)q * ld + col);
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (col + c < b.ncol) E_out[(col + c) * b.k + j] = e[c];
+}
+
+hipError_t launch_block_out(const IterBufs& b, float* E_out, hipStream_t s) {
+  hipLaunchKernelGGL(block_out_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b, E_out);
   return hipGetLastError();
 }
 

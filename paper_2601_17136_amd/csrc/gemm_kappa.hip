@@ -63,17 +63,17 @@ hipError_t launch_row_scales(const float* nrm, const unsigned* maxnrm_bits, int6
 // Four workgroups per CU (40 KB of LDS each): while some run their store
 // epilogue, others keep the matrix cores busy.  KT is the storage type of K
 // (float, or binary16 with entry (i, j) divided by kw[i]).
-// PANEL: the column panel K[:, c0 : c0 + ld) of one GPU's share (c0 a
-// multiple of kTile, columns past c1 stored as 0): every tile (I, J) with J
-// in the panel, each stored once at (i, j - c0); nt counts panel column
-// tiles there, and T = row tiles x nt.
+// PANEL: the block K[r0:r1, c0 : c0 + ld) of one GPU's share (r0 and c0
+// multiples of kTile, columns past c1 stored as 0): every tile (I, J) in
+// the block, each stored once at (i - r0, j - c0); nt counts the block's
+// column tiles there, and T = its row tiles x nt.
 template <int KIND, typename KT, bool PANEL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void gemm_kappa_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm,
     const unsigned* __restrict__ maxnrm_bits, int64_t n, int d_pad, int64_t ld, bool packed,
-    int64_t nt, int64_t T, int64_t c0, int64_t c1, KappaParams kp, KT* __restrict__ K,
-    const float* __restrict__ kw, float* __restrict__ diagK, int2* __restrict__ fix_list,
-    unsigned long long* __restrict__ fix_count, long long seg_cap) {
+    int64_t nt, int64_t T, int64_t r0, int64_t r1, int64_t c0, int64_t c1, KappaParams kp,
+    KT* __restrict__ K, const float* __restrict__ kw, float* __restrict__ diagK,
+    int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count, long long seg_cap) {
   constexpr bool kHalf = sizeof(KT) == 2;
   __shared__ __attribute__((aligned(16))) float lds[kLdsFloats];
   // No Gaussian entry can need the fix-up unless the largest norms allow it.
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   const int64_t t = x * per + (x < rem ? x : rem) + (b >> 3);
   int64_t I, J;
   if (PANEL) {
-    I = t / nt;
+    I = r0 / kTile + t / nt;
     J = c0 / kTile + t % nt;
   } else {
     triangle_tile(t, nt, I, J);
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         if (KIND == GAUSS && may_fix) {
           // the square layouts list each pair once (i < j) for both of its
           // entries; a panel lists every entry it stores
-          const bool f = (PANEL ? (gi != gj && gi < n && gj < c1) : (gi < gj && gj < n)) &&
+          const bool f = (PANEL ? (gi != gj && gi < r1 && gj < c1) : (gi < gj && gj < n)) &&
                          gauss_needs_fix(v, ni, nj[bj], kp);
           const unsigned long long m = __ballot(f);
           if (m) {
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     for (int rr = 0; rr < 32; ++rr) {
       const int64_t gi = row0 + wm * 64 + bi * 32 + rr;
       if (PANEL) {
-        if (gi < n) put(gi, (gj < c1) ? Tw[rr * 65 + lane] : 0.f, K + gi * ld + (gj - c0));
+        if (gi < r1) put(gi, (gj < c1) ? Tw[rr * 65 + lane] : 0.f, K + (gi - r0) * ld + (gj - c0));
       } else {
         const int64_t rowp = packed ? packed_row(gi, ld) : gi * ld;
         if (gi < n && gj < ld) put(gi, (gj < n) ? Tw[rr * 65 + lane] : 0.f, K + rowp + gj);
@@ -208,8 +208,8 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
   dim3 grid((unsigned)T), block(256);
 #define KKM_GEMM_LAUNCH(KIND, TY)                                                                        \
   hipLaunchKernelGGL((gemm_kappa_kernel<KIND, TY, false>), grid, block, 0, s, Xp, nrm, maxnrm_bits, n,     \
-                     d_pad, ld, packed, nt, T, (int64_t)0, n, kp, (TY*)K, kw, diagK, fix_list, fix_count,  \
-                     seg_cap)
+                     d_pad, ld, packed, nt, T, (int64_t)0, n, (int64_t)0, n, kp, (TY*)K, kw, diagK, fix_list, \
+                     fix_count, seg_cap)
   switch (kp.kind) {
     case LINEAR:
       if (f16) KKM_GEMM_LAUNCH(LINEAR, half_t);
@@ -229,17 +229,18 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
 }
 
 hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                                   int64_t n, int d_pad, int64_t c0, int64_t c1, int64_t ld,
-                                   const KappaParams& kp, float* K, float* diagK, int2* fix_list,
+                                   int64_t n, int d_pad, int64_t r0, int64_t r1, int64_t c0, int64_t c1,
+                                   int64_t ld, const KappaParams& kp, float* K, float* diagK, int2* fix_list,
                                    unsigned long long* fix_count, long long seg_cap, hipStream_t s) {
-  if (c0 % kTile || c1 <= c0 || c1 > n || ld % kTile || ld < c1 - c0) return hipErrorInvalidValue;
-  const int64_t nrow = (n + kTile - 1) / kTile, ncol = ld / kTile;
+  if (r0 % kTile || r1 <= r0 || r1 > n || c0 % kTile || c1 <= c0 || c1 > n || ld % kTile || ld < c1 - c0)
+    return hipErrorInvalidValue;
+  const int64_t nrow = (r1 - r0 + kTile - 1) / kTile, ncol = ld / kTile;
   const int64_t T = nrow * ncol;
   dim3 grid((unsigned)T), block(256);
 #define KKM_PANEL_LAUNCH(KIND)                                                                           \
   hipLaunchKernelGGL((gemm_kappa_kernel<KIND, float, true>), grid, block, 0, s, Xp, nrm, maxnrm_bits, n,   \
-                     d_pad, ld, false, ncol, T, c0, c1, kp, K, (const float*)nullptr, diagK, fix_list,     \
-                     fix_count, seg_cap)
+                     d_pad, ld, false, ncol, T, r0, r1, c0, c1, kp, K, (const float*)nullptr, diagK,       \
+                     fix_list, fix_count, seg_cap)
   switch (kp.kind) {
     case LINEAR: KKM_PANEL_LAUNCH(LINEAR); break;
     case POLY: KKM_PANEL_LAUNCH(POLY); break;
@@ -257,13 +258,13 @@ hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsi
 // every entry of the upper triangle is re-tested from the stored K with the
 // epilogue's estimate.  The counts are read on the device, so the build needs
 // no host round trip.
-// A panel (c1 > 0: columns [c0, c1) stored at j - c0) lists and stores each
-// of its entries once.
+// A block (c1 > 0: rows [r0, r1) and columns [c0, c1) stored at
+// (i - r0, j - c0)) lists and stores each of its entries once.
 template <typename T>
 __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp,
                                                           const float* __restrict__ nrm, int64_t n,
-                                                          int d_pad, int64_t ld, bool packed,
-                                                          int64_t c0, int64_t c1, KappaParams kp,
+                                                          int d_pad, int64_t ld, bool packed, int64_t r0,
+                                                          int64_t r1, int64_t c0, int64_t c1, KappaParams kp,
                                                           const int2* __restrict__ list,
                                                           const unsigned long long* __restrict__ counts,
                                                           long long seg_cap, T* __restrict__ K) {
@@ -303,7 +304,7 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
     if (gl == 0) {  // square layouts list pairs with i < j: (i, j) is stored in both
       const T v = (T)__builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
       if (panel) {
-        K[(int64_t)ij.x * ld + (ij.y - c0)] = v;
+        K[(int64_t)(ij.x - r0) * ld + (ij.y - c0)] = v;
       } else if (packed) {
         K[packed_row(ij.x, ld) + ij.y] = v;
         if (ij.x / kTile == ij.y / kTile) K[packed_row(ij.y, ld) + ij.x] = v;
@@ -316,12 +317,13 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
   __syncthreads();
   if (!overflow) return;
   if (panel) {
-    for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+    for (int64_t i = r0 + blockIdx.x; i < r1; i += gridDim.x) {
       const float ni = nrm[i];
+      T* row = K + (i - r0) * ld;
       for (int64_t j = c0 + threadIdx.x; j < c1; j += 256) {
-        const float v = (float)K[i * ld + (j - c0)];
+        const float v = (float)row[j - c0];
         if (j != i && gauss_needs_fix(v, ni, nrm[j], kp))
-          K[i * ld + (j - c0)] = (T)gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
+          row[j - c0] = (T)gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
       }
     }
     return;
@@ -344,13 +346,13 @@ __global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restric
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
                               bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, void* K,
-                              hipStream_t s, int64_t c0, int64_t c1) {
+                              hipStream_t s, int64_t r0, int64_t r1, int64_t c0, int64_t c1) {
   if (f16)
     hipLaunchKernelGGL(gauss_fixup_kernel<half_t>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                       ld, packed, c0, c1, kp, fix_list, fix_count, seg_cap, (half_t*)K);
+                       ld, packed, r0, r1, c0, c1, kp, fix_list, fix_count, seg_cap, (half_t*)K);
   else
     hipLaunchKernelGGL(gauss_fixup_kernel<float>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                       ld, packed, c0, c1, kp, fix_list, fix_count, seg_cap, (float*)K);
+                       ld, packed, r0, r1, c0, c1, kp, fix_list, fix_count, seg_cap, (float*)K);
   return hipGetLastError();
 }
 

@@ -125,9 +125,12 @@ struct kkm_ctx {
   std::string err;
 
   bool built = false;
-  int64_t pc0 = 0, pc1 = 0;  // a panel (one GPU's share): its points [pc0, pc1); pc1 = 0 otherwise
+  // A block of K (one GPU's share): rows [pr0, pr1) and columns [pc0, pc1);
+  // pc1 = 0 for the full K.  A panel is the block of all rows.
+  int64_t pr0 = 0, pr1 = 0, pc0 = 0, pc1 = 0;
   bool panel_e = false;       // the panel's E^T and sizes are current (kkm_panel_spmm ran)
-  Sizes sz{};
+  Sizes sz{};                 // the problem: n points (staging, norms, diag K)
+  Sizes wsz{};                // the stored K and the scratch: sz, or a block's rows as n
   int d = 0, kind = 0, mode = 0;
   kkm_params params{};
   KappaParams kp{};
@@ -294,13 +297,13 @@ void free_build(kkm_ctx* c) {
   c->fix_count = nullptr;
   c->fix_cap = 0;
   c->built = false;
-  c->pc0 = c->pc1 = 0;
+  c->pr0 = c->pr1 = c->pc0 = c->pc1 = 0;
   c->panel_e = false;
 }
 
 // Allocate one block and carve it (keeps the accounting to one number).
 int carve_ws(kkm_ctx* c, int k) {
-  const Sizes& s = c->sz;
+  const Sizes& s = c->wsz;
   void* base = nullptr;
   int rc = dalloc(c, &base, ws_bytes(s, k, c->mode), c->ws_allocs, "iteration scratch");
   if (rc) return rc;
@@ -464,7 +467,7 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
 int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
-  if (c->pc1 > 0) return fail(c, KKM_ERR_STATE, "the context holds a panel of K; use kkm_panel_spmm / kkm_panel_assign");
+  if (c->pc1 > 0) return fail(c, KKM_ERR_STATE, "the context holds a block of K; use the panel or block calls");
   if (kkm_check_iterate_args(c->sz.n, k, max_iter) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
   if (c->mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
     return fail(c, KKM_ERR_ARG, "k=%d exceeds %d, the most the packed storage handles; build RESIDENT or ONTHEFLY",
@@ -569,10 +572,10 @@ int kkm_destroy(kkm_ctx* c) {
 
 namespace {
 
-// The build of the full K (pc1 = 0) or of the column panel K[:, pc0 : pc1)
+// The build of the full K (pc1 = 0) or of the block K[pr0 : pr1, pc0 : pc1)
 // of one GPU's share (resident, fp32).
 int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
-               int64_t pc0, int64_t pc1) {
+               int64_t pr0, int64_t pr1, int64_t pc0, int64_t pc1) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (kkm_check_build_args(n, d, kind, params) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
   if (!X) return fail(c, KKM_ERR_ARG, "X is NULL");
@@ -580,7 +583,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
   int32_t mode = KKM_MODE_RESIDENT;
   size_t need = 0;
   if (panel) {
-    if (params->storage != KKM_STORE_F32) return fail(c, KKM_ERR_ARG, "a panel is stored in fp32");
+    if (params->storage != KKM_STORE_F32) return fail(c, KKM_ERR_ARG, "a block of K is stored in fp32");
   } else {
     // plan with k = 1: the k-dependent scratch is sized when kkm_iterate is called
     size_t held_by_build = 0;
@@ -596,15 +599,25 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
   // A rebuild of the same shape keeps every buffer (K alone can be 160 GB,
   // and allocating it costs far more than building it).
   const int storage = (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) ? params->storage : KKM_STORE_F32;
+  // (a block of the same shape elsewhere in K also keeps them)
   const bool reuse = c->built && c->sz.n == n && c->d == d && c->mode == mode && c->kind == kind &&
-                     c->storage == storage && c->pc0 == pc0 && c->pc1 == pc1;
+                     c->storage == storage && (c->pc1 > 0) == panel && c->pr1 - c->pr0 == pr1 - pr0 &&
+                     c->pc1 - c->pc0 == pc1 - pc0;
   if (!reuse) free_build(c);
 
   c->sz = sizes_for(n, d, mode);
-  if (panel) {  // the panel's columns: a multiple of kTile, so its tiles store whole
+  if (panel) {  // the block's columns: a multiple of kTile, so its tiles store whole
     c->sz.ld = round_up(pc1 - pc0, kTile);
     c->sz.nstripes = (int)((c->sz.ld + kStripe - 1) / kStripe);
   }
+  c->wsz = c->sz;
+  if (panel) {  // K and the scratch hold the block's rows
+    c->wsz.n = pr1 - pr0;
+    c->wsz.n_pad = round_up(pr1 - pr0, kTile);
+    c->wsz.nblk = (pr1 - pr0 + kBlk - 1) / kBlk;
+  }
+  c->pr0 = pr0;
+  c->pr1 = pr1;
   c->pc0 = pc0;
   c->pc1 = pc1;
   c->panel_e = false;
@@ -635,7 +648,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
     c->maxnrm = (unsigned*)((char*)p + 8);
     const bool stores_k = mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED;
     if (stores_k) {
-      if ((rc = dalloc(c, &p, k_bytes(s, mode, storage), c->build_allocs, "kernel matrix K"))) return rc;
+      if ((rc = dalloc(c, &p, k_bytes(c->wsz, mode, storage), c->build_allocs, "kernel matrix K"))) return rc;
       c->K = p;
     }
     if (row_scaled(mode, storage, kind)) {
@@ -643,7 +656,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
       c->kw = (float*)p;
     }
     if (kind == KKM_GAUSS && stores_k) {
-      const long long upper = panel ? (long long)(n * (pc1 - pc0)) : (long long)(n * (n - 1) / 2);
+      const long long upper = panel ? (long long)((pr1 - pr0) * (pc1 - pc0)) : (long long)(n * (n - 1) / 2);
       long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
       const size_t room = c->budget > c->held ? c->budget - c->held : 0;
       cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
@@ -680,7 +693,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
     return rc;
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
          if (panel)
-           return launch_gemm_kappa_panel(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, pc0, pc1, s.ld, kp,
+           return launch_gemm_kappa_panel(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, pr0, pr1, pc0, pc1, s.ld, kp,
                                           (float*)c->K, c->diagK, c->fix_list, c->fix_count,
                                           c->fix_cap / kFixSegs, c->stream);
          return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16,
@@ -691,10 +704,16 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
   if (kind == KKM_GAUSS &&
       (rc = run(c, KKM_PHASE_FIXUP, "gauss_fixup", [&] {
          return launch_gauss_fixup(c->Xp, c->nrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16, kp,
-                                   c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream, pc0, pc1);
+                                   c->fix_list, c->fix_count, c->fix_cap / kFixSegs, c->K, c->stream, pr0, pr1,
+                                   pc0, pc1);
        })))
     return rc;
-  if (panel) return KKM_OK;  // diag K is set for the panel's points only; no trace
+  // A panel's tiles set diag K for its points.  Another block's diagonal may
+  // lie elsewhere, so diag K of every point comes from the norms, as the
+  // on-the-fly mode takes it; no trace.
+  if (panel && (pr0 > 0 || pr1 < n))
+    return run(c, KKM_PHASE_STAGE, "diag", [&] { return launch_diag_from_norms(c->nrm, n, kp, c->diagK, c->stream); });
+  if (panel) return KKM_OK;
   return run(c, KKM_PHASE_OTHER, "trace", [&] { return launch_trace(c->diagK, n, c->trK, c->stream); });
 }
 
@@ -703,7 +722,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
 extern "C" {
 
 int kkm_build_kernel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params) {
-  return build_impl(c, X, n, d, kind, params, 0, 0);
+  return build_impl(c, X, n, d, kind, params, 0, 0, 0, 0);
 }
 
 int kkm_build_panel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
@@ -712,12 +731,24 @@ int kkm_build_panel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t ki
   if (c0 < 0 || c0 % kTile || c1 <= c0 || c1 > n)
     return fail(c, KKM_ERR_ARG, "bad panel [%lld, %lld): needs 0 <= c0 < c1 <= n=%lld, c0 a multiple of %d",
                 (long long)c0, (long long)c1, (long long)n, kTile);
-  return build_impl(c, X, n, d, kind, params, c0, c1);
+  return build_impl(c, X, n, d, kind, params, 0, n, c0, c1);
+}
+
+int kkm_build_block(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
+                    int64_t r0, int64_t r1, int64_t c0, int64_t c1) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (r0 < 0 || r0 % kTile || r1 <= r0 || r1 > n || c0 < 0 || c0 % kTile || c1 <= c0 || c1 > n)
+    return fail(c, KKM_ERR_ARG,
+                "bad block [%lld, %lld) x [%lld, %lld): needs 0 <= start < end <= n=%lld on both sides, "
+                "starts multiples of %d",
+                (long long)r0, (long long)r1, (long long)c0, (long long)c1, (long long)n, kTile);
+  return build_impl(c, X, n, d, kind, params, r0, r1, c0, c1);
 }
 
 int kkm_panel_spmm(kkm_ctx* c, const int32_t* cl, int32_t k, double* zpart, int32_t* counts) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
-  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no panel built on this context");
+  if (!c->built || c->pc1 == 0 || c->pr0 != 0 || c->pr1 != c->sz.n)
+    return fail(c, KKM_ERR_STATE, "no panel (all rows of K) built on this context");
   if (kkm_check_iterate_args(c->sz.n, k, 1) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
   if (!cl || !zpart) return fail(c, KKM_ERR_ARG, "cl or zpart is NULL");
   int rc;
@@ -753,7 +784,8 @@ int kkm_panel_spmm(kkm_ctx* c, const int32_t* cl, int32_t k, double* zpart, int3
 
 int kkm_panel_assign(kkm_ctx* c, int32_t k, const double* z, int32_t* cl_out, float* E_out, int32_t* counts_out) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
-  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no panel built on this context");
+  if (!c->built || c->pc1 == 0 || c->pr0 != 0 || c->pr1 != c->sz.n)
+    return fail(c, KKM_ERR_STATE, "no panel (all rows of K) built on this context");
   if (!c->panel_e || c->ib.k != k) return fail(c, KKM_ERR_STATE, "kkm_panel_spmm with this k must come first");
   if (!z || !cl_out) return fail(c, KKM_ERR_ARG, "z or cl_out is NULL");
   IterBufs& b = c->ib;
@@ -767,6 +799,106 @@ int kkm_panel_assign(kkm_ctx* c, int32_t k, const double* z, int32_t* cl_out, fl
     return rc;
   if ((rc = run(c, KKM_PHASE_ASSIGN, "panel_assign", [&] {
          return launch_panel_assign(b, zd, c->counts[0], cl_out, c->counts[1], E_out, c->stream);
+       })))
+    return rc;
+  if (counts_out)
+    HIP_TRY(c, hipMemcpyAsync(counts_out, c->counts[1], (size_t)k * 4, hipMemcpyDeviceToHost, c->stream),
+            "read sizes");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return KKM_OK;
+}
+
+int kkm_block_spmm(kkm_ctx* c, const int32_t* cl, int32_t k, float* E_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no block of K built on this context");
+  if (kkm_check_iterate_args(c->sz.n, k, 1) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  if (!cl || !E_out) return fail(c, KKM_ERR_ARG, "cl or E_out is NULL");
+  int rc;
+  c->panel_e = false;
+  if ((rc = ensure_ws(c, k, 1))) return rc;
+  if ((rc = label_pass(c, cl))) return rc;  // the block's rows: sizes in counts[0], per-block histograms
+  IterBufs& b = c->ib;
+  if ((rc = run(c, KKM_PHASE_SCATTER, "scatter", [&] {
+         return launch_scatter(b, cl, c->counts[0], c->counts[1], c->changed, c->stream);
+       })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_SPMM, "spmm_onehot", [&] { return launch_spmm_onehot(c->K, b, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_REDUCE, "block_out", [&] { return launch_block_out(b, E_out, c->stream); })))
+    return rc;
+  int status = 0;
+  HIP_TRY(c, hipMemcpyAsync(&status, b.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  return status_error(c, status);
+}
+
+namespace {
+// A piece [a0, a1) of the block's columns, for the calls that follow the
+// caller's reduce-scatter.
+int check_piece(kkm_ctx* c, int64_t a0, int64_t a1, int32_t k) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!c->built || c->pc1 == 0) return fail(c, KKM_ERR_STATE, "no block of K built on this context");
+  if (kkm_check_iterate_args(c->sz.n, k, 1) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  if (a0 < c->pc0 || a1 <= a0 || a1 > c->pc1)
+    return fail(c, KKM_ERR_ARG, "bad piece [%lld, %lld): needs %lld <= a0 < a1 <= %lld, the block's columns",
+                (long long)a0, (long long)a1, (long long)c->pc0, (long long)c->pc1);
+  return KKM_OK;
+}
+}  // namespace
+
+int kkm_block_zpart(kkm_ctx* c, const float* E, const int32_t* cl, int64_t a0, int64_t a1, int32_t k,
+                    double* zpart, int32_t* counts) {
+  int rc;
+  if ((rc = check_piece(c, a0, a1, k))) return rc;
+  if (!E || !cl || !zpart || !counts) return fail(c, KKM_ERR_ARG, "E, cl, zpart or counts is NULL");
+  if ((rc = ensure_ws(c, k, 1))) return rc;
+  IterBufs& b = c->ib;
+  const int64_t m = a1 - a0;
+  const int ng = (int)((m + 1023) / 1024);  // workgroups: at most one per column stripe, so <= nzpart
+  if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(c->counts[0], k, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_LABELS, "zero", [&] { return launch_zero_ints(b.status, 1, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_REDUCE, "cols_zpart", [&] {
+         return launch_cols_zpart(E, cl, m, k, b.zpart, b.nzpart, c->counts[0], b.status, c->stream);
+       })))
+    return rc;
+  std::vector<double> parts((size_t)k * b.nzpart);
+  int status = 0;
+  HIP_TRY(c, hipMemcpyAsync(parts.data(), b.zpart, parts.size() * sizeof(double), hipMemcpyDeviceToHost, c->stream),
+          "read z parts");
+  HIP_TRY(c, hipMemcpyAsync(counts, c->counts[0], (size_t)k * 4, hipMemcpyDeviceToHost, c->stream), "read sizes");
+  HIP_TRY(c, hipMemcpyAsync(&status, b.status, sizeof status, hipMemcpyDeviceToHost, c->stream), "read status");
+  HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+  if ((rc = status_error(c, status))) return rc;
+  for (int j = 0; j < k; ++j) {  // the workgroups in order
+    double zs = 0.0;
+    for (int g = 0; g < ng; ++g) zs += parts[(size_t)j * b.nzpart + g];
+    zpart[j] = zs;
+  }
+  return KKM_OK;
+}
+
+int kkm_block_assign(kkm_ctx* c, const float* E, int64_t a0, int64_t a1, int32_t k, const double* z,
+                     const int32_t* counts, int32_t* cl_out, int32_t* counts_out) {
+  int rc;
+  if ((rc = check_piece(c, a0, a1, k))) return rc;
+  if (!E || !z || !counts || !cl_out) return fail(c, KKM_ERR_ARG, "E, z, counts or cl_out is NULL");
+  for (int j = 0; j < k; ++j)
+    if (counts[j] < 0) return fail(c, KKM_ERR_ARG, "counts[%d] = %d is negative", j, counts[j]);
+  if ((rc = ensure_ws(c, k, 1))) return rc;
+  IterBufs& b = c->ib;
+  c->panel_e = false;  // z and the sizes below take the panel's places
+  std::vector<float> zf((size_t)k);
+  for (int j = 0; j < k; ++j) zf[j] = (float)z[j];
+  float* zd = (float*)b.zpart;
+  HIP_TRY(c, hipMemcpyAsync(zd, zf.data(), (size_t)k * 4, hipMemcpyHostToDevice, c->stream), "write z");
+  HIP_TRY(c, hipMemcpyAsync(c->counts[0], counts, (size_t)k * 4, hipMemcpyHostToDevice, c->stream), "write sizes");
+  if ((rc = run(c, KKM_PHASE_ASSIGN, "zero", [&] { return launch_zero_ints(c->counts[1], k, c->stream); })))
+    return rc;
+  if ((rc = run(c, KKM_PHASE_ASSIGN, "cols_assign", [&] {
+         return launch_cols_assign(E, k, 1, c->diagK + a0, a1 - a0, k, zd, c->counts[0], cl_out, c->counts[1],
+                                   nullptr, c->stream);
        })))
     return rc;
   if (counts_out)
@@ -901,12 +1033,15 @@ int kkm_init_kmeanspp(kkm_ctx* c, int32_t k, const double* u, int32_t* centers_o
 int kkm_copy_kernel_rows(kkm_ctx* c, int64_t r0, int64_t r1, float* out) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (!c->built) return fail(c, KKM_ERR_STATE, "no kernel matrix built on this context");
-  if (!out || r0 < 0 || r1 > c->sz.n || r0 > r1) return fail(c, KKM_ERR_ARG, "bad row range [%lld, %lld)", (long long)r0, (long long)r1);
+  const int64_t lo = c->pc1 > 0 ? c->pr0 : 0, hi = c->pc1 > 0 ? c->pr1 : c->sz.n;
+  if (!out || r0 < lo || r1 > hi || r0 > r1)
+    return fail(c, KKM_ERR_ARG, "bad row range [%lld, %lld): the stored rows are [%lld, %lld)", (long long)r0,
+                (long long)r1, (long long)lo, (long long)hi);
   if (r1 == r0) return KKM_OK;
-  if (c->pc1 > 0) {  // a panel: its c1 - c0 columns of each row
+  if (c->pc1 > 0) {  // a block: its c1 - c0 columns of each row
     const size_t w = (size_t)(c->pc1 - c->pc0) * 4;
-    HIP_TRY(c, hipMemcpy2DAsync(out, w, (const float*)c->K + r0 * c->sz.ld, (size_t)c->sz.ld * 4, w,
-                                (size_t)(r1 - r0), hipMemcpyDeviceToDevice, c->stream), "copy panel rows");
+    HIP_TRY(c, hipMemcpy2DAsync(out, w, (const float*)c->K + (r0 - c->pr0) * c->sz.ld, (size_t)c->sz.ld * 4, w,
+                                (size_t)(r1 - r0), hipMemcpyDeviceToDevice, c->stream), "copy block rows");
     HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
     return KKM_OK;
   }
@@ -977,7 +1112,7 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   out->mode = c->mode;
   out->ld = c->sz.ld;
   out->storage = c->storage;
-  out->bytes_K = k_bytes(c->sz, c->mode, c->storage);
+  out->bytes_K = k_bytes(c->wsz, c->mode, c->storage);
   out->bytes_total = c->held;
   if (c->fixups < 0) {
     unsigned long long cnt[kFixSegs] = {0};
@@ -991,6 +1126,11 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   }
   out->fixups = c->fixups;
   out->fixup_capacity = c->fix_cap;
+  const bool blk = c->pc1 > 0;
+  out->r0 = blk ? c->pr0 : 0;
+  out->r1 = blk ? c->pr1 : c->sz.n;
+  out->c0 = blk ? c->pc0 : 0;
+  out->c1 = blk ? c->pc1 : c->sz.n;
   return KKM_OK;
 }
 

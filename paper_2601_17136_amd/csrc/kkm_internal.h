@@ -131,20 +131,35 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
 hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int d_pad, int64_t ld,
                               bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, void* K,
-                              hipStream_t s, int64_t c0 = 0, int64_t c1 = 0);
-// One GPU's share of the 1D split: the column panel K[:, c0 : c0 + ld) (c0 a
-// multiple of kTile, c1 <= n, columns from c1 on stored as 0), fp32, row
-// stride ld; diagK of the panel's points; Gaussian entries to fix listed as
-// (i, j) with j the global column (launch_gauss_fixup with the same c0, c1).
+                              hipStream_t s, int64_t r0 = 0, int64_t r1 = 0, int64_t c0 = 0, int64_t c1 = 0);
+// One GPU's share of a split of K: the block K[r0 : r1, c0 : c0 + ld) (r0, c0
+// multiples of kTile, r1, c1 <= n, columns from c1 on stored as 0), fp32, row
+// i - r0 at stride ld; diagK of the points whose diagonal the block holds;
+// Gaussian entries to fix listed as (i, j), global indices
+// (launch_gauss_fixup with the same r0, r1, c0, c1).  The 1D split's column
+// panel is the block r0 = 0, r1 = n.
 hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
-                                   int64_t n, int d_pad, int64_t c0, int64_t c1, int64_t ld,
-                                   const KappaParams& kp, float* K, float* diagK, int2* fix_list,
+                                   int64_t n, int d_pad, int64_t r0, int64_t r1, int64_t c0, int64_t c1,
+                                   int64_t ld, const KappaParams& kp, float* K, float* diagK, int2* fix_list,
                                    unsigned long long* fix_count, long long seg_cap, hipStream_t s);
 // D and lowest-index argmin for the panel's points (columns [b.col0, b.col0 + b.ncol))
 // from E^T (k x ld, column = point - col0), the global z and the cluster sizes;
 // counts_out gets the panel's share of the new sizes (added; zeroed by the caller).
 hipError_t launch_panel_assign(const IterBufs& b, const float* z, const int* counts, int* cl_out,
                                int* counts_out, float* E_out, hipStream_t s);
+// Points u < m: D(u,j) = diag[u] - 2 E(u,j)/counts[j] + z[j] over nonempty j,
+// lowest-index argmin into cl_out, new sizes added to counts_out; E(u, j) at
+// E[u * s_pt + j * s_cl]; E_out (nullable) gets E point-major.
+hipError_t launch_cols_assign(const float* E, int64_t s_pt, int64_t s_cl, const float* diag, int64_t m, int k,
+                              const float* z, const int* counts, int* cl_out, int* counts_out, float* E_out,
+                              hipStream_t s);
+// A piece of m points (E point-major, ids cl): per-cluster fp64 parts of
+// sum_{u in L_j} E(u, j) at zpart[j * nz + g], g < ceil(m / 1024) <= nz;
+// sizes added to counts; a bad id sets bit 0 of status.
+hipError_t launch_cols_zpart(const float* E, const int* cl, int64_t m, int k, double* zpart, int nz, int* counts,
+                             int* status, hipStream_t s);
+// A block's partial E (ncol x k, point-major) from the SpMM's chunk partials.
+hipError_t launch_block_out(const IterBufs& b, float* E_out, hipStream_t s);
 hipError_t launch_trace(const float* diagK, int64_t n, double* trK, hipStream_t s);
 // K-means++ seeding (seed.hip): one distance pass per center, one draw per
 // center after the first; buffers of n (kd, D, best, bestc) and

@@ -49,7 +49,8 @@ class kkm_info(ctypes.Structure):
                 ("kind", ctypes.c_int32), ("mode", ctypes.c_int32), ("storage", ctypes.c_int32),
                 ("ld", ctypes.c_int64),
                 ("bytes_K", ctypes.c_size_t), ("bytes_total", ctypes.c_size_t),
-                ("fixups", ctypes.c_int64), ("fixup_capacity", ctypes.c_int64)]
+                ("fixups", ctypes.c_int64), ("fixup_capacity", ctypes.c_int64),
+                ("r0", ctypes.c_int64), ("r1", ctypes.c_int64), ("c0", ctypes.c_int64), ("c1", ctypes.c_int64)]
 
 
 _lib = None
@@ -70,6 +71,10 @@ _SIGS = {
     "kkm_build_panel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params), _i64, _i64], _i32),
     "kkm_panel_spmm": ([_vp, _vp, _i32, _vp, _vp], _i32),
     "kkm_panel_assign": ([_vp, _i32, _vp, _vp, _vp, _vp], _i32),
+    "kkm_build_block": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params), _i64, _i64, _i64, _i64], _i32),
+    "kkm_block_spmm": ([_vp, _vp, _i32, _vp], _i32),
+    "kkm_block_zpart": ([_vp, _vp, _vp, _i64, _i64, _i32, _vp, _vp], _i32),
+    "kkm_block_assign": ([_vp, _vp, _i64, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
     "kkm_copy_kernel_rows": ([_vp, _i64, _i64, _vp], _i32),
     "kkm_copy_diag": ([_vp, _vp], _i32),
     "kkm_set_timing": ([_vp, _i32], _i32),
@@ -205,13 +210,22 @@ def kkm_build_panel(ctx, X, n: int, d: int, kind: int, params: kkm_params, c0: i
                                  int(kind), ctypes.byref(params), int(c0), int(c1)), ctx)
 
 
+def _stored(ctx):
+    """(r0, r1, c0, c1) of the K the context holds, or None before a build."""
+    info = kkm_info()
+    if lib().kkm_get_info(ctx, ctypes.byref(info)) != KKM_OK:
+        return None
+    return info.r0, info.r1, info.c0, info.c1
+
+
 def kkm_panel_spmm(ctx, cl, k: int):
     """E for the panel's points (kept); returns (zpart as numpy fp64[k], sizes as numpy int32[k])."""
     import torch
+    st = _stored(ctx)
     zpart = np.zeros(int(k), dtype=np.float64)
     counts = np.zeros(int(k), dtype=np.int32)
-    _check(lib().kkm_panel_spmm(ctx, _dev_ptr(cl, torch.int32, "cl"), int(k), zpart.ctypes.data,
-                                counts.ctypes.data), ctx)
+    _check(lib().kkm_panel_spmm(ctx, _dev_ptr(cl, torch.int32, "cl", st and st[1] - st[0]), int(k),
+                                zpart.ctypes.data, counts.ctypes.data), ctx)
     return zpart, counts
 
 
@@ -222,10 +236,60 @@ def kkm_panel_assign(ctx, k: int, z, cl_out, E_out=None) -> np.ndarray:
     z = np.ascontiguousarray(z, dtype=np.float64)
     if z.shape != (int(k),):
         raise KKMError(KKM_ERR_ARG, f"z must hold k={k} values, got shape {z.shape}")
+    st = _stored(ctx)
+    w = st and st[3] - st[2]
     counts = np.zeros(int(k), dtype=np.int32)
-    _check(lib().kkm_panel_assign(ctx, int(k), z.ctypes.data, _dev_ptr(cl_out, torch.int32, "cl_out"),
-                                  _dev_ptr(E_out, torch.float32, "E_out"), counts.ctypes.data), ctx)
+    _check(lib().kkm_panel_assign(ctx, int(k), z.ctypes.data, _dev_ptr(cl_out, torch.int32, "cl_out", w),
+                                  _dev_ptr(E_out, torch.float32, "E_out", w and w * int(k)),
+                                  counts.ctypes.data), ctx)
     return counts
+
+
+def kkm_build_block(ctx, X, n: int, d: int, kind: int, params: kkm_params, r0: int, r1: int, c0: int,
+                    c1: int) -> None:
+    """One GPU's share of the 1.5D split: the block K[r0:r1, c0:c1] (r0, c0 multiples of 128)."""
+    import torch
+    _check(lib().kkm_build_block(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
+                                 int(kind), ctypes.byref(params), int(r0), int(r1), int(c0), int(c1)), ctx)
+
+
+def kkm_block_spmm(ctx, cl, k: int, E_out) -> None:
+    """The block's partial E (its c1 - c0 columns x k, point-major) into
+    E_out from the ids cl of its rows r0 .. r1-1."""
+    import torch
+    st = _stored(ctx)
+    _check(lib().kkm_block_spmm(ctx, _dev_ptr(cl, torch.int32, "cl", st and st[1] - st[0]), int(k),
+                                _dev_ptr(E_out, torch.float32, "E_out", st and (st[3] - st[2]) * int(k))), ctx)
+
+
+def kkm_block_zpart(ctx, E, cl, a0: int, a1: int, k: int):
+    """Self-term parts and sizes of the piece [a0, a1) of the block's columns
+    from its rows of E (device, (a1-a0) x k) and its ids; returns (zpart as
+    numpy fp64[k], sizes as numpy int32[k])."""
+    import torch
+    m = max(int(a1) - int(a0), 0)
+    zpart = np.zeros(int(k), dtype=np.float64)
+    counts = np.zeros(int(k), dtype=np.int32)
+    _check(lib().kkm_block_zpart(ctx, _dev_ptr(E, torch.float32, "E", m * int(k)),
+                                 _dev_ptr(cl, torch.int32, "cl", m), int(a0), int(a1), int(k),
+                                 zpart.ctypes.data, counts.ctypes.data), ctx)
+    return zpart, counts
+
+
+def kkm_block_assign(ctx, E, a0: int, a1: int, k: int, z, counts, cl_out) -> np.ndarray:
+    """New ids of the piece [a0, a1) into cl_out from its rows of E and the
+    global z and sizes; returns how many of its points took each id."""
+    import torch
+    m = max(int(a1) - int(a0), 0)
+    z = np.ascontiguousarray(z, dtype=np.float64)
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    if z.shape != (int(k),) or counts.shape != (int(k),):
+        raise KKMError(KKM_ERR_ARG, f"z and counts must hold k={k} values, got {z.shape}, {counts.shape}")
+    took = np.zeros(int(k), dtype=np.int32)
+    _check(lib().kkm_block_assign(ctx, _dev_ptr(E, torch.float32, "E", m * int(k)), int(a0), int(a1), int(k),
+                                  z.ctypes.data, counts.ctypes.data, _dev_ptr(cl_out, torch.int32, "cl_out", m),
+                                  took.ctypes.data), ctx)
+    return took
 
 
 def kkm_init_kmeanspp(ctx, k: int, u, V) -> np.ndarray:
@@ -242,13 +306,18 @@ def kkm_init_kmeanspp(ctx, k: int, u, V) -> np.ndarray:
 
 
 def kkm_copy_kernel_rows(ctx, r0: int, r1: int, out) -> None:
+    """Rows r0 .. r1-1 of the stored K (of a panel or block: its columns) into out."""
     import torch
-    _check(lib().kkm_copy_kernel_rows(ctx, int(r0), int(r1), _dev_ptr(out, torch.float32, "out")), ctx)
+    st = _stored(ctx)
+    numel = (int(r1) - int(r0)) * (st[3] - st[2]) if st and r1 > r0 else None
+    _check(lib().kkm_copy_kernel_rows(ctx, int(r0), int(r1), _dev_ptr(out, torch.float32, "out", numel)), ctx)
 
 
 def kkm_copy_diag(ctx, out) -> None:
     import torch
-    _check(lib().kkm_copy_diag(ctx, _dev_ptr(out, torch.float32, "out")), ctx)
+    st = _stored(ctx)
+    n = kkm_get_info(ctx)["n"] if st else None
+    _check(lib().kkm_copy_diag(ctx, _dev_ptr(out, torch.float32, "out", n)), ctx)
 
 
 KKM_TIME_ALL = (1 << len(PHASES)) - 1

@@ -35,10 +35,19 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 4
+    assert kkm.kkm_abi_version() == 5
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 4" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 5" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
+
+
+def test_info_struct_matches_header(L):
+    """The binding's kkm_info lists the header's fields in the header's order."""
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct kkm_info \{(.*?)\} kkm_info;", src, flags=re.S).group(1)
+    names = [nm for decl in body.split(";") if decl.strip()
+             for nm in re.findall(r"(\w+)\s*(?:,|$)", decl.strip().split(None, 1)[1])]
+    assert names == [f for f, _ in kkm.kkm_info._fields_]
 
 
 def test_library_is_built_for_gfx950_only(L):
