@@ -32,15 +32,15 @@ METRIC = "clustering iters/sec + K-build TFLOP/s, % of HBM / MFMA peak, 1 GPU"
 # Reported only while the kernel's sources still hash to what was counted.
 FETCH_SCALE, WRITE_SCALE = 1.9999, 1.0
 TRAFFIC = {
-    ("spmm_sym", 2, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 397405.7, 21345.2),
+    ("spmm_sym", 2, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 397406.3, 21345.2),
     ("spmm_sym", 2, "packed-f16"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 198963.7, 21344.9),
     ("gemm_kappa", 2, "packed"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                  ("602cb17e4e908f75", "f259045186003e25"), 2494455.7, 793825.7),
+                                  ("e7e8c0f4b2d06772", "f259045186003e25"), 2496999.6, 793826.7),
     ("gemm_kappa", 2, "packed-f16"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                      ("602cb17e4e908f75", "f259045186003e25"), 2494145.6, 396954.4),
-    ("spmm_onehot", 2, "resident"): (("csrc/cluster_ops.hip",), ("294f9032f000dcd2",), 782834.6, 1578.0),
+                                      ("e7e8c0f4b2d06772", "f259045186003e25"), 2493938.2, 396954.4),
+    ("spmm_onehot", 2, "resident"): (("csrc/cluster_ops.hip",), ("ffc98cf809a2ba97",), 782834.6, 1578.0),
     ("gemm_kappa", 2, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                    ("602cb17e4e908f75", "f259045186003e25"), 2482494.6, 1565086.4),
+                                    ("e7e8c0f4b2d06772", "f259045186003e25"), 2484325.1, 1565099.5),
 }
 
 
@@ -101,6 +101,9 @@ def parse():
     ap.add_argument("--panel", type=int, default=0, metavar="G",
                     help="measure one GPU's share of a G-GPU 1D split instead: GPU 0's column panel "
                          "of K (n x n/G), its build and its updates, without the exchanges")
+    ap.add_argument("--block", type=int, default=0, metavar="Q",
+                    help="measure one GPU's share of a Q x Q-GPU 1.5D split instead: GPU (0, 0)'s block "
+                         "of K (n/Q x n/Q), its build and its updates, without the exchanges")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB (a known-size "
                          "reference for memory-traffic counters)")
@@ -187,6 +190,9 @@ def main():
         torch.cuda.empty_cache()
     if args.panel:
         panel_main(args, w, X, cl0, kkm, torch)
+        return
+    if args.block:
+        block_main(args, w, X, cl0, kkm, torch)
         return
     Xd = torch.from_numpy(X).cuda()
     V0 = torch.from_numpy(cl0).cuda()
@@ -366,6 +372,87 @@ def panel_main(args, w, X, cl0, kkm, torch):
                                "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
                                "frac": round(tf / FP32_MFMA_PEAK_TF, 4), "avg_launch_ms": round(gemm_ms, 5),
                                "work": "2 n c1 d flop (the panel's tiles)"}}
+    print(json.dumps(out), flush=True)
+
+
+def block_main(args, w, X, cl0, kkm, torch):
+    """One GPU's share of a Q x Q-GPU 1.5D split at its real shape: grid
+    position (0, 0), whose block is K[0:b, 0:b] for the first of Q point
+    ranges cut at multiples of 128, and whose piece of the 1D partition is
+    the first Q-th of that range.  The exchanges a multi-GPU run adds (the
+    all-gather of row-block ids, the reduce-scatter of the partial E, the
+    all-reduce of 2k words) are replaced by local stand-ins: this GPU's own
+    partial E for its piece, its own z parts and sizes, and its new ids
+    copied into the id vector."""
+    import numpy as np
+    n, d, k, Q = w.n, w.d, w.k, args.block
+    b = n if Q == 1 else max(128, (n // Q) // 128 * 128)
+    a1 = max(1, b // Q)                        # the piece [0, a1)
+    Xd = torch.from_numpy(X).cuda()
+    V = torch.from_numpy(cl0).cuda()
+    part = torch.empty((b, k), device="cuda")
+    cl_out = torch.empty(a1, dtype=torch.int32, device="cuda")
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.KKM_MODE_RESIDENT)
+    kind = kkm.KINDS[w.kind]
+
+    def build():
+        kkm.kkm_build_block(ctx, Xd, n, d, kind, params, 0, b, 0, b)
+
+    def update():
+        kkm.kkm_block_spmm(ctx, V[:b], k, part)
+        Ep = part[:a1]
+        zpart, counts = kkm.kkm_block_zpart(ctx, Ep, V[:a1], 0, a1, k)
+        c = counts.astype(np.float64)
+        z = np.where(counts > 0, zpart / np.where(counts > 0, c * c, 1.0), 0.0)
+        kkm.kkm_block_assign(ctx, Ep, 0, a1, k, z, counts, cl_out)
+        V[:a1].copy_(cl_out)
+
+    for _ in range(args.warmup):
+        build()
+        update()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        build()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(args.steps * w.iters):
+        update()
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    kkm.kkm_set_timing(ctx, kkm.phase_mask("gemm", "spmm"))
+    build()
+    for _ in range(w.iters):
+        update()
+    ph = kkm.kkm_get_timing(ctx)
+    kkm.kkm_set_timing(ctx, 0)
+    kkm.kkm_destroy(ctx)
+    upd_ms = 1e3 * (t2 - t1) / (args.steps * w.iters)
+    build_ms = 1e3 * (t1 - t0) / args.steps
+    spmm_ms = ph["spmm"][0] / max(ph["spmm"][1], 1)
+    gemm_ms = ph["gemm"][0] / max(ph["gemm"][1], 1)
+    nbytes = 4.0 * b * b                       # the block, read once per update
+    flops = 2.0 * b * b * d                    # every tile of the block
+    gbs = nbytes / (spmm_ms * 1e-3) / 1e9
+    tf = flops / (gemm_ms * 1e-3) / 1e12
+    out = {"metric": "one GPU's share of a %dx%d-GPU 1.5D split: updates/s of its block" % (Q, Q),
+           "value": round(1e3 / upd_ms, 3), "unit": "updates/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(upd_ms, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": w.describe() + f", GPU (0, 0) of {Q}x{Q}: block K[0:{b}, 0:{b}], "
+                                                 f"piece [0, {a1})",
+                      "n": n, "d": d, "k": k, "block_points": b, "piece_points": a1, "block_bytes": int(nbytes),
+                      "parallelism": f"1 GPU's share of {Q * Q} (exchanges not included)"},
+           "block_build_ms": round(build_ms, 4),
+           "roofline": {"kernel": "spmm_onehot (block)", "bound": "hbm", "achieved": round(gbs, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "traffic": None, "traffic_unit": "GB per launch (algorithmic %.3f)" % (nbytes / 1e9),
+                        "avg_launch_ms": round(spmm_ms, 5), "launches": ph["spmm"][1]},
+           "roofline_kbuild": {"kernel": "gemm_kappa (block)", "bound": "mfma", "achieved": round(tf, 2),
+                               "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
+                               "frac": round(tf / FP32_MFMA_PEAK_TF, 4), "avg_launch_ms": round(gemm_ms, 5),
+                               "work": "2 b^2 d flop (the block's tiles)"}}
     print(json.dumps(out), flush=True)
 
 
