@@ -103,35 +103,69 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
   // ---- epilogue: acc[bi][bj][r] is B(i, j) with
   //      i = row0 + wm*64 + bi*32 + 8*(r/4) + 4*h + r%4,  j = col0 + wn*64 + bj*32 + l32
+  // Rows 8q + 4h .. 8q + 4h + 3 of a 32-row block are consecutive, so their
+  // norms come in one 16-byte load.
   float nj[2] = {0.f, 0.f};
+  const float* nrow = nrm + row0 + wm * 64 + 4 * h;
   if (KIND == GAUSS) {
     nj[0] = nrm[col0 + wn * 64 + l32];
     nj[1] = nrm[col0 + wn * 64 + 32 + l32];
   }
+  bool flagged = false;  // some entry of this lane may need the fix-up
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int il = wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-      const int64_t gi = row0 + il;
-      const float ni = (KIND == GAUSS) ? nrm[gi] : 0.f;
+    for (int q = 0; q < 4; ++q) {
+      float4 n4 = {0.f, 0.f, 0.f, 0.f};
+      if (KIND == GAUSS) n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
+      const float nq[4] = {n4.x, n4.y, n4.z, n4.w};
 #pragma unroll
-      for (int bj = 0; bj < 2; ++bj) {
-        const int jl = wn * 64 + bj * 32 + l32;
-        const int64_t gj = col0 + jl;
-        float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
-        if (I == J && il == jl) {
+      for (int e = 0; e < 4; ++e) {
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) {
+          const float v = kappa<KIND>(acc[bi][bj][4 * q + e], nq[e], nj[bj], kp);
+          if (KIND == GAUSS && may_fix) flagged |= gauss_needs_fix(v, nq[e], nj[bj], kp);
+          acc[bi][bj][4 * q + e] = v;
+        }
+      }
+    }
+  }
+  // The diagonal: only tiles I == J hold it, in the blocks bi == bj of the
+  // waves with wm == wn (il == jl there means 8*(r/4) + 4h + r%4 == l32).
+  if (I == J && wm == wn) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (8 * (r >> 2) + 4 * h + (r & 3) == l32) {
+          const int64_t gi = row0 + wm * 64 + bi * 32 + l32;
+          float v = acc[bi][bi][r];
           if (KIND == GAUSS) v = 1.f;  // exp(0): exact, whatever B(i,i) rounded to
+          acc[bi][bi][r] = v;
           if (gi < n) diagK[gi] = v;
         }
-        if (KIND == GAUSS && may_fix) {
-          // the square layouts list each pair once (i < j) for both of its
-          // entries; a panel lists every entry it stores
+      }
+    }
+  }
+  // Gaussian entries to recompute: the estimate above is taken for every
+  // entry; only where some lane flagged one are the listed pairs formed.
+  // The square layouts list each pair once (i < j) for both of its entries;
+  // a panel lists every entry it stores.
+  if (KIND == GAUSS && may_fix && __ballot(flagged)) {
+    const int seg = (int)(blockIdx.x % kFixSegs);
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const float ni = nrm[gi];
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) {
+          const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
           const bool f = (PANEL ? (gi != gj && gi < r1 && gj < c1) : (gi < gj && gj < n)) &&
-                         gauss_needs_fix(v, ni, nj[bj], kp);
+                         gauss_needs_fix(acc[bi][bj][r], ni, nj[bj], kp);
           const unsigned long long m = __ballot(f);
           if (m) {
-            const int seg = (int)(blockIdx.x % kFixSegs);
             const int leader = __ffsll((long long)m) - 1;
             unsigned long long base = 0;
             if (lane == leader) base = atomicAdd(fix_count + seg, (unsigned long long)__popcll(m));
@@ -143,20 +177,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             }
           }
         }
-        acc[bi][bj][r] = v;
       }
     }
   }
 
   // ---- stores, staged through LDS so each instruction writes one row's
   //      contiguous run (256 bytes in fp32, 128 in binary16); non-temporal,
-  //      since K is not read again by this kernel
+  //      since K is not read again by this kernel.  The rows of a tile lie
+  //      at a fixed stride in every layout (packed: ld - row0), so each
+  //      32-row block has one base address and a row count.
   auto put = [&](int64_t gi, float v, KT* dst) {
     if (kHalf) {
       const float inv = kw ? 1.f / kw[gi] : 1.f;
       __builtin_nontemporal_store((KT)(v * inv), dst);
     } else {
       __builtin_nontemporal_store((KT)v, dst);
+    }
+  };
+  auto rows = [&](int64_t gi0, int nrows, KT* dst, int64_t stride, bool col_ok, bool col_val, const float* Tl) {
+    if (!col_ok) return;
+    if (nrows >= 32) {
+#pragma unroll 8
+      for (int rr = 0; rr < 32; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
+    } else {
+      for (int rr = 0; rr < nrows; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
     }
   };
   float* Tw = lds + wave * (32 * 65);
@@ -169,14 +213,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         Tw[(8 * (r >> 2) + 4 * h + (r & 3)) * 65 + bj * 32 + l32] = acc[bi][bj][r];
     __syncthreads();
     const int64_t gj = col0 + wn * 64 + lane;
-    for (int rr = 0; rr < 32; ++rr) {
-      const int64_t gi = row0 + wm * 64 + bi * 32 + rr;
-      if (PANEL) {
-        if (gi < r1) put(gi, (gj < c1) ? Tw[rr * 65 + lane] : 0.f, K + (gi - r0) * ld + (gj - c0));
-      } else {
-        const int64_t rowp = packed ? packed_row(gi, ld) : gi * ld;
-        if (gi < n && gj < ld) put(gi, (gj < n) ? Tw[rr * 65 + lane] : 0.f, K + rowp + gj);
-      }
+    const int64_t gi0 = row0 + wm * 64 + bi * 32;
+    if (PANEL) {
+      const int nrows = (int)min<int64_t>(32, r1 - gi0);
+      rows(gi0, nrows, K + (gi0 - r0) * ld + (gj - c0), ld, true, gj < c1, Tw + lane);
+    } else {
+      const int nrows = (int)min<int64_t>(32, n - gi0);
+      const int64_t base = packed ? packed_row(gi0, ld) : gi0 * ld;
+      rows(gi0, nrows, K + base + gj, packed ? ld - row0 : ld, gj < ld, gj < n, Tw + lane);
     }
     __syncthreads();
   }
@@ -190,10 +234,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
           Tw[l32 * 65 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = acc[bi][bj][r];
       __syncthreads();
       const int64_t gj = row0 + wm * 64 + lane;  // I < J, so gj < n
-      for (int rr = 0; rr < 32; ++rr) {
-        const int64_t gi = col0 + wn * 64 + bj * 32 + rr;
-        if (gi < n) put(gi, Tw[rr * 65 + lane], K + gi * ld + gj);
-      }
+      const int64_t gi0 = col0 + wn * 64 + bj * 32;
+      rows(gi0, (int)min<int64_t>(32, n - gi0), K + gi0 * ld + gj, ld, true, true, Tw + lane);
       __syncthreads();
     }
   }

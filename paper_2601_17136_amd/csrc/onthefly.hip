@@ -86,7 +86,7 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
     nj[0] = ny[col0 + cbase];
     nj[1] = ny[col0 + cbase + 32];
   }
-  unsigned long long fixmask = 0;
+  bool flagged = false;  // some entry of this lane may need the fix-up
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
@@ -97,8 +97,7 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
       for (int bj = 0; bj < 2; ++bj) {
         const int jl = cbase + bj * 32;
         float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
-        if (FIX && gauss_needs_fix(v, ni, nj[bj], kp) && !(diag && il == jl))
-          fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
+        if (FIX) flagged |= gauss_needs_fix(v, ni, nj[bj], kp);
         if (!interior) {
           if (KIND == GAUSS && diag && il == jl) v = 1.f;
           if (il >= nrows || jl >= ncols) v = 0.f;
@@ -106,7 +105,27 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
         acc[bi][bj][r] = v;
       }
     }
-  if (KIND == GAUSS && FIX) {
+  // Only where some lane of the wave flagged an entry is the exact set
+  // formed: the entries off the diagonal whose estimate (on the value kept,
+  // which outside n x n is 0) calls for the recomputation.
+  if (KIND == GAUSS && FIX && __ballot(flagged)) {
+    // the row norms are read again here rather than kept in registers
+    // across the common path
+    asm volatile("" ::: "memory");
+    unsigned long long fixmask = 0;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3);
+        const float ni = rn[il];
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) {
+          const int jl = cbase + bj * 32;
+          if (gauss_needs_fix(acc[bi][bj][r], ni, nj[bj], kp) && !(diag && il == jl))
+            fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
+        }
+      }
     while (fixmask) {
       const int e = __ffsll((long long)fixmask) - 1;
       fixmask &= fixmask - 1;
