@@ -105,26 +105,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   //      i = row0 + wm*64 + bi*32 + 8*(r/4) + 4*h + r%4,  j = col0 + wn*64 + bj*32 + l32
   // Rows 8q + 4h .. 8q + 4h + 3 of a 32-row block are consecutive, so their
   // norms come in one 16-byte load.
-  float nj[2] = {0.f, 0.f};
+  // The Gaussian works on the norms scaled by c = -gamma log2(e) (gauss_scaled).
+  const float cg = kp.neg_g_log2e;
+  float cnj[2] = {0.f, 0.f};
   const float* nrow = nrm + row0 + wm * 64 + 4 * h;
   if (KIND == GAUSS) {
-    nj[0] = nrm[col0 + wn * 64 + l32];
-    nj[1] = nrm[col0 + wn * 64 + 32 + l32];
+    cnj[0] = cg * nrm[col0 + wn * 64 + l32];
+    cnj[1] = cg * nrm[col0 + wn * 64 + 32 + l32];
   }
   bool flagged = false;  // some entry of this lane may need the fix-up
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi) {
+    // u = c|x_i|^2 + c|x_j|^2 rounds the same for (i, j) and (j, i) only
+    // if the products are not fused into the sum
+#pragma clang fp contract(off)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float4 n4 = {0.f, 0.f, 0.f, 0.f};
       if (KIND == GAUSS) n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
-      const float nq[4] = {n4.x, n4.y, n4.z, n4.w};
+      const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
-          const float v = kappa<KIND>(acc[bi][bj][4 * q + e], nq[e], nj[bj], kp);
-          if (KIND == GAUSS && may_fix) flagged |= gauss_needs_fix(v, nq[e], nj[bj], kp);
+          float v;
+          if (KIND == GAUSS) {
+            const float u = cn[e] + cnj[bj];
+            v = gauss_scaled(acc[bi][bj][4 * q + e], u, kp);
+            if (may_fix) flagged |= gauss_needs_fix_scaled(v, u, kp);
+          } else {
+            v = kappa<KIND>(acc[bi][bj][4 * q + e], 0.f, 0.f, kp);
+          }
           acc[bi][bj][4 * q + e] = v;
         }
       }
@@ -157,13 +168,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     for (int bi = 0; bi < 2; ++bi) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
+#pragma clang fp contract(off)
         const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const float ni = nrm[gi];
+        const float cni = cg * nrm[gi];
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
           const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
           const bool f = (PANEL ? (gi != gj && gi < r1 && gj < c1) : (gi < gj && gj < n)) &&
-                         gauss_needs_fix(acc[bi][bj][r], ni, nj[bj], kp);
+                         gauss_needs_fix_scaled(acc[bi][bj][r], cni + cnj[bj], kp);
           const unsigned long long m = __ballot(f);
           if (m) {
             const int leader = __ffsll((long long)m) - 1;

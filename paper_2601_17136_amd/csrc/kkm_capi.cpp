@@ -634,6 +634,8 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
   kp.neg_g_log2e = (float)(-(double)params->gamma * 1.4426950408889634);
   kp.fix_scale = (float)((double)params->gamma * kFixAcc * std::ldexp(1.0, -24));
   kp.fix_tol = kFixTol;
+  kp.m2c = -2.0f * kp.neg_g_log2e;
+  kp.fix_uthr = (float)((double)kp.neg_g_log2e * kFixTol / (double)kp.fix_scale);
 
   const Sizes& s = c->sz;
   int rc;

@@ -63,6 +63,9 @@ struct KappaParams {
   float neg_g_log2e;  // -gamma * log2(e): exp(-gamma s) = exp2(neg_g_log2e * s)
   float fix_scale;    // Gaussian: error estimate of s is fix_scale * (|x|^2 + |y|^2)
   float fix_tol;      // recompute an entry when gamma * err(s) * K exceeds this
+  // The same Gaussian in terms of the scaled norms c|x|^2 (c = neg_g_log2e):
+  float m2c;          // -2c: the exponent c s = m2c * (x.y) + c(|x|^2 + |y|^2)
+  float fix_uthr;     // c * fix_tol / fix_scale: the fix-up test as u K < fix_uthr, u = c(|x|^2 + |y|^2)
 };
 
 // Everything a clustering iteration reads and writes on the device.

@@ -64,8 +64,9 @@ __device__ inline bool any_fix(const unsigned* maxnrm_bits, const KappaParams& k
 }
 
 // One 128 x 128 tile of K from its B tile (acc), rows at row0 and columns at
-// col0 of the staged points Y (n_pad x d_pad, column norms ny; row norms
-// rn[0..127] for the tile's rows): kappa applied, the Gaussian diagonal set to
+// col0 of the staged points Y (n_pad x d_pad, column norms ny; rn[0..127]
+// for the tile's rows: their norms, for the Gaussian scaled by
+// c = -gamma log2(e) as gauss_scaled takes them): kappa applied, the Gaussian diagonal set to
 // exactly 1, entries outside n x n zeroed, and (FIX) Gaussian entries flagged
 // as cancellation-prone recomputed from the differences after the unrolled
 // pass.  Row indices are block-local 32-bit values, so no per-row 64-bit
@@ -74,6 +75,9 @@ template <int KIND, bool FIX>
 __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ Y,
                                   const float* __restrict__ ny, const float* rn, int64_t n,
                                   int d_pad, int64_t row0, int64_t col0, const KappaParams& kp) {
+  // u = c|x_i|^2 + c|x_j|^2 rounds the same for (i, j) and (j, i) only if
+  // the products are not fused into the sum
+#pragma clang fp contract(off)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
   const int nrows = (int)(n - row0 < kTile ? n - row0 : kTile);
@@ -81,10 +85,10 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
   const bool diag = row0 == col0;
   const bool interior = nrows == kTile && ncols == kTile && !diag;
   const int rbase = wm * 64 + 4 * h, cbase = wn * 64 + l32;
-  float nj[2] = {0.f, 0.f};
+  float cnj[2] = {0.f, 0.f};
   if (KIND == GAUSS) {
-    nj[0] = ny[col0 + cbase];
-    nj[1] = ny[col0 + cbase + 32];
+    cnj[0] = kp.neg_g_log2e * ny[col0 + cbase];
+    cnj[1] = kp.neg_g_log2e * ny[col0 + cbase + 32];
   }
   bool flagged = false;  // some entry of this lane may need the fix-up
 #pragma unroll
@@ -92,12 +96,18 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3);
-      const float ni = (KIND == GAUSS) ? rn[il] : 0.f;
+      const float cni = (KIND == GAUSS) ? rn[il] : 0.f;
 #pragma unroll
       for (int bj = 0; bj < 2; ++bj) {
         const int jl = cbase + bj * 32;
-        float v = kappa<KIND>(acc[bi][bj][r], ni, nj[bj], kp);
-        if (FIX) flagged |= gauss_needs_fix(v, ni, nj[bj], kp);
+        float v;
+        if (KIND == GAUSS) {
+          const float u = cni + cnj[bj];
+          v = gauss_scaled(acc[bi][bj][r], u, kp);
+          if (FIX) flagged |= gauss_needs_fix_scaled(v, u, kp);
+        } else {
+          v = kappa<KIND>(acc[bi][bj][r], 0.f, 0.f, kp);
+        }
         if (!interior) {
           if (KIND == GAUSS && diag && il == jl) v = 1.f;
           if (il >= nrows || jl >= ncols) v = 0.f;
@@ -118,11 +128,11 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3);
-        const float ni = rn[il];
+        const float cni = rn[il];
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
           const int jl = cbase + bj * 32;
-          if (gauss_needs_fix(acc[bi][bj][r], ni, nj[bj], kp) && !(diag && il == jl))
+          if (gauss_needs_fix_scaled(acc[bi][bj][r], cni + cnj[bj], kp) && !(diag && il == jl))
             fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
         }
       }
@@ -217,7 +227,7 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(
   const int runA = cA[I], nr = nruns[I];
   float* const cp = Cpart + cbase[I] * kTile;  // this block's column-side partials
   float* const rn = lds + kLdsFloats;
-  if (tid < kTile) rn[tid] = nrm_s[row0 + tid];
+  if (tid < kTile) rn[tid] = (KIND == GAUSS ? kp.neg_g_log2e : 1.f) * nrm_s[row0 + tid];
 
   float rowacc[2][16];
 #pragma unroll
@@ -378,7 +388,7 @@ __global__ __launch_bounds__(256, 2) void kernel_rows_kernel(const float* __rest
   const int J = (int)(blockIdx.x % (unsigned)nt), I = (int)(blockIdx.x / (unsigned)nt);
   const int64_t row0 = R0 + (int64_t)I * kTile, col0 = (int64_t)J * kTile;
   float* const rn = lds + kLdsFloats;
-  if (threadIdx.x < kTile) rn[threadIdx.x] = nrm[row0 + threadIdx.x];
+  if (threadIdx.x < kTile) rn[threadIdx.x] = (KIND == GAUSS ? kp.neg_g_log2e : 1.f) * nrm[row0 + threadIdx.x];
   floatx16 acc[2][2];
   mma_tile(Xp + row0 * d_pad, Xp + col0 * d_pad, d_pad, lds, acc);
   if (any_fix(maxnrm_bits, kp)) kappa_tile<KIND, true>(acc, Xp, nrm, rn, n, d_pad, row0, col0, kp);

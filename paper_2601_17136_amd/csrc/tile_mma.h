@@ -114,6 +114,21 @@ __device__ inline bool gauss_needs_fix(float v, float nx, float ny, const KappaP
   return kp.fix_scale * (nx + ny) * v > kp.fix_tol;
 }
 
+// The Gaussian entry from b = x.y and u = c(|x|^2 + |y|^2), c = -gamma log2(e)
+// (the norms scaled once per row and column): exp2(c s) with
+// c s = -2c b + u, clamped at 0 (s >= 0).  Two operations fewer per entry
+// than kappa<GAUSS> with its estimate below, for the same value up to
+// rounding.
+__device__ inline float gauss_scaled(float b, float u, const KappaParams& kp) {
+  return __builtin_amdgcn_exp2f(fminf(fmaf(kp.m2c, b, u), 0.f));
+}
+
+// gauss_needs_fix in the scaled form: fix_scale (|x|^2 + |y|^2) v > fix_tol,
+// multiplied through by c < 0.
+__device__ inline bool gauss_needs_fix_scaled(float v, float u, const KappaParams& kp) {
+  return u * v < kp.fix_uthr;
+}
+
 // The Gaussian entry from the coordinate differences (fp32, d_pad terms).
 __device__ inline float gauss_direct(const float* __restrict__ x, const float* __restrict__ y,
                                      int d_pad, const KappaParams& kp) {
