@@ -209,7 +209,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   auto rows = [&](int64_t gi0, int nrows, KT* dst, int64_t stride, bool col_ok, bool col_val, const float* Tl) {
     if (!col_ok) return;
     if (nrows >= 32) {
-#pragma unroll 8
+#pragma unroll
       for (int rr = 0; rr < 32; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
     } else {
       for (int rr = 0; rr < nrows; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
