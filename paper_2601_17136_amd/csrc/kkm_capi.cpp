@@ -53,7 +53,7 @@ Sizes sizes_for(int64_t n, int32_t d, int mode) {
   s.n = n;
   s.n_pad = round_up(n, kTile);
   s.ld = mode == KKM_MODE_PACKED ? s.n_pad : round_up(n, 64);
-  s.d_pad = (int)round_up(d, kBK);
+  s.d_pad = (int)round_up(d, 8);  // the K-build mainloop takes a last chunk of 8
   s.nblk = (n + kBlk - 1) / kBlk;
   s.nstripes = (int)((s.ld + kStripe - 1) / kStripe);
   return s;

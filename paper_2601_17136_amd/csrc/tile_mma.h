@@ -13,14 +13,17 @@ constexpr int kLdsBuf = 2 * kTile * kLdsK;  // one stage: A and B chunk
 constexpr int kLdsFloats = 2 * kLdsBuf;     // double-buffered: 40 KB
 
 // acc[bi][bj][r] = sum_k Xa[i][k] Xb[j][k] for the 128 x 128 tile whose rows
-// start at Xa and columns at Xb (row stride d_pad, d_pad a multiple of 16):
+// start at Xa and columns at Xb (row stride d_pad, d_pad a multiple of 8):
 //   i = wm*64 + bi*32 + 8*(r/4) + 4*h + r%4,   j = wn*64 + bj*32 + lane%32
 // with wave = 2*wm + wn and h = lane/32.  256 threads; ends with a barrier, so
 // the caller may reuse lds right away.
 //
 // Within a 16-wide k chunk the half-wave h takes k = 8h .. 8h+7 and step s of
 // v_mfma_f32_32x32x2_f32 pairs k = s with k = 8 + s: every lane fetches its
-// operands with two 16-byte LDS reads per 32-row block.
+// operands with two 16-byte LDS reads per 32-row block.  When d_pad is an odd
+// multiple of 8 the last chunk is 8 wide: its upper half is neither loaded
+// nor multiplied (h takes k = 4h .. 4h+3, four steps), so a row pays for at
+// most 7 zero columns.
 __device__ inline void mma_tile(const float* __restrict__ Xa, const float* __restrict__ Xb,
                                 int d_pad, float* lds, floatx16 acc[2][2]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -33,6 +36,13 @@ __device__ inline void mma_tile(const float* __restrict__ Xa, const float* __res
   const float* Bg1 = Xb + (int64_t)(f1 >> 2) * d_pad + (f1 & 3) * 4;
   const int so0 = (f0 >> 2) * kLdsK + (f0 & 3) * 4;
   const int so1 = (f1 >> 2) * kLdsK + (f1 & 3) * 4;
+  const int nkf = d_pad / kBK;                  // full 16-wide chunks
+  const bool half_last = (d_pad % kBK) != 0;    // then one 8-wide chunk
+  const int nk = nkf + (half_last ? 1 : 0);
+  // in the 8-wide chunk, the threads at k offsets 8 and 12 load nothing
+  // (f1 = f0 + 256 has the same k offset as f0)
+  const bool upper = (f0 & 3) >= 2;
+  const float4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
@@ -41,23 +51,24 @@ __device__ inline void mma_tile(const float* __restrict__ Xa, const float* __res
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
 
-  float4 ra0 = *(const float4*)Ag0, ra1 = *(const float4*)Ag1;
-  float4 rb0 = *(const float4*)Bg0, rb1 = *(const float4*)Bg1;
+  const bool skip0 = nkf == 0 && upper;
+  float4 ra0 = skip0 ? zero4 : *(const float4*)Ag0, ra1 = skip0 ? zero4 : *(const float4*)Ag1;
+  float4 rb0 = skip0 ? zero4 : *(const float4*)Bg0, rb1 = skip0 ? zero4 : *(const float4*)Bg1;
   *(float4*)(lds + so0) = ra0;
   *(float4*)(lds + so1) = ra1;
   *(float4*)(lds + kTile * kLdsK + so0) = rb0;
   *(float4*)(lds + kTile * kLdsK + so1) = rb1;
   __syncthreads();
 
-  const int nk = d_pad / kBK;
-  for (int kc = 0; kc < nk; ++kc) {
+  for (int kc = 0; kc < nkf; ++kc) {
     const int cur = kc & 1;
     if (kc + 1 < nk) {  // prefetch the next chunk into registers
       const int ko = (kc + 1) * kBK;
-      ra0 = *(const float4*)(Ag0 + ko);
-      ra1 = *(const float4*)(Ag1 + ko);
-      rb0 = *(const float4*)(Bg0 + ko);
-      rb1 = *(const float4*)(Bg1 + ko);
+      const bool skip = kc + 1 == nkf && upper;  // the next chunk is the 8-wide one
+      ra0 = skip ? zero4 : *(const float4*)(Ag0 + ko);
+      ra1 = skip ? zero4 : *(const float4*)(Ag1 + ko);
+      rb0 = skip ? zero4 : *(const float4*)(Bg0 + ko);
+      rb1 = skip ? zero4 : *(const float4*)(Bg1 + ko);
     }
     const float* As = lds + cur * kLdsBuf;
     const float* Bs = As + kTile * kLdsK;
@@ -87,6 +98,26 @@ __device__ inline void mma_tile(const float* __restrict__ Xa, const float* __res
       *(float4*)(nxt + kTile * kLdsK + so0) = rb0;
       *(float4*)(nxt + kTile * kLdsK + so1) = rb1;
     }
+    __syncthreads();
+  }
+  if (half_last) {  // the 8-wide chunk, in buffer nkf & 1: h takes k = 4h .. 4h+3
+    const float* As = lds + (nkf & 1) * kLdsBuf;
+    const float* Bs = As + kTile * kLdsK;
+    float a[2][4], bv[2][4];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float4 a0 = *(const float4*)(As + (wm * 64 + q * 32 + l32) * kLdsK + h * 4);
+      const float4 b0 = *(const float4*)(Bs + (wn * 64 + q * 32 + l32) * kLdsK + h * 4);
+      a[q][0] = a0.x; a[q][1] = a0.y; a[q][2] = a0.z; a[q][3] = a0.w;
+      bv[q][0] = b0.x; bv[q][1] = b0.y; bv[q][2] = b0.z; bv[q][3] = b0.w;
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+          acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[bi][s], bv[bj][s], acc[bi][bj], 0, 0, 0);
     __syncthreads();
   }
 }
