@@ -161,80 +161,141 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   // Gaussian entries to recompute: the estimate above is taken for every
   // entry; only where some lane flagged one are the listed pairs formed.
   // The square layouts list each pair once (i < j) for both of its entries;
-  // a panel lists every entry it stores.
+  // a panel lists every entry it stores.  Each lane marks its listed
+  // entries in a 64-bit mask (entry g = ((bi*4 + q)*4 + e)*2 + bj); a scan
+  // of the lanes' counts and one atomic per wavefront give the slots.  (A
+  // returning atomic per group of 64 entries left the wavefront waiting on
+  // one round trip per group.)  The test repeats the estimate above with
+  // the same operands.
   if (KIND == GAUSS && may_fix && __ballot(flagged)) {
     const int seg = (int)(blockIdx.x % kFixSegs);
+    unsigned mlo = 0u, mhi = 0u;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
 #pragma clang fp contract(off)
-        const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const float cni = cg * nrm[gi];
 #pragma unroll
-        for (int bj = 0; bj < 2; ++bj) {
-          const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
-          const bool f = (PANEL ? (gi != gj && gi < r1 && gj < c1) : (gi < gj && gj < n)) &&
-                         gauss_needs_fix_scaled(acc[bi][bj][r], cni + cnj[bj], kp);
-          const unsigned long long m = __ballot(f);
-          if (m) {
-            const int leader = __ffsll((long long)m) - 1;
-            unsigned long long base = 0;
-            if (lane == leader) base = atomicAdd(fix_count + seg, (unsigned long long)__popcll(m));
-            base = __shfl(base, leader, 64);
-            if (f) {
-              const unsigned long long idx = base + __popcll(m & ((1ull << lane) - 1ull));
-              if (idx < (unsigned long long)seg_cap)
-                fix_list[(int64_t)seg * seg_cap + (int64_t)idx] = make_int2((int)gi, (int)gj);
-            }
+      for (int q = 0; q < 4; ++q) {
+        const float4 n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
+        const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * q + 4 * h + e;
+#pragma unroll
+          for (int bj = 0; bj < 2; ++bj) {
+            const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
+            const bool f = (PANEL ? (gi != gj && gi < r1 && gj < c1) : (gi < gj && gj < n)) &&
+                           gauss_needs_fix_scaled(acc[bi][bj][4 * q + e], cn[e] + cnj[bj], kp);
+            const int g = ((bi * 4 + q) * 4 + e) * 2 + bj;
+            if (g < 32) mlo |= f ? 1u << g : 0u;
+            else mhi |= f ? 1u << (g - 32) : 0u;
           }
         }
       }
     }
+    const unsigned cnt = (unsigned)(__popc(mlo) + __popc(mhi));
+    unsigned pre = cnt;  // inclusive scan over the lanes
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned v = __shfl_up(pre, o, 64);
+      if (lane >= o) pre += v;
+    }
+    const unsigned total = __shfl(pre, 63, 64);
+    unsigned long long base = 0;
+    if (lane == 0 && total) base = atomicAdd(fix_count + seg, (unsigned long long)total);
+    base = __shfl(base, 0, 64) + (pre - cnt);
+    while (mlo | mhi) {
+      const int g = mlo ? __ffs(mlo) - 1 : 32 + __ffs(mhi) - 1;
+      if (g < 32) mlo &= mlo - 1u;
+      else mhi &= mhi - 1u;
+      const int bj = g & 1, e = (g >> 1) & 3, q = (g >> 3) & 3, bi = g >> 5;
+      const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * q + 4 * h + e;
+      const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
+      if (base < (unsigned long long)seg_cap)
+        fix_list[(int64_t)seg * seg_cap + (int64_t)base] = make_int2((int)gi, (int)gj);
+      ++base;
+    }
   }
 
-  // ---- stores, staged through LDS so each instruction writes one row's
-  //      contiguous run (256 bytes in fp32, 128 in binary16); non-temporal,
-  //      since K is not read again by this kernel.  The rows of a tile lie
-  //      at a fixed stride in every layout (packed: ld - row0), so each
-  //      32-row block has one base address and a row count.
-  auto put = [&](int64_t gi, float v, KT* dst) {
-    if (kHalf) {
+  // ---- stores of tile (I, J).  The rows of a tile lie at a fixed stride S
+  //      in every layout (packed: ld - row0), so entry (il, jl) of the tile
+  //      is at Kb + il S + jl.  Non-temporal: K is not read again here.
+  //      fp32 goes straight from the MFMA layout: each instruction writes
+  //      rows il and il + 4, 32 consecutive floats (128 bytes) each, and
+  //      the address is a uniform base plus a per-lane 32-bit offset fixed
+  //      for the tile (127 S + 127 floats stay far below 2^32 bytes for any
+  //      K that fits in memory).  Binary16 is staged through LDS instead,
+  //      so each instruction writes one row's 128 contiguous bytes.
+  // Columns j < clim hold entries, clim <= j < cend hold 0 (the padding of
+  // a row), and j >= cend lie past the row's end.
+  KT* Kb;
+  int64_t S, rlim, clim, cend;
+  if (PANEL) {
+    Kb = K + (row0 - r0) * ld + (col0 - c0);
+    S = ld;
+    rlim = r1;
+    clim = c1;
+    cend = c0 + ld;
+  } else {
+    Kb = K + (packed ? packed_row(row0, ld) : row0 * ld) + col0;
+    S = packed ? ld - row0 : ld;
+    rlim = n;
+    clim = n;
+    cend = ld;
+  }
+  float* Tw = lds + wave * (32 * 65);
+  if (!kHalf) {
+    // row il = bi*32 + 8(r/4) + (r%4) + 4h: the uniform part gives each
+    // row's base address, the rest is one per-lane byte offset for all rows
+    const unsigned lane_b = ((unsigned)(wm * 64 + 4 * h) * (unsigned)S + (unsigned)(wn * 64 + l32)) * 4u;
+    char* const Kc = (char*)Kb;
+    const bool full = row0 + kTile <= rlim && col0 + kTile <= clim;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int iu = bi * 32 + 8 * (r >> 2) + (r & 3);
+        char* const rowp = Kc + (size_t)iu * (size_t)S * 4u;
+        float v0 = acc[bi][0][r], v1 = acc[bi][1][r];
+        if (full) {
+          __builtin_nontemporal_store(v0, (float*)(rowp + lane_b));
+          __builtin_nontemporal_store(v1, (float*)(rowp + lane_b + 128u));
+          continue;
+        }
+        // the last row or column block: rows past rlim are not stored;
+        // columns past clim hold 0 up to the row's end (ld), none beyond
+        if (row0 + wm * 64 + 4 * h + iu >= rlim) continue;
+        const int64_t j0 = col0 + wn * 64 + l32, j1 = j0 + 32;
+        if (j0 < cend) __builtin_nontemporal_store(j0 < clim ? v0 : 0.f, (float*)(rowp + lane_b));
+        if (j1 < cend) __builtin_nontemporal_store(j1 < clim ? v1 : 0.f, (float*)(rowp + lane_b + 128u));
+      }
+  } else {
+    auto put = [&](int64_t gi, float v, KT* dst) {
       const float inv = kw ? 1.f / kw[gi] : 1.f;
       __builtin_nontemporal_store((KT)(v * inv), dst);
-    } else {
-      __builtin_nontemporal_store((KT)v, dst);
+    };
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          Tw[(8 * (r >> 2) + 4 * h + (r & 3)) * 65 + bj * 32 + l32] = acc[bi][bj][r];
+      __syncthreads();
+      const int jl = wn * 64 + lane;
+      const int il0 = wm * 64 + bi * 32;
+      const int nrows = (int)min<int64_t>(32, rlim - (row0 + il0));
+      const bool col_val = col0 + jl < clim;
+      KT* dst = Kb + il0 * S + jl;
+      if (col0 + jl < cend) {
+        if (nrows >= 32) {
+#pragma unroll
+          for (int rr = 0; rr < 32; ++rr) put(row0 + il0 + rr, col_val ? Tw[rr * 65 + lane] : 0.f, dst + rr * S);
+        } else {
+          for (int rr = 0; rr < nrows; ++rr) put(row0 + il0 + rr, col_val ? Tw[rr * 65 + lane] : 0.f, dst + rr * S);
+        }
+      }
+      __syncthreads();
     }
-  };
-  auto rows = [&](int64_t gi0, int nrows, KT* dst, int64_t stride, bool col_ok, bool col_val, const float* Tl) {
-    if (!col_ok) return;
-    if (nrows >= 32) {
-#pragma unroll
-      for (int rr = 0; rr < 32; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
-    } else {
-      for (int rr = 0; rr < nrows; ++rr) put(gi0 + rr, col_val ? Tl[rr * 65] : 0.f, dst + rr * stride);
-    }
-  };
-  float* Tw = lds + wave * (32 * 65);
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi) {  // tile (I, J): rows i, columns j
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        Tw[(8 * (r >> 2) + 4 * h + (r & 3)) * 65 + bj * 32 + l32] = acc[bi][bj][r];
-    __syncthreads();
-    const int64_t gj = col0 + wn * 64 + lane;
-    const int64_t gi0 = row0 + wm * 64 + bi * 32;
-    if (PANEL) {
-      const int nrows = (int)min<int64_t>(32, r1 - gi0);
-      rows(gi0, nrows, K + (gi0 - r0) * ld + (gj - c0), ld, true, gj < c1, Tw + lane);
-    } else {
-      const int nrows = (int)min<int64_t>(32, n - gi0);
-      const int64_t base = packed ? packed_row(gi0, ld) : gi0 * ld;
-      rows(gi0, nrows, K + base + gj, packed ? ld - row0 : ld, gj < ld, gj < n, Tw + lane);
-    }
-    __syncthreads();
   }
   if (!PANEL && I != J && !packed) {
 #pragma unroll
@@ -247,7 +308,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       __syncthreads();
       const int64_t gj = row0 + wm * 64 + lane;  // I < J, so gj < n
       const int64_t gi0 = col0 + wn * 64 + bj * 32;
-      rows(gi0, (int)min<int64_t>(32, n - gi0), K + gi0 * ld + gj, ld, true, true, Tw + lane);
+      const int nrows = (int)min<int64_t>(32, n - gi0);
+      KT* dst = K + gi0 * ld + gj;
+      auto put = [&](int rr) {
+        const float v = Tw[rr * 65 + lane];
+        if (kHalf) __builtin_nontemporal_store((KT)(v * (kw ? 1.f / kw[gi0 + rr] : 1.f)), dst + rr * ld);
+        else __builtin_nontemporal_store((KT)v, dst + rr * ld);
+      };
+      if (nrows >= 32) {
+#pragma unroll
+        for (int rr = 0; rr < 32; ++rr) put(rr);
+      } else {
+        for (int rr = 0; rr < nrows; ++rr) put(rr);
+      }
       __syncthreads();
     }
   }
