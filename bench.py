@@ -104,6 +104,9 @@ def parse():
     ap.add_argument("--block", type=int, default=0, metavar="Q",
                     help="measure one GPU's share of a Q x Q-GPU 1.5D split instead: GPU (0, 0)'s block "
                          "of K (n/Q x n/Q), its build and its updates, without the exchanges")
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure the achievable peaks instead (16 GiB non-temporal streaming read and "
+                         "write, fp32 MFMA register loop) and print them as one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB (a known-size "
                          "reference for memory-traffic counters)")
@@ -188,6 +191,9 @@ def main():
         print(f"bench: calibration copy of {args.copy_calibration} MiB done", file=sys.stderr, flush=True)
         del src, dst
         torch.cuda.empty_cache()
+    if args.peaks:
+        peaks_main(kkm, torch)
+        return
     if args.panel:
         panel_main(args, w, X, cl0, kkm, torch)
         return
@@ -299,6 +305,38 @@ def main():
         out["cpu_baseline"] = cpu_baseline_sized(w, X, cl0, args.cpu_seconds)
     kkm.kkm_destroy(ctx)
     print(json.dumps(out), flush=True)
+
+
+def peaks_main(kkm, torch):
+    """What this GPU sustains, for the roofline fractions against measured peaks:
+    a 16 GiB streaming read and write with non-temporal 16-byte accesses, and a
+    register loop of v_mfma_f32_32x32x2_f32 (about 18 ms per launch, long enough
+    for the clocks to settle).  One warm-up launch each, then the average of 5."""
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    try:
+        buf = torch.empty(4 << 30, dtype=torch.float32, device="cuda")   # 16 GiB
+        sums = torch.zeros(kkm.PEAK_READ_GROUPS, dtype=torch.float32, device="cuda")
+        kkm.kkm_peak_write(ctx, buf, 1.0, 1)
+        w_ms = kkm.kkm_peak_write(ctx, buf, 1.0, 5)
+        kkm.kkm_peak_read(ctx, buf, sums, 1)
+        r_ms = kkm.kkm_peak_read(ctx, buf, sums, 5)
+        read_ok = float(sums.double().sum().item()) == float(buf.numel())
+        nbytes = buf.numel() * 4
+        del buf
+        out = torch.zeros(4096, dtype=torch.float32, device="cuda")
+        kkm.kkm_peak_mfma(ctx, 40000, out, 1)
+        m_ms, flops = kkm.kkm_peak_mfma(ctx, 40000, out, 5)
+    finally:
+        kkm.kkm_destroy(ctx)
+    res = {"metric": "achievable peaks (measurement aids, not the clustering path)",
+           "read_GBps": round(nbytes / (r_ms * 1e-3) / 1e9, 1), "write_GBps": round(nbytes / (w_ms * 1e-3) / 1e9, 1),
+           "mfma_f32_TFLOPs": round(flops / (m_ms * 1e-3) / 1e12, 2),
+           "read_frac_of_8TBps": round(nbytes / (r_ms * 1e-3) / 8e12, 4),
+           "write_frac_of_8TBps": round(nbytes / (w_ms * 1e-3) / 8e12, 4),
+           "mfma_frac_of_157.3TF": round(flops / (m_ms * 1e-3) / 157.3e12, 4),
+           "bytes": nbytes, "read_ms": round(r_ms, 4), "write_ms": round(w_ms, 4), "mfma_ms": round(m_ms, 4),
+           "mfma_flop_per_launch": flops, "read_sums_exact": read_ok}
+    print(json.dumps(res), flush=True)
 
 
 def panel_main(args, w, X, cl0, kkm, torch):

@@ -382,6 +382,28 @@ int kkm_get_timing(kkm_ctx *ctx, kkm_timing *out);
 
 int kkm_get_info(kkm_ctx *ctx, kkm_info *out);
 
+/* Achievable-peak microbenchmarks.  These are measurement aids and no step of
+ * the method: they give what this GPU sustains, so the roofline fractions of
+ * the kernels above can be stated against measured peaks as well as the
+ * datasheet ones.  Each runs reps launches of one kernel on the context's
+ * stream and writes the average launch time in ms to *ms_out (host); it
+ * returns after the launches have completed.  Errors: KKM_ERR_ARG (NULL
+ * pointers, bytes not a positive multiple of 16, a buffer not 16-byte
+ * aligned, reps or iters < 1), KKM_ERR_HIP.
+ *  - kkm_peak_read: non-temporal 16-byte loads over buf (device, `bytes`
+ *    bytes read as fp32), 2040 workgroups, each streaming a contiguous
+ *    range 16 KB at a time; workgroup g writes the fp32 sum
+ *    of the values it read to sums[g] (device, at least 2040 floats), so
+ *    the loads cannot be elided and the caller can check them.
+ *  - kkm_peak_write: non-temporal 16-byte stores of `value` over buf.
+ *  - kkm_peak_mfma: four independent chains of v_mfma_f32_32x32x2_f32 per
+ *    wavefront, `iters` instructions each, 1024 workgroups of four
+ *    wavefronts; one float per wavefront to out (device, at least 4096
+ *    floats); *flops_out (host) = the fp32 matrix flop of one launch. */
+int kkm_peak_read(kkm_ctx *ctx, const void *buf, size_t bytes, float *sums, int32_t reps, float *ms_out);
+int kkm_peak_write(kkm_ctx *ctx, void *buf, size_t bytes, float value, int32_t reps, float *ms_out);
+int kkm_peak_mfma(kkm_ctx *ctx, int32_t iters, float *out, int32_t reps, float *ms_out, double *flops_out);
+
 int kkm_abi_version(void);
 
 #ifdef __cplusplus

@@ -1136,4 +1136,65 @@ int kkm_get_info(kkm_ctx* c, kkm_info* out) {
   return KKM_OK;
 }
 
+
+// ---- achievable-peak microbenchmarks (measurement aids)
+
+}  // extern "C"
+
+namespace {
+
+// Average duration of reps launches of `launch` on the context's stream,
+// from one pair of HIP events around all of them.
+template <class F>
+int time_launches(kkm_ctx* c, int32_t reps, float* ms_out, F&& launch, const char* what) {
+  hipEvent_t a = nullptr, b = nullptr;
+  HIP_TRY(c, hipEventCreate(&a), "hipEventCreate");
+  hipError_t e = hipEventCreate(&b);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hip_fail(c, e, "hipEventCreate");
+  }
+  e = hipEventRecord(a, c->stream);
+  for (int32_t r = 0; r < reps && e == hipSuccess; ++r) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(b, c->stream);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  if (e != hipSuccess) return hip_fail(c, e, what);
+  *ms_out = ms / (float)reps;
+  return KKM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kkm_peak_read(kkm_ctx* c, const void* buf, size_t bytes, float* sums, int32_t reps, float* ms_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!buf || !sums || !ms_out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  if (bytes < 16 || bytes % 16 || (uintptr_t)buf % 16) return fail(c, KKM_ERR_ARG, "bytes=%zu must be a positive multiple of 16 on a 16-byte aligned buffer", bytes);
+  if (reps < 1) return fail(c, KKM_ERR_ARG, "reps=%d must be >= 1", reps);
+  return time_launches(c, reps, ms_out, [&] { return launch_peak_read(buf, (int64_t)bytes, sums, c->stream); },
+                       "peak read");
+}
+
+int kkm_peak_write(kkm_ctx* c, void* buf, size_t bytes, float value, int32_t reps, float* ms_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!buf || !ms_out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  if (bytes < 16 || bytes % 16 || (uintptr_t)buf % 16) return fail(c, KKM_ERR_ARG, "bytes=%zu must be a positive multiple of 16 on a 16-byte aligned buffer", bytes);
+  if (reps < 1) return fail(c, KKM_ERR_ARG, "reps=%d must be >= 1", reps);
+  return time_launches(c, reps, ms_out, [&] { return launch_peak_write(buf, (int64_t)bytes, value, c->stream); },
+                       "peak write");
+}
+
+int kkm_peak_mfma(kkm_ctx* c, int32_t iters, float* out, int32_t reps, float* ms_out, double* flops_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!out || !ms_out || !flops_out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  if (iters < 1 || reps < 1) return fail(c, KKM_ERR_ARG, "iters=%d and reps=%d must be >= 1", iters, reps);
+  *flops_out = (double)kPeakMfmaGrid * 4.0 * 4.0 * 4096.0 * (double)iters;
+  return time_launches(c, reps, ms_out, [&] { return launch_peak_mfma(iters, out, c->stream); }, "peak mfma");
+}
+
 }  // extern "C"

@@ -227,4 +227,17 @@ hipError_t launch_kernel_rows(const float* Xp, const float* nrm, const unsigned*
                               int64_t n, int d_pad, const KappaParams& kp, int64_t r0, int64_t r1,
                               float* out, hipStream_t s);
 
+
+// Achievable-peak microbenchmarks (measurement aids, not on the clustering
+// path): kPeakGrid workgroups of 256 threads stream the buffer (2040, not
+// 2048, so that the workgroups' ranges do not start a power of two apart
+// and their write fronts spread over the memory channels); the MFMA loop
+// runs kPeakMfmaGrid workgroups of four wavefronts (four per SIMD on 256
+// CUs).
+constexpr int kPeakGrid = 2040;
+constexpr int kPeakMfmaGrid = 1024;
+hipError_t launch_peak_read(const void* buf, int64_t bytes, float* sums, hipStream_t s);
+hipError_t launch_peak_write(void* buf, int64_t bytes, float value, hipStream_t s);
+hipError_t launch_peak_mfma(int iters, float* out, hipStream_t s);
+
 }  // namespace kkm

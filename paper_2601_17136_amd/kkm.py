@@ -78,6 +78,9 @@ _SIGS = {
     "kkm_copy_kernel_rows": ([_vp, _i64, _i64, _vp], _i32),
     "kkm_copy_diag": ([_vp, _vp], _i32),
     "kkm_set_timing": ([_vp, _i32], _i32),
+    "kkm_peak_read": ([_vp, _vp, _sz, _vp, _i32, ctypes.POINTER(ctypes.c_float)], _i32),
+    "kkm_peak_write": ([_vp, _vp, _sz, ctypes.c_float, _i32, ctypes.POINTER(ctypes.c_float)], _i32),
+    "kkm_peak_mfma": ([_vp, _i32, _vp, _i32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_f64)], _i32),
     "kkm_get_timing": ([_vp, ctypes.POINTER(kkm_timing)], _i32),
     "kkm_get_info": ([_vp, ctypes.POINTER(kkm_info)], _i32),
 }
@@ -318,6 +321,41 @@ def kkm_copy_diag(ctx, out) -> None:
     st = _stored(ctx)
     n = kkm_get_info(ctx)["n"] if st else None
     _check(lib().kkm_copy_diag(ctx, _dev_ptr(out, torch.float32, "out", n)), ctx)
+
+
+PEAK_READ_GROUPS = 2040  # workgroups of the streaming read and write
+
+
+def kkm_peak_read(ctx, buf, sums, reps: int = 1) -> float:
+    """Streaming-read microbenchmark over the fp32 device tensor buf; the sum read by
+    workgroup g goes to sums[g], g < PEAK_READ_GROUPS.  Returns ms per launch."""
+    import torch
+    if sums.numel() < PEAK_READ_GROUPS:
+        raise KKMError(KKM_ERR_ARG, f"sums must hold at least {PEAK_READ_GROUPS} floats (one per workgroup)")
+    ms = ctypes.c_float()
+    _check(lib().kkm_peak_read(ctx, _dev_ptr(buf, torch.float32, "buf"), buf.numel() * 4,
+                               _dev_ptr(sums, torch.float32, "sums"), int(reps), ctypes.byref(ms)), ctx)
+    return ms.value
+
+
+def kkm_peak_write(ctx, buf, value: float, reps: int = 1) -> float:
+    """Streaming-write microbenchmark: value into every element of buf.  Returns ms per launch."""
+    import torch
+    ms = ctypes.c_float()
+    _check(lib().kkm_peak_write(ctx, _dev_ptr(buf, torch.float32, "buf"), buf.numel() * 4, float(value),
+                                int(reps), ctypes.byref(ms)), ctx)
+    return ms.value
+
+
+def kkm_peak_mfma(ctx, iters: int, out, reps: int = 1):
+    """fp32 MFMA register loop; out >= 4096 floats.  Returns (ms per launch, flop per launch)."""
+    import torch
+    if out.numel() < 4096:
+        raise KKMError(KKM_ERR_ARG, "out must hold at least 4096 floats (one per wavefront)")
+    ms, fl = ctypes.c_float(), _f64()
+    _check(lib().kkm_peak_mfma(ctx, int(iters), _dev_ptr(out, torch.float32, "out"), int(reps),
+                               ctypes.byref(ms), ctypes.byref(fl)), ctx)
+    return ms.value, fl.value
 
 
 KKM_TIME_ALL = (1 << len(PHASES)) - 1

@@ -102,6 +102,10 @@ def test_null_context_is_rejected_without_a_gpu(L):
     assert L.kkm_iterate(None, None, 2, 1, -1.0, None, None) == kkm.KKM_ERR_ARG
     assert L.kkm_destroy(None) == kkm.KKM_OK
     assert L.kkm_create(None, None, 0) == kkm.KKM_ERR_ARG
+    ms, fl = ctypes.c_float(), ctypes.c_double()
+    assert L.kkm_peak_read(None, None, 16, None, 1, ctypes.byref(ms)) == kkm.KKM_ERR_ARG
+    assert L.kkm_peak_write(None, None, 16, 1.0, 1, ctypes.byref(ms)) == kkm.KKM_ERR_ARG
+    assert L.kkm_peak_mfma(None, 1, None, 1, ctypes.byref(ms), ctypes.byref(fl)) == kkm.KKM_ERR_ARG
 
 
 def test_plan_resident_when_it_fits(L):
