@@ -35,12 +35,12 @@ TRAFFIC = {
     ("spmm_sym", 2, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 397405.5, 21345.2),
     ("spmm_sym", 2, "packed-f16"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 198963.7, 21344.9),
     ("gemm_kappa", 2, "packed"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                  ("5640c58fdbb0d023", "21ea801568c098f4"), 2521025.0, 793823.0),
+                                  ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2521025.0, 793823.0),
     ("gemm_kappa", 2, "packed-f16"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                      ("5640c58fdbb0d023", "21ea801568c098f4"), 2504742.1, 396951.0),
+                                      ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2504742.1, 396951.0),
     ("spmm_onehot", 2, "resident"): (("csrc/cluster_ops.hip",), ("ffc98cf809a2ba97",), 782834.6, 1578.0),
     ("gemm_kappa", 2, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                    ("5640c58fdbb0d023", "21ea801568c098f4"), 2506375.9, 1565078.8),
+                                    ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2506375.9, 1565078.8),
 }
 
 

@@ -268,7 +268,8 @@ int kkm_init_kmeanspp(kkm_ctx *ctx, int32_t k, const double *u, int32_t *centers
  *
  * kkm_build_panel: as kkm_build_kernel (params->mode is ignored; storage must
  * be KKM_STORE_F32) for the panel of points [c0, c1): 0 <= c0 < c1 <= n, c0
- * a multiple of 128.  The panel takes n x round_up(c1 - c0, 128) floats; its
+ * a multiple of 128, c1 - c0 <= 8,388,480 (the K build addresses a tile's
+ * stores with 32-bit offsets).  The panel takes n x round_up(c1 - c0, 128) floats; its
  * tiles are computed whole (no symmetry saving), the Gaussian diagonal is 1
  * and flagged Gaussian entries are recomputed from the differences, as in
  * the full build.  Only the panel's points get diag K.  After it,
@@ -322,7 +323,8 @@ int kkm_panel_assign(kkm_ctx *ctx, int32_t k, const double *z, int32_t *cl_out, 
  *
  * kkm_build_block: as kkm_build_panel for the block rows [r0, r1) x columns
  * [c0, c1): 0 <= r0 < r1 <= n and 0 <= c0 < c1 <= n, r0 and c0 multiples of
- * 128.  The block takes (r1 - r0) x round_up(c1 - c0, 128) floats.  diag K is
+ * 128, c1 - c0 <= 8,388,480 (as for a panel).  The block takes
+ * (r1 - r0) x round_up(c1 - c0, 128) floats.  diag K is
  * set for every point, from the staged norms (Gaussian: 1).  A rebuild with
  * blocks of the same size keeps the buffers.  After it, kkm_copy_kernel_rows
  * copies rows r0 <= r < r1 of the block ((r1-r0) x (c1-c0)); the full-K and

@@ -222,8 +222,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   //      fp32 goes straight from the MFMA layout: each instruction writes
   //      rows il and il + 4, 32 consecutive floats (128 bytes) each, and
   //      the address is a uniform base plus a per-lane 32-bit offset fixed
-  //      for the tile (127 S + 127 floats stay far below 2^32 bytes for any
-  //      K that fits in memory).  Binary16 is staged through LDS instead,
+  //      for the tile (S < kMaxKStride keeps it below 2^32 bytes; the
+  //      launchers and the panel and block builds check).  Binary16 is
+  //      staged through LDS instead,
   //      so each instruction writes one row's 128 contiguous bytes.
   // Columns j < clim hold entries, clim <= j < cend hold 0 (the padding of
   // a row), and j >= cend lie past the row's end.
@@ -330,6 +331,7 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
                              int64_t n, int d_pad, int64_t ld, bool packed, bool f16, const float* kw,
                              const KappaParams& kp, void* K, float* diagK, int2* fix_list,
                              unsigned long long* fix_count, long long seg_cap, hipStream_t s) {
+  if (ld >= kMaxKStride) return hipErrorInvalidValue;
   const int64_t nt = (n + kTile - 1) / kTile;
   const int64_t T = nt * (nt + 1) / 2;
   dim3 grid((unsigned)T), block(256);
@@ -359,7 +361,8 @@ hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsi
                                    int64_t n, int d_pad, int64_t r0, int64_t r1, int64_t c0, int64_t c1,
                                    int64_t ld, const KappaParams& kp, float* K, float* diagK, int2* fix_list,
                                    unsigned long long* fix_count, long long seg_cap, hipStream_t s) {
-  if (r0 % kTile || r1 <= r0 || r1 > n || c0 % kTile || c1 <= c0 || c1 > n || ld % kTile || ld < c1 - c0)
+  if (r0 % kTile || r1 <= r0 || r1 > n || c0 % kTile || c1 <= c0 || c1 > n || ld % kTile || ld < c1 - c0 ||
+      ld >= kMaxKStride)
     return hipErrorInvalidValue;
   const int64_t nrow = (r1 - r0 + kTile - 1) / kTile, ncol = ld / kTile;
   const int64_t T = nrow * ncol;

@@ -733,6 +733,9 @@ int kkm_build_panel(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t ki
   if (c0 < 0 || c0 % kTile || c1 <= c0 || c1 > n)
     return fail(c, KKM_ERR_ARG, "bad panel [%lld, %lld): needs 0 <= c0 < c1 <= n=%lld, c0 a multiple of %d",
                 (long long)c0, (long long)c1, (long long)n, kTile);
+  if (round_up(c1 - c0, kTile) >= kMaxKStride)
+    return fail(c, KKM_ERR_ARG, "panel of %lld columns: at most %lld fit the K build's 32-bit store offsets",
+                (long long)(c1 - c0), (long long)(kMaxKStride - kTile));
   return build_impl(c, X, n, d, kind, params, 0, n, c0, c1);
 }
 
@@ -744,6 +747,9 @@ int kkm_build_block(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t ki
                 "bad block [%lld, %lld) x [%lld, %lld): needs 0 <= start < end <= n=%lld on both sides, "
                 "starts multiples of %d",
                 (long long)r0, (long long)r1, (long long)c0, (long long)c1, (long long)n, kTile);
+  if (round_up(c1 - c0, kTile) >= kMaxKStride)
+    return fail(c, KKM_ERR_ARG, "block of %lld columns: at most %lld fit the K build's 32-bit store offsets",
+                (long long)(c1 - c0), (long long)(kMaxKStride - kTile));
   return build_impl(c, X, n, d, kind, params, r0, r1, c0, c1);
 }
 

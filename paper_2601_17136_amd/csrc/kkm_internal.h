@@ -12,6 +12,11 @@ namespace kkm {
 // wavefronts, each 64 x 64 = 2 x 2 MFMA 32x32 blocks), 16-wide k chunks.
 constexpr int kTile = 128;
 constexpr int kBK = 16;
+// The K build addresses a tile's fp32 stores as a row base plus a 32-bit
+// byte offset of at most (127 S + 128) * 4 for the row stride S, so every
+// layout keeps S below kMaxKStride floats (a square K that wide would not
+// fit in memory; a panel or block is checked when it is built).
+constexpr int64_t kMaxKStride = (int64_t)1 << 23;
 
 // One-hot SpMM: a workgroup streams a stripe of kStripe columns of K over a
 // chunk of at most kChunk rows that all belong to one cluster (long chunks:

@@ -159,6 +159,16 @@ def test_block_errors(oracle):
                                 kkm.make_params(0.5, 0.0, 1, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16),
                                 0, 128, 0, 128)
         assert e.value.code == kkm.KKM_ERR_ARG
+        # a block or panel wider than the K build's 32-bit store offsets allow
+        # is refused before anything runs (X is not read, so a small buffer
+        # stands in for the 9M points)
+        import ctypes
+        L = kkm.lib()
+        for c1 in (8_388_480 + 1, 8_400_000):
+            assert L.kkm_build_block(ctx, Xd.data_ptr(), 9_000_000, 8, G, ctypes.byref(prm),
+                                     0, 128, 0, c1) == kkm.KKM_ERR_ARG
+            assert L.kkm_build_panel(ctx, Xd.data_ptr(), 9_000_000, 8, G, ctypes.byref(prm),
+                                     0, c1) == kkm.KKM_ERR_ARG
         kkm.kkm_build_block(ctx, Xd, 500, 8, G, prm, 128, 384, 256, 500)
         info = kkm.kkm_get_info(ctx)
         assert (info["r0"], info["r1"], info["c0"], info["c1"]) == (128, 384, 256, 500)
