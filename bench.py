@@ -8,10 +8,12 @@ included), timed with no kernel instrumented.  Per-kernel times come from
 HIP events the library records on its stream in as many further jobs; the
 K-build and per-update roofline figures are derived from them.
 
-Default workload: n=20,000 points, d=784, k=10, Gaussian kernel gamma=1/784,
-30 updates, K stored packed (its upper block triangle, 0.81 GB; the default
-for k <= 16, else the full K).  ``--config N`` picks another workload and
-``--mode`` another storage.
+Default workload: the largest, n=200,000 points, d=54, k=7, Gaussian kernel
+gamma=1/54, 50 updates, K stored packed (its upper block triangle, 80 GB;
+the default storage for k <= 16, else the full K).  Beside it, under their
+own keys, the same workload with the full K resident (160 GB) and with K
+tiles recomputed on the fly each update (nothing stored), each over fewer
+jobs.  ``--config N`` picks another workload and ``--mode`` another storage.
 """
 import argparse
 import json
@@ -88,12 +90,17 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", type=int, default=2, help="workload 1-5 (default 2: n=20000, d=784)")
+    ap.add_argument("--config", type=int, default=5,
+                    help="workload 1-5 (default 5: n=200000, d=54, k=7, the largest)")
     ap.add_argument("--mode", choices=["packed", "resident", "onthefly"], default=None,
                     help="K storage (default: packed when k <= 16, else resident)")
     ap.add_argument("--storage", choices=["f32", "f16"], default="f32",
                     help="number format of the stored K (f16: binary16 with fp32 sums, a mixed-precision "
                          "option with its own error bound; the default keeps fp32)")
+    ap.add_argument("--extra", default=None,
+                    help="comma-separated further storage modes measured beside the headline "
+                         "(default: resident,onthefly for workload 5, none otherwise)")
+    ap.add_argument("--extra-steps", type=int, default=3, help="timed jobs per further mode (after 1 warm-up)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="oracle sample sized for about this much host time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -114,18 +121,21 @@ def parse():
 
 
 def cpu_baseline_sized(w, X, cl0, seconds):
-    """Pilot on 256 rows, then a sample sized for about ``seconds`` of host work."""
+    """Pilot on 256 rows, then a sample sized for about ``seconds`` of host work
+    (at most 4 GB of fp64 kernel rows)."""
     pilot = cpu_baseline(w, X, cl0, 256)
     per_row = (w.iters / pilot["value"]) / X.shape[0]      # seconds of oracle work per row
-    rows = int(min(X.shape[0], max(256, seconds / max(per_row, 1e-9))))
+    cap = max(256, int(4e9 / (8.0 * X.shape[0])))
+    rows = int(min(X.shape[0], cap, max(256, seconds / max(per_row, 1e-9))))
     return cpu_baseline(w, X, cl0, rows)
 
 
 def cpu_baseline(w, X, cl0, rows):
     """The oracle (fp64 kernel entries from their definitions + NumPy steps) on a
     row sample: K rows and w.iters updates restricted to those rows, scaled by
-    n / rows to the whole job.  The self-terms z are taken once from the sample
-    rows' own-cluster sums (what the update needs besides E)."""
+    n / rows to the whole job (labelled extrapolated when rows < n).  The
+    self-terms z are taken from the sample rows' own-cluster sums (what the
+    update needs besides E)."""
     import numpy as np
 
     from oracle import kkm_oracle as oracle
@@ -139,7 +149,12 @@ def cpu_baseline(w, X, cl0, rows):
     diag = kern.pairs(X, sample, sample)
     t1 = time.perf_counter()
     cl = cl0.copy()
+    fixed = 0.0   # per-update work over all n points (sizes, one-hot ids): not scaled by n / rows
     for _ in range(w.iters):
+        ta = time.perf_counter()
+        oracle.cluster_sizes(cl, w.k)
+        oracle.one_hot(cl, w.k)
+        fixed += time.perf_counter() - ta
         counts = oracle.cluster_sizes(cl, w.k)
         E = oracle.one_hot_product(K_rows, cl, w.k)
         own = oracle.mask(E, cl[sample])
@@ -150,12 +165,151 @@ def cpu_baseline(w, X, cl0, rows):
         cl[sample] = new
     t2 = time.perf_counter()
     scale = n / rows
-    total = (t1 - t0 + t2 - t1) * scale
+    upd = (t2 - t1 - 2.0 * fixed)         # the oracle's own update calls, less their all-n part
+    total = (t1 - t0) * scale + fixed + max(upd, 0.0) * scale
     threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    how = "extrapolated" if rows < n else "measured"
     return {"value": w.iters / total, "unit": "iters/s", "cores": threads, "kind": "oracle",
-            "sample": f"K rows and {w.iters} updates on {rows} of {n} rows (fp64), "
+            "cpu_model": cpu_model(), "estimate": how,
+            "sample": f"{how}: K rows and {w.iters} updates on {rows} of {n} rows (fp64), "
                       f"times scaled by n/rows={scale:.1f}: K {1e3 * (t1 - t0) * scale:.0f} ms, "
-                      f"updates {1e3 * (t2 - t1) * scale:.0f} ms"}
+                      f"updates {1e3 * (fixed + max(upd, 0.0) * scale):.0f} ms "
+                      f"(of which {1e3 * fixed:.0f} ms over all n points, not scaled)"}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (lscpu's "Model name"), for the oracle baseline."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def measure(args, w, X, cl0, mode, steps, warmup, kkm, torch):
+    """One storage mode: `warmup` + `steps` whole jobs (build + w.iters updates),
+    the timed ones with no launch bracketed; then, unless --no-timing, as many
+    jobs again with HIP events around the dominant kernels only, and one job
+    with every launch bracketed for the per-phase breakdown.  The context (and
+    its K) is freed before returning, so the next mode has the memory."""
+    n, d, k = w.n, w.d, w.k
+    Xd = torch.from_numpy(X).cuda()
+    V0 = torch.from_numpy(cl0).cuda()
+    Vs = [V0.clone() for _ in range(steps + warmup)]
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.MODES[mode], kkm.STORAGES[args.storage])
+    kind = kkm.KINDS[w.kind]
+
+    def job(V):
+        kkm.kkm_build_kernel(ctx, Xd, n, d, kind, params)
+        return kkm.kkm_iterate(ctx, V, k, w.iters, -1.0)
+
+    res = {}
+    try:
+        for s in range(warmup):
+            job(Vs[s])
+            print(f"bench: {mode}: warmup step {s} done", file=sys.stderr, flush=True)
+        # Timed steps, uninstrumented: a HIP event bracket costs several us of
+        # stream time, so no kernel is bracketed here.
+        kkm.kkm_set_timing(ctx, 0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            it, hist = job(Vs[warmup + s])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        assert it == w.iters
+        info = kkm.kkm_get_info(ctx)
+        print(f"bench: {mode}: timed {steps} steps in {t1 - t0:.3f} s", file=sys.stderr, flush=True)
+        ms_per_step = 1e3 * (t1 - t0) / steps
+        res.update(value=w.iters / (ms_per_step / 1e3), ms_per_step=ms_per_step, steps=steps, warmup=warmup,
+                   info=info, J_final=float(hist[-1]))
+        if not args.no_timing:
+            # Kernel durations for the roofline: the same jobs again with events
+            # around the dominant kernels only.
+            kkm.kkm_set_timing(ctx, kkm.phase_mask("gemm", "spmm", "onthefly"))
+            for s in range(steps):
+                job(V0.clone())
+            res["phases"] = kkm.kkm_get_timing(ctx)
+            # One more job with every launch bracketed, for the per-phase breakdown.
+            kkm.kkm_set_timing(ctx, kkm.KKM_TIME_ALL)
+            job(V0.clone())
+            res["breakdown"] = kkm.kkm_get_timing(ctx)
+            kkm.kkm_set_timing(ctx, 0)
+            res["kmeanspp"] = time_seeding(kkm, ctx, n, k, info["d_pad"])
+    finally:
+        kkm.kkm_destroy(ctx)
+        del Xd, V0, Vs
+        torch.cuda.empty_cache()
+    return res
+
+
+def roofline_fields(args, w, mode, res):
+    """The roofline objects of one measured mode (needs its event timings)."""
+    n, d = w.n, w.d
+    phases, breakdown = res["phases"], res["breakdown"]
+
+    def avg(ph):
+        ms, cnt = phases[ph]
+        return (ms / cnt if cnt else float("nan")), cnt
+
+    f16 = args.storage == "f16"
+    traffic_tag = "-f16" if f16 else ""   # counted traffic is kept per storage format
+    out = {}
+    spmm_ms, spmm_cnt = avg("spmm")
+    gemm_ms, gemm_cnt = avg("gemm")
+    kbuild_ms = sum(breakdown[p][0] for p in ("stage", "gemm", "fixup"))
+    iter_ms = sum(breakdown[p][0] for p in ("labels", "scatter", "spmm", "reduce", "assign", "onthefly", "other"))
+    flops = float(n) * (n + 1) * d                     # symmetric half of X X^T, 2 flops per MAC
+    out["kbuild_ms"] = round(kbuild_ms, 4)
+    out["kbuild_tflops"] = round(flops / (gemm_ms * 1e-3) / 1e12, 3) if gemm_cnt else None
+    out["kbuild_frac_mfma"] = round(out["kbuild_tflops"] / FP32_MFMA_PEAK_TF, 4) if out["kbuild_tflops"] else None
+    out["update_ms"] = round(iter_ms / w.iters, 4)
+    out["updates_per_s_loop"] = round(w.iters / (iter_ms * 1e-3), 2)
+    from paper_2601_17136_amd.kkm import PHASES
+    out["phases_ms_one_step"] = {p: round(breakdown[p][0], 4) for p in PHASES if breakdown[p][1]}
+    if mode in ("resident", "packed"):
+        # K streamed once per update: all of it, or its upper triangle
+        # n(n+1)/2 (what symmetry leaves to read; the stored diagonal
+        # tiles and column padding count against the kernel)
+        kname = "spmm_onehot" if mode == "resident" else "spmm_sym"
+        esize = 2.0 if f16 else 4.0   # bytes per stored entry
+        bytes_per = esize * n * n if mode == "resident" else esize * n * (n + 1) / 2
+        gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
+        out["roofline"] = {"kernel": kname, "bound": "hbm", "achieved": round(gbs, 1),
+                           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                           "traffic": counted_traffic(kname, w.cfg, mode + traffic_tag),
+                           "traffic_unit": "GB per launch (algorithmic %.4f)" % (bytes_per / 1e9),
+                           "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt,
+                           "stored_K_bytes": res["info"]["bytes_K"]}
+    else:
+        otf_ms, otf_cnt = avg("onthefly")
+        otf_tf = flops / (otf_ms * 1e-3) / 1e12   # the symmetric half, per update
+        out["roofline"] = {"kernel": "onthefly", "bound": "mfma", "achieved": round(otf_tf, 2),
+                           "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
+                           "frac": round(otf_tf / FP32_MFMA_PEAK_TF, 4),
+                           "traffic": counted_traffic("onthefly", w.cfg, mode),
+                           "traffic_unit": "GB per launch", "avg_launch_ms": round(otf_ms, 5),
+                           "launches": otf_cnt,
+                           "work": "n(n+1)d flop per update (symmetric half of X X^T)"}
+    tf = out["kbuild_tflops"]
+    if gemm_cnt:
+        out["roofline_kbuild"] = {"kernel": "gemm_kappa", "bound": "mfma", "achieved": tf,
+                                  "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
+                                  "frac": round(tf / FP32_MFMA_PEAK_TF, 4) if tf else None,
+                                  "traffic": counted_traffic("gemm_kappa", w.cfg, mode + traffic_tag),
+                                  "traffic_unit": "GB per launch", "avg_launch_ms": round(gemm_ms, 5),
+                                  "work": "n(n+1)d flop (symmetric half of X X^T)",
+                                  "gauss_fixups": res["info"]["fixups"]}
+        if mode == "resident" or (mode == "packed" and not f16):
+            # the write roof: the stored bytes of K at the HBM peak
+            wbytes = float(res["info"]["bytes_K"])
+            out["roofline_kbuild"]["write_gbs"] = round(wbytes / (gemm_ms * 1e-3) / 1e9, 1)
+            out["roofline_kbuild"]["write_frac"] = round(wbytes / (gemm_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    return out
 
 
 def main():
@@ -164,7 +318,7 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the engine is single-GPU; multi-GPU sharding is a design note, not built)", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
+    import numpy as np  # noqa: F401
     import torch
 
     from paper_2601_17136_amd import datagen, kkm
@@ -174,11 +328,13 @@ def main():
         # the packed SpMM's column side costs one MFMA per 16 labels per entry:
         # below the HBM time for k <= 16, above it for larger k
         args.mode = "packed" if w.k <= 16 else "resident"
+    extra = [m for m in (args.extra.split(",") if args.extra is not None else
+                         (["resident", "onthefly"] if args.config == 5 else [])) if m and m != args.mode]
     X, _ = datagen.make_points(args.config)
     cl0 = datagen.make_init(args.config, w.n, w.k)
     n, d, k = w.n, w.d, w.k
-    print(f"bench: {w.describe()} mode={args.mode} steps={args.steps} warmup={args.warmup}",
-          file=sys.stderr, flush=True)
+    print(f"bench: {w.describe()} mode={args.mode} steps={args.steps} warmup={args.warmup} "
+          f"extra={','.join(extra) or '-'}", file=sys.stderr, flush=True)
 
     torch.cuda.set_device(0)
     torch.cuda.empty_cache()
@@ -200,49 +356,10 @@ def main():
     if args.block:
         block_main(args, w, X, cl0, kkm, torch)
         return
-    Xd = torch.from_numpy(X).cuda()
-    V0 = torch.from_numpy(cl0).cuda()
-    Vs = [V0.clone() for _ in range(args.steps + args.warmup)]
-    ctx = kkm.kkm_create(kkm.current_stream_handle())
-    params = kkm.make_params(w.gamma, w.coef0, w.degree, kkm.MODES[args.mode], kkm.STORAGES[args.storage])
-    kind = kkm.KINDS[w.kind]
 
-    def job(V):
-        kkm.kkm_build_kernel(ctx, Xd, n, d, kind, params)
-        return kkm.kkm_iterate(ctx, V, k, w.iters, -1.0)
-
-    for s in range(args.warmup):
-        job(Vs[s])
-        print(f"bench: warmup step {s} done", file=sys.stderr, flush=True)
-    # Timed steps, uninstrumented: a HIP event bracket costs several us of
-    # stream time, so no kernel is bracketed here.
-    kkm.kkm_set_timing(ctx, 0)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        it, hist = job(Vs[args.warmup + s])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    info = kkm.kkm_get_info(ctx)
-    print(f"bench: timed {args.steps} steps in {t1 - t0:.3f} s", file=sys.stderr, flush=True)
-    phases = breakdown = None
-    if not args.no_timing:
-        # Kernel durations for the roofline: the same jobs again with events
-        # around the dominant kernels only.
-        kkm.kkm_set_timing(ctx, kkm.phase_mask("gemm", "spmm", "onthefly"))
-        for s in range(args.steps):
-            job(V0.clone())
-        phases = kkm.kkm_get_timing(ctx)
-        # One more job with every launch bracketed, for the per-phase breakdown.
-        kkm.kkm_set_timing(ctx, kkm.KKM_TIME_ALL)
-        job(V0.clone())
-        breakdown = kkm.kkm_get_timing(ctx)
-    kkm.kkm_set_timing(ctx, 0)
-
-    ms_per_step = 1e3 * (t1 - t0) / args.steps
-    value = w.iters / (ms_per_step / 1e3)
+    res = measure(args, w, X, cl0, args.mode, args.steps, args.warmup, kkm, torch)
     f16 = args.storage == "f16"
-    traffic_tag = "-f16" if f16 else ""   # counted traffic is kept per storage format
+    value, ms_per_step = res["value"], res["ms_per_step"]
     out = {"metric": METRIC, "value": round(value, 3), "unit": "iters/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
@@ -250,60 +367,25 @@ def main():
            "config": {"workload": w.describe() + f", K {args.mode}" + (", binary16 K" if f16 else ""),
                       "n": n, "d": d, "k": k, "iters": w.iters, "kernel": w.kind, "mode": args.mode,
                       "storage": args.storage, "parallelism": "1 GPU"}}
-
-    def avg(ph):
-        ms, cnt = phases[ph]
-        return (ms / cnt if cnt else float("nan")), cnt
-
     if not args.no_timing:
-        spmm_ms, spmm_cnt = avg("spmm")
-        gemm_ms, gemm_cnt = avg("gemm")
-        kbuild_ms = sum(breakdown[p][0] for p in ("stage", "gemm", "fixup"))
-        iter_ms = sum(breakdown[p][0] for p in ("labels", "scatter", "spmm", "reduce", "assign", "onthefly", "other"))
-        flops = float(n) * (n + 1) * d                     # symmetric half of X X^T, 2 flops per MAC
-        out["kbuild_ms"] = round(kbuild_ms, 4)
-        out["kbuild_tflops"] = round(flops / (gemm_ms * 1e-3) / 1e12, 3) if gemm_cnt else None
-        out["kbuild_frac_mfma"] = round(out["kbuild_tflops"] / FP32_MFMA_PEAK_TF, 4) if out["kbuild_tflops"] else None
-        out["update_ms"] = round(iter_ms / w.iters, 4)
-        out["updates_per_s_loop"] = round(w.iters / (iter_ms * 1e-3), 2)
-        out["phases_ms_one_step"] = {p: round(breakdown[p][0], 4) for p in kkm.PHASES if breakdown[p][1]}
-        if args.mode in ("resident", "packed"):
-            # K streamed once per update: all of it, or its upper triangle
-            # n(n+1)/2 (what symmetry leaves to read; the stored diagonal
-            # tiles and column padding count against the kernel)
-            kname = "spmm_onehot" if args.mode == "resident" else "spmm_sym"
-            esize = 2.0 if f16 else 4.0   # bytes per stored entry
-            bytes_per = esize * n * n if args.mode == "resident" else esize * n * (n + 1) / 2
-            gbs = bytes_per / (spmm_ms * 1e-3) / 1e9
-            out["roofline"] = {"kernel": kname, "bound": "hbm", "achieved": round(gbs, 1),
-                               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                               "traffic": counted_traffic(kname, args.config, args.mode + traffic_tag),
-                               "traffic_unit": "GB per launch (algorithmic %.4f)" % (bytes_per / 1e9),
-                               "avg_launch_ms": round(spmm_ms, 5), "launches": spmm_cnt,
-                               "stored_K_bytes": info["bytes_K"]}
-        else:
-            otf_ms, otf_cnt = avg("onthefly")
-            otf_tf = flops / (otf_ms * 1e-3) / 1e12   # the symmetric half, per update
-            out["roofline"] = {"kernel": "onthefly", "bound": "mfma", "achieved": round(otf_tf, 2),
-                               "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
-                               "frac": round(otf_tf / FP32_MFMA_PEAK_TF, 4), "traffic": None,
-                               "traffic_unit": "GB per launch", "avg_launch_ms": round(otf_ms, 5),
-                               "launches": otf_cnt,
-                               "work": "n(n+1)d flop per update (symmetric half of X X^T)"}
-        tf = out["kbuild_tflops"]
-        if gemm_cnt:
-            out["roofline_kbuild"] = {"kernel": "gemm_kappa", "bound": "mfma", "achieved": tf,
-                                      "peak": FP32_MFMA_PEAK_TF, "unit": "TFLOP/s",
-                                      "frac": round(tf / FP32_MFMA_PEAK_TF, 4) if tf else None,
-                                      "traffic": counted_traffic("gemm_kappa", args.config, args.mode + traffic_tag),
-                                      "traffic_unit": "GB per launch", "avg_launch_ms": round(gemm_ms, 5),
-                                      "gauss_fixups": info["fixups"]}
-    if not args.no_timing:
-        out["kmeanspp"] = time_seeding(kkm, ctx, n, k, info["d_pad"])
+        out.update(roofline_fields(args, w, args.mode, res))
+        out["kmeanspp"] = res["kmeanspp"]
+    # The other storage modes of the same workload (the resident K and the
+    # on-the-fly sweep of workload 5): fewer jobs each, reported beside the
+    # headline under their own keys.
+    for m in extra:
+        steps_x, warm_x = max(1, min(args.steps, args.extra_steps)), 1
+        rx = measure(args, w, X, cl0, m, steps_x, warm_x, kkm, torch)
+        key = {"resident": "run_resident", "onthefly": "run_onthefly", "packed": "run_packed"}[m]
+        ent = {"mode": m, "value": round(rx["value"], 3), "unit": "iters/s", "steps": steps_x,
+               "warmup": warm_x, "ms_per_step": round(rx["ms_per_step"], 4),
+               "stored_K_bytes": rx["info"]["bytes_K"]}
+        if not args.no_timing:
+            ent.update(roofline_fields(args, w, m, rx))
+        out[key] = ent
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline_sized(w, X, cl0, args.cpu_seconds)
-    kkm.kkm_destroy(ctx)
     print(json.dumps(out), flush=True)
 
 
