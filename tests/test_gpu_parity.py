@@ -186,27 +186,66 @@ def test_blobs_stepwise_along_engine_trajectory(oracle):
     print(f"[gpu] workload 1: {flips} near-tie flips over {w.iters} updates", flush=True)
 
 
-def test_stop_rules_match_oracle(oracle):
-    """tol = 0 stops when no id changed, tol > 0 also on a small objective drop,
-    tol < 0 runs every update; on certified well-separated input the counts match."""
+STOP_GOLDEN = ["stop_rule_linear_1d_a.json", "stop_rule_linear_1d_b.json"]
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("name", STOP_GOLDEN)
+def test_stop_rule_hand_worked(name, mode):
+    """The loop and its stop rule (Alg. 1 'while not converged'; the tol reading)
+    on the hand-worked trajectories of tests/golden: the relative drop of J
+    reaches tol at update t = 2, one update before tol = 0 stops, and at
+    tol = 0.25 (fixture a) and 1/16 (fixture b) with equality.  Every value is
+    exact in fp32 and fp64, so done, the final ids and J must match exactly."""
+    import json
+    import os
     _torch_cuda()
-    X, lab = datagen.make_points(1)
-    rng = np.random.default_rng(1)
-    cl0 = lab.copy()
-    scr = rng.random(lab.size) < 0.9
-    cl0[scr] = rng.integers(0, 8, int(scr.sum()))
-    K = oracle.Kernel("poly", 0.01, 1.0, 2).matrix(X)
-    assert min(_margins(oracle, K, cl0, 8, 30)) > 1e-3
-    with Engine(X, "poly", 0.01, 1.0, 2) as eng:
-        dones = []
-        for tol in (0.0, 0.95, -1.0):
-            cl_ref, done_ref, hist_ref, _ = oracle.iterate_full(K, cl0, 8, 30, tol=tol)
-            cl, done, hist = eng.iterate(cl0, 8, 30, tol=tol)
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", name)))
+    X = np.array(g["X"], dtype=np.float32)
+    cl0 = np.array(g["cl0"], dtype=np.int32)
+    with Engine(X, "linear", mode=mode) as eng:
+        for r in g["runs"]:
+            cl, done, hist = eng.iterate(cl0, g["k"], r["max_iter"], tol=r["tol"])
+            assert done == r["done"], (r["tol"], done, r["done"])
+            np.testing.assert_array_equal(cl, r["cl_final"])
+            np.testing.assert_array_equal(hist, r["obj_hist"])
+
+
+def _chain(oracle):
+    """Twelve tight groups of 40 points on a line (3-D, sigma 0.05), two clusters
+    from a misplaced split: Lloyd moves the boundary over 7 updates, and the
+    relative drops of J are 0.239, 0.118, 0.057, 0.110, 0.168, 0.206."""
+    pos = [4, 8, 14, 16, 18, 20, 24, 25, 27, 31, 53, 54]
+    lab = [0, 0, 1, 0, 1, 1, 1, 1, 1, 1, 1, 1]
+    rng = np.random.default_rng(31)
+    X = np.zeros((len(pos) * 40, 3), np.float32)
+    X[:, 0] = np.repeat(pos, 40)
+    X = (X + 0.05 * rng.standard_normal(X.shape)).astype(np.float32)
+    cl0 = np.repeat(lab, 40).astype(np.int32)
+    perm = rng.permutation(X.shape[0])
+    return X[perm], cl0[perm]
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_stop_rules_match_oracle(oracle, mode):
+    """tol = 0 stops when no id changed, tol > 0 also on a small relative drop of
+    J, tol < 0 runs every update.  On a certified well-separated trajectory of 7
+    updates, tol = 0.08 stops after update 3 and tol = 0.15 after update 2:
+    both differ from tol = 0 and from the first update where the rule can fire,
+    so a rule with the drop's sign flipped (which fires there) fails."""
+    _torch_cuda()
+    X, cl0 = _chain(oracle)
+    K = oracle.Kernel("linear").matrix(X)
+    assert min(_margins(oracle, K, cl0, 2, 40)) > 1e-3
+    expect = {0.0: 7, 0.08: 4, 0.15: 3, -1.0: 40}
+    with Engine(X, "linear", mode=mode) as eng:
+        for tol, want in expect.items():
+            cl_ref, done_ref, hist_ref, _ = oracle.iterate_full(K, cl0, 2, 40, tol=tol)
+            assert done_ref == want, (tol, done_ref)
+            cl, done, hist = eng.iterate(cl0, 2, 40, tol=tol)
             assert done == done_ref, (tol, done, done_ref)
             np.testing.assert_array_equal(cl, cl_ref)
             assert np.max(np.abs(hist - hist_ref) / np.abs(hist_ref)) <= TOL
-            dones.append(done)
-    assert dones == [3, 2, 30]
 
 
 @pytest.mark.parametrize("mode", MODES)

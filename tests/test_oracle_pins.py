@@ -55,6 +55,26 @@ def check_golden(o, path):
                                    rtol=1e-7, atol=1e-9)
 
 
+def check_stop_golden(o, path):
+    """A hand-worked trajectory of the loop (Alg. 1) and the stop rule under several tol."""
+    g = json.load(open(path))
+    kp = g["kernel"]
+    kern = o.Kernel(kp["kind"], kp["gamma"], kp["coef0"], kp["degree"])
+    X = np.array(g["X"], dtype=np.float32)
+    K = kern.matrix(X)
+    k = g["k"]
+    for u in g["updates"]:
+        out = o.step_full(K, np.array(u["cl"]), k)
+        np.testing.assert_array_equal(out["cl"], u["cl_new"])
+        assert out["changed"] == u["changed"]
+        assert out["J"] == u["J"]
+    for r in g["runs"]:
+        cl, done, hist, traj = o.iterate_full(K, np.array(g["cl0"], dtype=np.int32), k, r["max_iter"], tol=r["tol"])
+        assert done == r["done"], (path, r["tol"], done, r["done"])
+        np.testing.assert_array_equal(cl, r["cl_final"])
+        np.testing.assert_array_equal(hist, r["obj_hist"])
+
+
 def check_poly_explicit(o, seed=0, n=48, d=4, k=5, degree=2, gamma=0.7, coef0=1.3):
     rng = np.random.default_rng(seed)
     X = rng.standard_normal((n, d)).astype(np.float32)
@@ -119,6 +139,12 @@ def check_linear_lloyd(o, seed=3, n=300, d=3, k=6, iters=8):
                          ids=os.path.basename)
 def test_golden_worked_examples(oracle, path):
     check_golden(oracle, path)
+
+
+@pytest.mark.parametrize("path", sorted(glob.glob(os.path.join(GOLDEN, "stop_rule_*.json"))),
+                         ids=os.path.basename)
+def test_golden_stop_rule(oracle, path):
+    check_stop_golden(oracle, path)
 
 
 def test_linear_kernel_is_blas_gram(oracle):
@@ -306,8 +332,30 @@ def _mutants(o):
     def shifted_ids(K_rows, cl, k):
         return K_rows @ o.one_hot((np.asarray(cl) + 1) % k, k)
 
+    def stop_sign_flip(tol, changed, J_prev, J_cur):
+        if tol < 0:
+            return False
+        if changed == 0:
+            return True
+        return bool(tol > 0 and J_prev is not None and (J_cur - J_prev) <= tol * abs(J_prev))
+
+    def stop_current_ref(tol, changed, J_prev, J_cur):
+        if tol < 0:
+            return False
+        if changed == 0:
+            return True
+        return bool(tol > 0 and J_prev is not None and (J_prev - J_cur) <= tol * abs(J_cur))
+
+    def stop_strict(tol, changed, J_prev, J_cur):
+        if tol < 0:
+            return False
+        if changed == 0:
+            return True
+        return bool(tol > 0 and J_prev is not None and (J_prev - J_cur) < tol * abs(J_prev))
+
     return {"distances": [no_diag, sign_flip], "self_terms": [z_single_norm], "assign": [argmax],
-            "mask": [wrong_index], "one_hot_product": [shifted_ids]}
+            "mask": [wrong_index], "one_hot_product": [shifted_ids],
+            "stop_now": [stop_sign_flip, stop_current_ref, stop_strict]}
 
 
 _CHECKS = [
@@ -316,11 +364,14 @@ _CHECKS = [
     check_poly_explicit,
     check_gauss_explicit,
     check_linear_lloyd,
+    lambda o: check_stop_golden(o, os.path.join(GOLDEN, "stop_rule_linear_1d_a.json")),
+    lambda o: check_stop_golden(o, os.path.join(GOLDEN, "stop_rule_linear_1d_b.json")),
 ]
 
 
 @pytest.mark.parametrize("name,idx", [("distances", 0), ("distances", 1), ("self_terms", 0),
-                                      ("assign", 0), ("mask", 0), ("one_hot_product", 0)])
+                                      ("assign", 0), ("mask", 0), ("one_hot_product", 0),
+                                      ("stop_now", 0), ("stop_now", 1), ("stop_now", 2)])
 def test_pins_catch_planted_mistakes(oracle, monkeypatch, name, idx):
     oracle.__dict__.setdefault("_orig_distances", oracle.distances)
     oracle.__dict__.setdefault("_orig_self_terms", oracle.self_terms)
