@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 5
+#define KKM_ABI_VERSION 6
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -67,9 +67,14 @@ typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
  * KKM_PACKED_MAX_K clusters; it is the fastest mode for small k.  ONTHEFLY
  * never stores K: every iteration recomputes its tiles and folds them
  * straight into E, which is the paper's single-GPU sliding-window baseline
- * (Section VI-D) done tile by tile.  AUTO picks RESIDENT when K fits the
- * memory budget, else ONTHEFLY (it never picks PACKED, whose k limit is not
- * known when K is built). */
+ * (Section VI-D) done tile by tile.  AUTO picks by the memory budget and
+ * the cluster count the caller announces in kkm_params.k_hint:
+ *   k_hint in 1..KKM_PACKED_FAST_K: PACKED if it fits (measured fastest for
+ *     k <= 16 on every workload of n >= 20000), else as below;
+ *   otherwise: RESIDENT if it fits, else PACKED if it fits (and k_hint is 0
+ *     or at most KKM_PACKED_MAX_K), else ONTHEFLY.
+ * A kkm_iterate with more than KKM_PACKED_MAX_K clusters on a K that AUTO
+ * stored PACKED (k_hint 0) fails with KKM_ERR_ARG. */
 typedef enum kkm_mode {
   KKM_MODE_AUTO = 0,
   KKM_MODE_RESIDENT = 1,
@@ -77,6 +82,7 @@ typedef enum kkm_mode {
   KKM_MODE_PACKED = 3
 } kkm_mode;
 #define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
+#define KKM_PACKED_FAST_K 16 /* AUTO stores PACKED for a k_hint up to this */
 
 /* Number format of a stored K (RESIDENT or PACKED; ONTHEFLY stores nothing
  * and ignores it).  F32 keeps the fp32 entries.  F16 keeps them in IEEE
@@ -99,6 +105,8 @@ typedef struct kkm_params {
   int32_t degree; /* POLY: integer exponent, 1..16.  Ignored otherwise. */
   int32_t mode;   /* kkm_mode */
   int32_t storage;/* kkm_storage of a stored K (ignored ONTHEFLY) */
+  int32_t k_hint; /* clusters the loop will run with, 1..KKM_MAX_K, or 0 if not
+                     known; only AUTO reads it (see kkm_mode) */
 } kkm_params;
 
 typedef struct kkm_ctx kkm_ctx; /* opaque; owns K, the staged points and all scratch */
@@ -158,9 +166,18 @@ int kkm_destroy(kkm_ctx *ctx);
  * the last failure of a call that had no context (kkm_create, kkm_plan). */
 const char *kkm_last_error(const kkm_ctx *ctx);
 
+/* Warning of the last build on ctx ("" if none); with ctx NULL, of the last
+ * kkm_check_build_args on the calling thread.  A build that warns still
+ * succeeds.  The one warning: a polynomial kernel with coef0 < 0 or
+ * gamma < 0 is not positive semidefinite (Eq. 2 with integer degree is PSD
+ * only for gamma, coef0 >= 0), so K may have negative eigenvalues and the
+ * objective need not fall from update to update. */
+const char *kkm_last_warning(const kkm_ctx *ctx);
+
 /* Pure host planning, no HIP call.  Picks the mode for a problem and the
  * device bytes it needs (K, staged points, per-iteration scratch for k
- * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget.
+ * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget and k
+ * as a build with k_hint = k does (see kkm_mode).
  * storage: kkm_storage of K (sizes K and the row scales).
  * Errors: KKM_ERR_ARG (bad sizes or storage, or PACKED with
  * k > KKM_PACKED_MAX_K), KKM_ERR_OOM (even the on-the-fly mode does not fit,
@@ -169,7 +186,8 @@ int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t request
              int32_t *mode_out, size_t *bytes_out);
 
 /* Host-only argument checks that the entry points apply first; exported so
- * they can be exercised without a GPU.  Return KKM_OK or KKM_ERR_ARG. */
+ * they can be exercised without a GPU.  Return KKM_OK or KKM_ERR_ARG;
+ * kkm_check_build_args also sets the warning kkm_last_warning(NULL) reads. */
 int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params *params);
 int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
 
@@ -177,7 +195,8 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  * X:      device, n x d fp32 row-major.  The engine copies it (zero-padded to
  *         d_pad columns); the caller may free X once this call has returned.
  * n:      points, 1 .. 2^31-1.   d: features, 1 .. 65536.
- * kind:   kkm_kind.   params: host pointer (gamma, coef0, degree, mode, storage).
+ * kind:   kkm_kind.   params: host pointer (gamma, coef0, degree, mode, storage,
+ *         k_hint).
  * RESIDENT: stores K (n rows, stride ld) in device memory; diag K is exact
  *   (Gaussian: exactly 1).  Gaussian entries whose expansion
  *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are

@@ -382,92 +382,124 @@ hipError_t launch_gemm_kappa_panel(const float* Xp, const float* nrm, const unsi
 
 // ---- Gaussian fix-up: |x_i - x_j|^2 summed from the coordinate differences.
 //
-// Phase 1: workgroups b, b + kFixSegs, ... share list segment b % kFixSegs;
-// 16 lanes per listed pair, float4 steps along k, fixed shuffle tree.
-// Phase 2 (only when some segment received more entries than it holds):
-// every entry of the upper triangle is re-tested from the stored K with the
-// epilogue's estimate.  The counts are read on the device, so the build needs
-// no host round trip.
-// A block (c1 > 0: rows [r0, r1) and columns [c0, c1) stored at
-// (i - r0, j - c0)) lists and stores each of its entries once.
+// Both passes below evaluate a recomputed entry with the same routine: a group
+// of 16 lanes, lane gl summing the float4 chunks gl, gl + 16, ... in order,
+// then a fixed shuffle tree over the group.  So an entry recomputed twice gets
+// the same bits, and its mirror (written by the same lane) equals it.
+__device__ inline float sqdist_group16(const float* __restrict__ Xp, int64_t i, int64_t j, int d_pad, int gl) {
+  const float4* xi = (const float4*)(Xp + i * d_pad);
+  const float4* xj = (const float4*)(Xp + j * d_pad);
+  const int nq = d_pad >> 2;
+  float s = 0.f;
+  for (int cc = gl; cc < nq; cc += 16) {
+    const float4 a = xi[cc], b = xj[cc];
+    float dx = a.x - b.x;
+    s = fmaf(dx, dx, s);
+    dx = a.y - b.y;
+    s = fmaf(dx, dx, s);
+    dx = a.z - b.z;
+    s = fmaf(dx, dx, s);
+    dx = a.w - b.w;
+    s = fmaf(dx, dx, s);
+  }
+  s += __shfl_xor(s, 8, 16);
+  s += __shfl_xor(s, 4, 16);
+  s += __shfl_xor(s, 2, 16);
+  s += __shfl_xor(s, 1, 16);
+  return s;
+}
+
+// Store a recomputed entry (i, j) and, in the square layouts, its mirror.  A
+// block (c1 > 0: rows [r0, r1) and columns [c0, c1) stored at (i - r0, j - c0))
+// stores each of its entries once; the square layouts get pairs with i < j.
 template <typename T>
-__global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp,
-                                                          const float* __restrict__ nrm, int64_t n,
-                                                          int d_pad, int64_t ld, bool packed, int64_t r0,
-                                                          int64_t r1, int64_t c0, int64_t c1, KappaParams kp,
-                                                          const int2* __restrict__ list,
-                                                          const unsigned long long* __restrict__ counts,
-                                                          long long seg_cap, T* __restrict__ K) {
-  const bool panel = c1 > 0;
+__device__ inline void store_fixed(T* __restrict__ K, int64_t i, int64_t j, float s, int64_t ld, bool packed,
+                                   int64_t r0, int64_t c0, bool panel, const KappaParams& kp) {
+  const T v = (T)__builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
+  if (panel) {
+    K[(i - r0) * ld + (j - c0)] = v;
+  } else if (packed) {
+    K[packed_row(i, ld) + j] = v;
+    if (i / kTile == j / kTile) K[packed_row(j, ld) + i] = v;
+  } else {
+    K[i * ld + j] = v;
+    K[j * ld + i] = v;
+  }
+}
+
+__device__ inline bool fix_list_overflowed(const unsigned long long* __restrict__ counts, long long seg_cap) {
   __shared__ int overflow;
   if (threadIdx.x == 0) overflow = 0;
   __syncthreads();
-  for (int q = threadIdx.x; q < kFixSegs; q += 256)
+  for (int q = threadIdx.x; q < kFixSegs; q += blockDim.x)
     if (counts[q] > (unsigned long long)seg_cap) overflow = 1;
+  __syncthreads();
+  return overflow != 0;
+}
+
+// Pass 1: the listed pairs.  Workgroups b, b + kFixSegs, ... share list
+// segment b % kFixSegs; a group of 16 lanes per pair.
+template <typename T>
+__global__ __launch_bounds__(256) void gauss_fixup_kernel(const float* __restrict__ Xp, int d_pad, int64_t ld,
+                                                          bool packed, int64_t r0, int64_t c0, bool panel,
+                                                          KappaParams kp, const int2* __restrict__ list,
+                                                          const unsigned long long* __restrict__ counts,
+                                                          long long seg_cap, T* __restrict__ K) {
   const int seg = (int)(blockIdx.x % kFixSegs), part = (int)(blockIdx.x / kFixSegs);
   const int parts = (int)(gridDim.x / kFixSegs);
   const unsigned long long c = counts[seg];
   const long long count = c < (unsigned long long)seg_cap ? (long long)c : seg_cap;
   const int2* seg_list = list + (int64_t)seg * seg_cap;
   const int g = threadIdx.x >> 4, gl = threadIdx.x & 15;
-  const int nq = d_pad >> 2;
   for (long long p = (long long)part * 16 + g; p < count; p += (long long)parts * 16) {
     const int2 ij = seg_list[p];
-    const float4* xi = (const float4*)(Xp + (int64_t)ij.x * d_pad);
-    const float4* xj = (const float4*)(Xp + (int64_t)ij.y * d_pad);
-    float s = 0.f;
-    for (int cc = gl; cc < nq; cc += 16) {
-      const float4 a = xi[cc], b = xj[cc];
-      float dx = a.x - b.x;
-      s = fmaf(dx, dx, s);
-      dx = a.y - b.y;
-      s = fmaf(dx, dx, s);
-      dx = a.z - b.z;
-      s = fmaf(dx, dx, s);
-      dx = a.w - b.w;
-      s = fmaf(dx, dx, s);
-    }
-    s += __shfl_xor(s, 8, 16);
-    s += __shfl_xor(s, 4, 16);
-    s += __shfl_xor(s, 2, 16);
-    s += __shfl_xor(s, 1, 16);
-    if (gl == 0) {  // square layouts list pairs with i < j: (i, j) is stored in both
-      const T v = (T)__builtin_amdgcn_exp2f(kp.neg_g_log2e * s);
-      if (panel) {
-        K[(int64_t)(ij.x - r0) * ld + (ij.y - c0)] = v;
-      } else if (packed) {
-        K[packed_row(ij.x, ld) + ij.y] = v;
-        if (ij.x / kTile == ij.y / kTile) K[packed_row(ij.y, ld) + ij.x] = v;
-      } else {
-        K[(int64_t)ij.x * ld + ij.y] = v;
-        K[(int64_t)ij.y * ld + ij.x] = v;
-      }
-    }
+    const float s = sqdist_group16(Xp, ij.x, ij.y, d_pad, gl);
+    if (gl == 0) store_fixed(K, ij.x, ij.y, s, ld, packed, r0, c0, panel, kp);
   }
-  __syncthreads();
-  if (!overflow) return;
-  if (panel) {
-    for (int64_t i = r0 + blockIdx.x; i < r1; i += gridDim.x) {
-      const float ni = nrm[i];
-      T* row = K + (i - r0) * ld;
-      for (int64_t j = c0 + threadIdx.x; j < c1; j += 256) {
-        const float v = (float)row[j - c0];
-        if (j != i && gauss_needs_fix(v, ni, nrm[j], kp))
-          row[j - c0] = (T)gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
-      }
-    }
-    return;
-  }
-  for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+}
+
+// Pass 2, launched after pass 1 and only doing work when some list segment
+// received more entries than it holds: every entry of the upper triangle (of
+// the block) is re-tested from the stored K with the epilogue's estimate.
+// Each wavefront tests 64 entries at once and recomputes the flagged ones
+// four at a time, one 16-lane group each.  An entry pass 1 already fixed may
+// be flagged again; it is recomputed to the same value.
+template <typename T>
+__global__ __launch_bounds__(256) void gauss_refix_kernel(const float* __restrict__ Xp,
+                                                          const float* __restrict__ nrm, int64_t n, int d_pad,
+                                                          int64_t ld, bool packed, int64_t r0, int64_t r1,
+                                                          int64_t c0, int64_t c1, KappaParams kp,
+                                                          const unsigned long long* __restrict__ counts,
+                                                          long long seg_cap, T* __restrict__ K) {
+  if (!fix_list_overflowed(counts, seg_cap)) return;
+  const bool panel = c1 > 0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, gl = lane & 15;
+  const int64_t ilo = panel ? r0 : 0, ihi = panel ? r1 : n;
+  for (int64_t i = ilo + blockIdx.x; i < ihi; i += gridDim.x) {  // uniform over the workgroup
     const float ni = nrm[i];
-    const int64_t ri = packed ? packed_row(i, ld) : i * ld;
-    for (int64_t j = i + 1 + threadIdx.x; j < n; j += 256) {
-      const float v = (float)K[ri + j];
-      if (gauss_needs_fix(v, ni, nrm[j], kp)) {
-        const T w = (T)gauss_direct(Xp + i * d_pad, Xp + j * d_pad, d_pad, kp);
-        K[ri + j] = w;
-        if (!packed) K[j * ld + i] = w;
-        else if (i / kTile == j / kTile) K[packed_row(j, ld) + i] = w;
+    const int64_t jlo = panel ? c0 : i + 1, jhi = panel ? c1 : n;
+    const int64_t ri = panel ? (i - r0) * ld - c0 : (packed ? packed_row(i, ld) : i * ld);
+    for (int64_t jb = jlo + wave * 64; jb < jhi; jb += 256) {  // uniform over the wavefront
+      const int64_t j = jb + lane;
+      bool need = false;
+      if (j < jhi && j != i) need = gauss_needs_fix((float)K[ri + j], ni, nrm[j], kp);
+      uint64_t m = __ballot(need);
+      while (m) {
+        // group g takes the g-th lowest flagged lane of this round
+        uint64_t mm = m;
+        int src = -1;
+        for (int q = 0; q <= g; ++q) {
+          if (!mm) {
+            src = -1;
+            break;
+          }
+          src = __ffsll((unsigned long long)mm) - 1;
+          mm &= mm - 1;
+        }
+        const int64_t jj = jb + (src < 0 ? 0 : src);
+        const float s = sqdist_group16(Xp, i, src < 0 ? i : jj, d_pad, gl);
+        if (src >= 0 && gl == 0) store_fixed(K, i, jj, s, ld, packed, r0, c0, panel, kp);
+        for (int q = 0; q < 4 && m; ++q) m &= m - 1;
       }
     }
   }
@@ -477,12 +509,19 @@ hipError_t launch_gauss_fixup(const float* Xp, const float* nrm, int64_t n, int 
                               bool packed, bool f16, const KappaParams& kp, const int2* fix_list,
                               const unsigned long long* fix_count, long long seg_cap, void* K,
                               hipStream_t s, int64_t r0, int64_t r1, int64_t c0, int64_t c1) {
-  if (f16)
-    hipLaunchKernelGGL(gauss_fixup_kernel<half_t>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                       ld, packed, r0, r1, c0, c1, kp, fix_list, fix_count, seg_cap, (half_t*)K);
-  else
-    hipLaunchKernelGGL(gauss_fixup_kernel<float>, dim3(16 * kFixSegs), dim3(256), 0, s, Xp, nrm, n, d_pad,
-                       ld, packed, r0, r1, c0, c1, kp, fix_list, fix_count, seg_cap, (float*)K);
+  const bool panel = c1 > 0;
+  const dim3 grid(16 * kFixSegs), block(256);
+  if (f16) {
+    hipLaunchKernelGGL(gauss_fixup_kernel<half_t>, grid, block, 0, s, Xp, d_pad, ld, packed, r0, c0, panel, kp,
+                       fix_list, fix_count, seg_cap, (half_t*)K);
+    hipLaunchKernelGGL(gauss_refix_kernel<half_t>, grid, block, 0, s, Xp, nrm, n, d_pad, ld, packed, r0, r1, c0,
+                       c1, kp, fix_count, seg_cap, (half_t*)K);
+  } else {
+    hipLaunchKernelGGL(gauss_fixup_kernel<float>, grid, block, 0, s, Xp, d_pad, ld, packed, r0, c0, panel, kp,
+                       fix_list, fix_count, seg_cap, (float*)K);
+    hipLaunchKernelGGL(gauss_refix_kernel<float>, grid, block, 0, s, Xp, nrm, n, d_pad, ld, packed, r0, r1, c0,
+                       c1, kp, fix_count, seg_cap, (float*)K);
+  }
   return hipGetLastError();
 }
 

@@ -33,6 +33,7 @@ struct Alloc {
 };
 
 thread_local std::string g_noctx_err;
+thread_local std::string g_noctx_warn;  // last warning of kkm_check_build_args on this thread
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
@@ -123,6 +124,7 @@ struct kkm_ctx {
   int device = 0;
   size_t budget = 0, held = 0;
   std::string err;
+  std::string warn;  // warning of the last build ("" if none)
 
   bool built = false;
   // A block of K (one GPU's share): rows [pr0, pr1) and columns [pc0, pc1);
@@ -385,6 +387,16 @@ int ensure_ws(kkm_ctx* c, int k, int iters) {
     int rc = carve_ws(c, k);
     if (rc) return rc;
   }
+  // A rebuild of the same shape keeps the scratch, but a panel or block of
+  // that shape may sit at other columns of K: the fields that locate it (and
+  // the build's buffers) are refreshed on every call.
+  IterBufs& b = c->ib;
+  b.col0 = c->pc1 > 0 ? c->pc0 : 0;
+  b.ncol = c->pc1 > 0 ? c->pc1 - c->pc0 : c->wsz.n;
+  b.diagK = c->diagK;
+  b.trK = c->trK;
+  b.kw = c->kw;
+  b.kf16 = c->storage == KKM_STORE_F16;
   if (c->iter_ws < iters || !c->obj) {
     free_hist(c);
     int cap = std::max(iters, 64);
@@ -475,6 +487,48 @@ int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
   return KKM_OK;
 }
 
+// The mode AUTO resolves to, and the device bytes of a mode.  k_known: k is
+// the cluster count the loop will run with; otherwise (a build without a
+// hint) k only sizes the scratch and the mode is picked without it.
+//   AUTO with k known: PACKED when k <= KKM_PACKED_FAST_K and it fits (it
+//   streams half the bytes per update, and its per-label column side stays
+//   below the HBM time up to 16 labels); else RESIDENT when it fits; else
+//   PACKED when k <= KKM_PACKED_MAX_K and it fits; else ONTHEFLY.
+//   AUTO with k unknown: RESIDENT, else PACKED, else ONTHEFLY, whichever
+//   fits first.
+// ONTHEFLY is picked only when no stored K fits: at every width measured
+// (d >= 54) a stored K is at least as fast per update.
+int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, size_t mem_budget, int32_t requested_mode,
+              int32_t storage, int32_t* mode_out, size_t* bytes_out) {
+  if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
+    return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
+  if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_PACKED)
+    return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
+  if (requested_mode == KKM_MODE_PACKED && k_known && k > KKM_PACKED_MAX_K)
+    return fail(nullptr, KKM_ERR_ARG, "packed storage handles k <= %d, not %d", KKM_PACKED_MAX_K, k);
+  if (storage != KKM_STORE_F32 && storage != KKM_STORE_F16) return fail(nullptr, KKM_ERR_ARG, "bad storage=%d", storage);
+  auto need_for = [&](int m) {
+    const Sizes s = sizes_for(n, d, m);
+    const size_t scales = row_scaled(m, storage, KKM_POLY) ? (size_t)n * 4 + 256 : 0;
+    return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m, storage) + scales;
+  };
+  auto fits = [&](int m) { return need_for(m) <= mem_budget; };
+  int mode = requested_mode;
+  if (mode == KKM_MODE_AUTO) {
+    if (k_known && k <= KKM_PACKED_FAST_K && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
+    else if (fits(KKM_MODE_RESIDENT)) mode = KKM_MODE_RESIDENT;
+    else if ((!k_known || k <= KKM_PACKED_MAX_K) && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
+    else mode = KKM_MODE_ONTHEFLY;
+  }
+  const size_t need = need_for(mode);
+  if (mode_out) *mode_out = mode;
+  if (bytes_out) *bytes_out = need;
+  static const char* names[] = {"auto", "resident", "on-the-fly", "packed"};
+  if (need > mem_budget)
+    return fail(nullptr, KKM_ERR_OOM, "%s mode needs %zu bytes, budget %zu", names[mode], need, mem_budget);
+  return KKM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -482,6 +536,8 @@ extern "C" {
 int kkm_abi_version(void) { return KKM_ABI_VERSION; }
 
 const char* kkm_last_error(const kkm_ctx* ctx) { return ctx ? ctx->err.c_str() : g_noctx_err.c_str(); }
+
+const char* kkm_last_warning(const kkm_ctx* ctx) { return ctx ? ctx->warn.c_str() : g_noctx_warn.c_str(); }
 
 int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params* p) {
   if (n < 1 || n > 2147483647LL) return fail(nullptr, KKM_ERR_ARG, "n=%lld must be in [1, 2^31-1]", (long long)n);
@@ -493,11 +549,25 @@ int kkm_check_build_args(int64_t n, int32_t d, int32_t kind, const kkm_params* p
     return fail(nullptr, KKM_ERR_ARG, "mode=%d is not AUTO(0), RESIDENT(1), ONTHEFLY(2) or PACKED(3)", p->mode);
   if (p->storage != KKM_STORE_F32 && p->storage != KKM_STORE_F16)
     return fail(nullptr, KKM_ERR_ARG, "storage=%d is not F32(0) or F16(1)", p->storage);
+  if (p->k_hint < 0 || p->k_hint > KKM_MAX_K)
+    return fail(nullptr, KKM_ERR_ARG, "k_hint=%d must be 0 (unknown) or in [1, %d]", p->k_hint, KKM_MAX_K);
+  g_noctx_warn.clear();
   if (kind == KKM_POLY) {
     if (!(std::isfinite(p->gamma) && std::isfinite(p->coef0)))
       return fail(nullptr, KKM_ERR_ARG, "polynomial gamma and coef0 must be finite");
     if (p->degree < 1 || p->degree > 16)
       return fail(nullptr, KKM_ERR_ARG, "polynomial degree=%d must be in [1, 16]", p->degree);
+    // (gamma x.y + c)^p is a positive semidefinite kernel for gamma >= 0,
+    // c >= 0 and integer p (a sum of products of PSD kernels); otherwise K
+    // may have negative eigenvalues and J need not fall from update to update.
+    if (p->coef0 < 0.f || p->gamma < 0.f) {
+      char buf[256];
+      snprintf(buf, sizeof buf,
+               "polynomial kernel with gamma=%g, coef0=%g is not positive semidefinite: the objective J "
+               "need not decrease from update to update",
+               (double)p->gamma, (double)p->coef0);
+      g_noctx_warn = buf;
+    }
   }
   if (kind == KKM_GAUSS && !(p->gamma > 0.f && std::isfinite(p->gamma)))
     return fail(nullptr, KKM_ERR_ARG, "Gaussian gamma=%g must be finite and > 0", (double)p->gamma);
@@ -516,26 +586,7 @@ int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t request
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
     return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
   if (k < 1 || k > KKM_MAX_K || (int64_t)k > n) return fail(nullptr, KKM_ERR_ARG, "bad k=%d", k);
-  if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_PACKED)
-    return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
-  if (requested_mode == KKM_MODE_PACKED && k > KKM_PACKED_MAX_K)
-    return fail(nullptr, KKM_ERR_ARG, "packed storage handles k <= %d, not %d", KKM_PACKED_MAX_K, k);
-  if (storage != KKM_STORE_F32 && storage != KKM_STORE_F16) return fail(nullptr, KKM_ERR_ARG, "bad storage=%d", storage);
-  auto need_for = [&](int m) {
-    const Sizes s = sizes_for(n, d, m);
-    const size_t scales = row_scaled(m, storage, KKM_POLY) ? (size_t)n * 4 + 256 : 0;
-    return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m, storage) + scales;
-  };
-  int mode = requested_mode;
-  if (mode == KKM_MODE_AUTO)
-    mode = need_for(KKM_MODE_RESIDENT) <= mem_budget ? KKM_MODE_RESIDENT : KKM_MODE_ONTHEFLY;
-  const size_t need = need_for(mode);
-  if (mode_out) *mode_out = mode;
-  if (bytes_out) *bytes_out = need;
-  static const char* names[] = {"auto", "resident", "on-the-fly", "packed"};
-  if (need > mem_budget)
-    return fail(nullptr, KKM_ERR_OOM, "%s mode needs %zu bytes, budget %zu", names[mode], need, mem_budget);
-  return KKM_OK;
+  return plan_impl(n, d, k, true, mem_budget, requested_mode, storage, mode_out, bytes_out);
 }
 
 int kkm_create(kkm_ctx** out, void* hip_stream, size_t mem_budget) {
@@ -577,7 +628,9 @@ namespace {
 int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, const kkm_params* params,
                int64_t pr0, int64_t pr1, int64_t pc0, int64_t pc1) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  c->warn.clear();
   if (kkm_check_build_args(n, d, kind, params) != KKM_OK) return fail(c, KKM_ERR_ARG, "%s", g_noctx_err.c_str());
+  c->warn = g_noctx_warn;
   if (!X) return fail(c, KKM_ERR_ARG, "X is NULL");
   const bool panel = pc1 > 0;
   int32_t mode = KKM_MODE_RESIDENT;
@@ -585,13 +638,17 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
   if (panel) {
     if (params->storage != KKM_STORE_F32) return fail(c, KKM_ERR_ARG, "a block of K is stored in fp32");
   } else {
-    // plan with k = 1: the k-dependent scratch is sized when kkm_iterate is called
+    // plan with the caller's k hint (else k = 1 sizes the scratch and the
+    // mode is picked without k): the k-dependent scratch is sized when
+    // kkm_iterate is called
     size_t held_by_build = 0;
     for (const Alloc& a : c->build_allocs) held_by_build += a.bytes;
     for (const Alloc& a : c->ws_allocs) held_by_build += a.bytes;
     for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
     const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
-    if (kkm_plan(n, d, 1, budget_left, params->mode, params->storage, &mode, &need) != KKM_OK)
+    const int32_t kh = std::min<int64_t>(params->k_hint, n);
+    if (plan_impl(n, d, kh > 0 ? kh : 1, kh > 0, budget_left, params->mode, params->storage, &mode, &need) !=
+        KKM_OK)
       return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
   }
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");

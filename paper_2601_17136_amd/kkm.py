@@ -22,6 +22,7 @@ KKM_STORE_F32, KKM_STORE_F16 = 0, 1
 STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
+KKM_PACKED_FAST_K = 16
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
           "seed")
 KINDS = {"linear": KKM_LINEAR, "poly": KKM_POLY, "gauss": KKM_GAUSS}
@@ -37,7 +38,8 @@ class KKMError(RuntimeError):
 
 class kkm_params(ctypes.Structure):
     _fields_ = [("gamma", ctypes.c_float), ("coef0", ctypes.c_float),
-                ("degree", ctypes.c_int32), ("mode", ctypes.c_int32), ("storage", ctypes.c_int32)]
+                ("degree", ctypes.c_int32), ("mode", ctypes.c_int32), ("storage", ctypes.c_int32),
+                ("k_hint", ctypes.c_int32)]
 
 
 class kkm_timing(ctypes.Structure):
@@ -58,6 +60,7 @@ _vp, _i32, _i64, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ct
 _SIGS = {
     "kkm_abi_version": ([], _i32),
     "kkm_last_error": ([_vp], ctypes.c_char_p),
+    "kkm_last_warning": ([_vp], ctypes.c_char_p),
     "kkm_create": ([ctypes.POINTER(_vp), _vp, _sz], _i32),
     "kkm_destroy": ([_vp], _i32),
     "kkm_plan": ([_i64, _i32, _i32, _sz, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
@@ -160,8 +163,21 @@ def kkm_plan(n: int, d: int, k: int, mem_budget: int, mode: int = KKM_MODE_AUTO,
     return m.value, b.value
 
 
-def make_params(gamma=1.0, coef0=0.0, degree=1, mode=KKM_MODE_AUTO, storage=KKM_STORE_F32) -> kkm_params:
-    return kkm_params(float(gamma), float(coef0), int(degree), int(mode), int(storage))
+def make_params(gamma=1.0, coef0=0.0, degree=1, mode=KKM_MODE_AUTO, storage=KKM_STORE_F32,
+                k_hint=0) -> kkm_params:
+    return kkm_params(float(gamma), float(coef0), int(degree), int(mode), int(storage), int(k_hint))
+
+
+def kkm_last_warning(ctx=None) -> str:
+    m = lib().kkm_last_warning(ctx)
+    return m.decode() if m else ""
+
+
+def _warn_if_any(ctx):
+    msg = kkm_last_warning(ctx)
+    if msg:
+        import warnings
+        warnings.warn(msg, RuntimeWarning, stacklevel=3)
 
 
 def kkm_check_build_args(n, d, kind, params: kkm_params) -> int:
@@ -176,6 +192,7 @@ def kkm_build_kernel(ctx, X, n: int, d: int, kind: int, params: kkm_params) -> N
     import torch
     _check(lib().kkm_build_kernel(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
                                   int(kind), ctypes.byref(params)), ctx)
+    _warn_if_any(ctx)
 
 
 def kkm_iterate(ctx, V, k: int, max_iter: int, tol: float = -1.0):
@@ -211,6 +228,7 @@ def kkm_build_panel(ctx, X, n: int, d: int, kind: int, params: kkm_params, c0: i
     import torch
     _check(lib().kkm_build_panel(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
                                  int(kind), ctypes.byref(params), int(c0), int(c1)), ctx)
+    _warn_if_any(ctx)
 
 
 def _stored(ctx):
@@ -254,6 +272,7 @@ def kkm_build_block(ctx, X, n: int, d: int, kind: int, params: kkm_params, r0: i
     import torch
     _check(lib().kkm_build_block(ctx, _dev_ptr(X, torch.float32, "X", int(n) * int(d)), int(n), int(d),
                                  int(kind), ctypes.byref(params), int(r0), int(r1), int(c0), int(c1)), ctx)
+    _warn_if_any(ctx)
 
 
 def kkm_block_spmm(ctx, cl, k: int, E_out) -> None:

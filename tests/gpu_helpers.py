@@ -52,7 +52,7 @@ class Engine:
     """A context with a built kernel matrix on torch's current stream."""
 
     def __init__(self, X: np.ndarray, kind: str, gamma=1.0, coef0=0.0, degree=1, mode="resident",
-                 mem_budget=0, storage="f32"):
+                 mem_budget=0, storage="f32", k_hint=0):
         import torch
 
         from paper_2601_17136_amd import kkm
@@ -61,7 +61,8 @@ class Engine:
         self.X = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).cuda()
         self.ctx = kkm.kkm_create(kkm.current_stream_handle(), mem_budget)
         kkm.kkm_build_kernel(self.ctx, self.X, self.n, self.d, kkm.KINDS[kind],
-                             kkm.make_params(gamma, coef0, degree, kkm.MODES[mode], kkm.STORAGES[storage]))
+                             kkm.make_params(gamma, coef0, degree, kkm.MODES[mode], kkm.STORAGES[storage],
+                                             k_hint))
 
     def K_rows(self, r0=0, r1=None):
         import torch

@@ -35,9 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 5
+    assert kkm.kkm_abi_version() == 6
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 5" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 6" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
@@ -77,6 +77,9 @@ def test_library_is_built_for_gfx950_only(L):
     (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 3, kkm.KKM_STORE_F16), True),
     (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 1, 2), False),
     (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 1, -1), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0, 0, 10), True),        # k_hint
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0, 0, -1), False),
+    (1000, 16, kkm.KKM_POLY, (1.0, 1.0, 2, 0, 0, kkm.KKM_MAX_K + 1), False),
 ])
 def test_build_argument_checks(L, n, d, kind, params, ok):
     rc = kkm.kkm_check_build_args(n, d, kind, kkm.make_params(*params))
@@ -109,7 +112,7 @@ def test_null_context_is_rejected_without_a_gpu(L):
 
 
 def test_plan_resident_when_it_fits(L):
-    n, d, k = 20000, 784, 10
+    n, d, k = 20000, 784, 64
     mode, need = kkm.kkm_plan(n, d, k, 288 << 30)
     assert mode == kkm.KKM_MODE_RESIDENT
     assert 4 * n * n <= need <= 4 * n * n * 1.1
@@ -117,10 +120,43 @@ def test_plan_resident_when_it_fits(L):
 
 def test_plan_falls_back_to_on_the_fly(L):
     n, d, k = 200000, 54, 7
-    mode, need = kkm.kkm_plan(n, d, k, 100 << 30)          # K alone is 160 GB
+    mode, need = kkm.kkm_plan(n, d, k, 50 << 30)           # K alone is 160 GB, its triangle 80 GB
     assert mode == kkm.KKM_MODE_ONTHEFLY and need < (1 << 30)
-    mode, need = kkm.kkm_plan(n, d, k, 288 << 30)
+    mode, need = kkm.kkm_plan(n, d, 100, 288 << 30)        # too many labels for packed to pay
     assert mode == kkm.KKM_MODE_RESIDENT and need > 4 * n * n
+    mode, need = kkm.kkm_plan(n, d, 100, 100 << 30)        # and beyond its limit of 64
+    assert mode == kkm.KKM_MODE_ONTHEFLY
+
+
+# Each workload's storage mode measured fastest on MI355X (whole job, updates/s):
+# 1: packed (n = 2000, k = 8); 2: packed 3593 vs resident 2810; 3: packed 562 vs
+# resident 372; 4 (k = 64): resident 153 vs packed 126; 5: packed 66.0 vs
+# resident 38.8 vs on the fly 36.1.
+MEASURED_FASTEST = {1: kkm.KKM_MODE_PACKED, 2: kkm.KKM_MODE_PACKED, 3: kkm.KKM_MODE_PACKED,
+                    4: kkm.KKM_MODE_RESIDENT, 5: kkm.KKM_MODE_PACKED}
+
+
+@pytest.mark.parametrize("cfg", sorted(MEASURED_FASTEST))
+def test_plan_auto_picks_the_measured_fastest(L, cfg):
+    """AUTO with the workload's k (kkm_plan, or a build's k_hint) on one
+    MI355X's memory (288 GB less 5%) picks the mode measured fastest."""
+    from paper_2601_17136_amd import datagen
+    w = datagen.WORKLOADS[cfg]
+    mode, _ = kkm.kkm_plan(w.n, w.d, w.k, int(0.95 * (288 << 30)))
+    assert mode == MEASURED_FASTEST[cfg]
+
+
+def test_nonpsd_polynomial_warns(L):
+    """Eq. 2 with coef0 < 0 (or gamma < 0) is not a PSD kernel: the build
+    argument check passes and leaves a warning; a PSD kernel leaves none."""
+    assert kkm.kkm_check_build_args(100, 4, kkm.KKM_POLY, kkm.make_params(1.0, -1.0, 2)) == kkm.KKM_OK
+    assert "positive semidefinite" in kkm.kkm_last_warning()
+    assert kkm.kkm_check_build_args(100, 4, kkm.KKM_POLY, kkm.make_params(-0.5, 1.0, 2)) == kkm.KKM_OK
+    assert "positive semidefinite" in kkm.kkm_last_warning()
+    assert kkm.kkm_check_build_args(100, 4, kkm.KKM_POLY, kkm.make_params(1.0, 1.0, 2)) == kkm.KKM_OK
+    assert kkm.kkm_last_warning() == ""
+    assert kkm.kkm_check_build_args(100, 4, kkm.KKM_GAUSS, kkm.make_params(0.5, -3.0, 1)) == kkm.KKM_OK
+    assert kkm.kkm_last_warning() == ""
 
 
 def test_plan_packed_holds_half_of_k(L):
@@ -137,8 +173,8 @@ def test_plan_packed_holds_half_of_k(L):
     with pytest.raises(kkm.KKMError) as e:          # more clusters than the packed SpMM handles
         kkm.kkm_plan(n, d, kkm.KKM_PACKED_MAX_K + 1, 1 << 40, kkm.KKM_MODE_PACKED)
     assert e.value.code == kkm.KKM_ERR_ARG
-    mode, _ = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO)   # AUTO never picks packed
-    assert mode == kkm.KKM_MODE_ONTHEFLY
+    mode, _ = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO)   # k <= 16: AUTO picks packed
+    assert mode == kkm.KKM_MODE_PACKED
 
 
 def test_plan_binary16_storage_halves_k(L):
@@ -150,10 +186,11 @@ def test_plan_binary16_storage_halves_k(L):
     _, need32 = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F32)
     assert mode == kkm.KKM_MODE_RESIDENT
     assert 2 * n * n <= need16 <= 0.51 * need32
-    mode, needp = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
-    assert mode == kkm.KKM_MODE_RESIDENT and needp == need16
-    _, needpk = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_PACKED, kkm.KKM_STORE_F16)
-    assert needpk < 0.53 * need16
+    mode, needp = kkm.kkm_plan(n, d, 100, 100 << 30, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
+    _, need16_k100 = kkm.kkm_plan(n, d, 100, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
+    assert mode == kkm.KKM_MODE_RESIDENT and needp == need16_k100
+    mode, needpk = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
+    assert mode == kkm.KKM_MODE_PACKED and needpk < 0.53 * need16
     with pytest.raises(kkm.KKMError) as e:
         kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, 7)
     assert e.value.code == kkm.KKM_ERR_ARG

@@ -179,3 +179,50 @@ def test_panels_workload5_shape(oracle):
     flips = assignment_mismatches(out["cl"][rows], ref["cl"], ref["D"])
     np.testing.assert_array_equal(out["took"], np.bincount(out["cl"], minlength=k))
     print(f"[gpu] panels cfg 5: K {eK:.2e} E {eE:.2e} z {ez:.2e} flips {flips}", flush=True)
+
+
+def test_panels_rebuilt_on_one_context(oracle):
+    """All G panels of equal width built one after another on ONE context, so
+    every rebuild after the first keeps the buffers of the first: the panel's
+    column offset must still reach the self-term parts (ids of its own points)
+    and the assignment (diag K of its own points).  A polynomial kernel makes
+    diag K differ from point to point."""
+    import torch
+
+    from paper_2601_17136_amd import kkm
+    n, d, k, G = 768, 11, 5, 3                 # three panels of 256 points
+    X = datagen.separated_blobs(n, d, k, seed=8, spread=2.0, sigma=1.0)[0]
+    cl = datagen.random_init(n, k, 35)
+    kern = oracle.Kernel("poly", 0.3, 1.0, 2)
+    ref = oracle.step_full(kern.matrix(X), cl, k)
+    Xd = torch.from_numpy(X).cuda()
+    cl_d = torch.from_numpy(cl).cuda()
+    params = kkm.make_params(0.3, 1.0, 2, kkm.KKM_MODE_RESIDENT)
+    bounds = panel_bounds(n, G)
+    assert len({c1 - c0 for c0, c1 in bounds}) == 1
+    ctx = kkm.kkm_create(kkm.current_stream_handle())
+    try:
+        zsum = np.zeros(k)
+        for c0, c1 in bounds:
+            kkm.kkm_build_panel(ctx, Xd, n, d, kkm.KKM_POLY, params, c0, c1)
+            zpart, counts = kkm.kkm_panel_spmm(ctx, cl_d, k)
+            zsum += zpart
+        c = counts.astype(np.float64)
+        z = np.where(counts > 0, zsum / np.where(counts > 0, c * c, 1.0), 0.0)
+        new = np.empty(n, dtype=np.int32)
+        E = np.empty((n, k), dtype=np.float32)
+        for c0, c1 in bounds:
+            kkm.kkm_build_panel(ctx, Xd, n, d, kkm.KKM_POLY, params, c0, c1)
+            kkm.kkm_panel_spmm(ctx, cl_d, k)
+            out = torch.empty(c1 - c0, dtype=torch.int32, device="cuda")
+            Eo = torch.empty((c1 - c0, k), device="cuda")
+            kkm.kkm_panel_assign(ctx, k, z, out, Eo)
+            new[c0:c1] = out.cpu().numpy()
+            E[c0:c1] = Eo.cpu().numpy()
+    finally:
+        kkm.kkm_destroy(ctx)
+    np.testing.assert_array_equal(counts, ref["counts"])
+    assert rel_err(z, ref["z"]) <= TOL
+    assert rowscaled_err(E, ref["E"]) <= TOL
+    flips = assignment_mismatches(new, ref["cl"], ref["D"])
+    print(f"[gpu] panels rebuilt on one context: {flips} near-tie flips", flush=True)

@@ -326,9 +326,44 @@ def test_gauss_fixup_overflow_path(oracle, mode):
     assert info["fixups"] > info["fixup_capacity"] > 0, info
     err = rowscaled_err(K, oracle.Kernel("gauss", 0.5).matrix(X))
     assert err <= TOL, err
+    # the re-test pass runs after the listed pairs and recomputes with the same
+    # routine: K is exactly symmetric and the same bits come back on a rebuild
+    np.testing.assert_array_equal(K, K.T)
+    with Engine(X, "gauss", 0.5, mode=mode, mem_budget=need + 4096) as eng:
+        np.testing.assert_array_equal(eng.K_rows(), K)
     with Engine(X, "gauss", 0.5, mode=mode) as eng:
         K2 = eng.K_rows()
     assert rowscaled_err(K2, oracle.Kernel("gauss", 0.5).matrix(X)) <= TOL
+
+
+@pytest.mark.parametrize("k_hint,want", [(8, "packed"), (40, "resident"), (0, "resident")])
+def test_auto_mode_follows_the_k_hint(oracle, k_hint, want):
+    """AUTO stores K packed when the announced k is at most 16 and fully
+    otherwise (memory allowing); either way the step matches the oracle."""
+    _torch_cuda()
+    from paper_2601_17136_amd import kkm
+    X = datagen.make_points(2, n=700, d=12)[0]
+    k = k_hint or 5
+    cl = datagen.random_init(700, k, 3)
+    ref = oracle.step_full(oracle.Kernel("gauss", 0.1).matrix(X), cl, k)
+    with Engine(X, "gauss", 0.1, mode="auto", k_hint=k_hint) as eng:
+        assert eng.info()["mode"] == kkm.MODES[want]
+        out = eng.step(cl, k)
+    assert rowscaled_err(out["E"], ref["E"]) <= TOL and rowscaled_err(out["D"], ref["D"]) <= TOL
+
+
+def test_nonpsd_polynomial_build_warns(oracle):
+    """A polynomial kernel with coef0 < 0 builds, warns that J need not fall,
+    and still matches the oracle's step."""
+    _torch_cuda()
+    X = datagen.make_points(2, n=300, d=6)[0]
+    cl = datagen.random_init(300, 4, 5)
+    with pytest.warns(RuntimeWarning, match="positive semidefinite"):
+        eng = Engine(X, "poly", 1.0, -2.0, 2)
+    with eng:
+        out = eng.step(cl, 4)
+    ref = oracle.step_full(oracle.Kernel("poly", 1.0, -2.0, 2).matrix(X), cl, 4)
+    assert rowscaled_err(out["E"], ref["E"]) <= TOL and rowscaled_err(out["D"], ref["D"]) <= TOL
 
 
 def test_packed_k_limit(oracle):
