@@ -83,6 +83,7 @@ typedef enum kkm_mode {
 } kkm_mode;
 #define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
 #define KKM_PACKED_FAST_K 16 /* AUTO stores PACKED for a k_hint up to this */
+#define KKM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20) /* static scratch of kkm_iterate_noalloc, per GPU */
 
 /* Number format of a stored K (RESIDENT or PACKED; ONTHEFLY stores nothing
  * and ignores it).  F32 keeps the fp32 entries.  F16 keeps them in IEEE
@@ -229,6 +230,24 @@ int kkm_build_kernel(kkm_ctx *ctx, const float *X, int64_t n, int32_t d, int32_t
  * Errors: KKM_ERR_ARG, KKM_ERR_STATE (no build), KKM_ERR_DEVICE_DATA, KKM_ERR_OOM, KKM_ERR_HIP. */
 int kkm_iterate(kkm_ctx *ctx, int32_t *V, int32_t k, int32_t max_iter, double tol,
                 int32_t *iters_done, double *obj_hist);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): kkm_iterate
+ * with the same arguments, results and errors, whose per-update scratch and
+ * objective history live in a static device array of
+ * KKM_NOALLOC_SCRATCH_BYTES per GPU (allocated when the library's code is
+ * loaded on that GPU, held until the process ends) instead of buffers the
+ * context allocates.  It calls no hipMalloc or hipFree; the K and staged
+ * points of the build are the context's.  Problems whose scratch does not fit
+ * (for example n = 20000 with packed K and k = 10 needs about 45 MB, with the
+ * full K about 4 MB) fail with KKM_ERR_ARG before anything is enqueued.  Every call
+ * on a GPU shares that GPU's array and leaves its contents behind: calls
+ * that overlap on one GPU (other threads, streams or contexts) race, so the
+ * caller serializes them.  No launch is bracketed by timing events.
+ * The context's own scratch, if an earlier kkm_iterate made one, is left as
+ * it was. */
+int kkm_iterate_noalloc(kkm_ctx *ctx, int32_t *V, int32_t k, int32_t max_iter, double tol,
+                        int32_t *iters_done, double *obj_hist);
 
 /* J(cl) = sum_i D(i, cl(i)) = tr K - sum_j |L_j| z_j for the ids V (device
  * int32[n]); written to *J (host).  Errors as kkm_iterate. */

@@ -12,6 +12,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -20,7 +21,32 @@
 
 using namespace kkm;
 
+// Device scratch of kkm_iterate_noalloc: one copy per GPU, held until the
+// process ends.  Host code never passes this name to a kernel or a copy (on
+// the host it is a stand-in, not a device address); it uses the address
+// hipGetSymbolAddress returns for the current device, looked up once per
+// device by kkm_create.
+static __device__ __align__(256) unsigned char scratch[KKM_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+std::mutex g_scratch_mu;
+std::vector<void*> g_scratch_ptr;  // by device ordinal; null until looked up
+
+// The device address of `scratch` on device dev (current), looked up once.
+hipError_t scratch_address(int dev, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 
 struct TimedLaunch {
   int phase;
@@ -168,6 +194,8 @@ struct kkm_ctx {
   int *sd_bestc = nullptr, *sd_centers = nullptr;
   double* sd_bsum = nullptr;
 
+  void* scratch = nullptr;  // this device's static scratch (kkm_iterate_noalloc)
+
   int32_t timing = 0;  // mask of timed phases
   std::vector<TimedLaunch> pending;
   std::vector<hipEvent_t> pool;
@@ -303,12 +331,11 @@ void free_build(kkm_ctx* c) {
   c->panel_e = false;
 }
 
-// Allocate one block and carve it (keeps the accounting to one number).
-int carve_ws(kkm_ctx* c, int k) {
+// Lay the per-update scratch for k clusters out over base (ws_bytes of it)
+// and clear what must start at zero.
+int carve_from(kkm_ctx* c, int k, void* base) {
   const Sizes& s = c->wsz;
-  void* base = nullptr;
-  int rc = dalloc(c, &base, ws_bytes(s, k, c->mode), c->ws_allocs, "iteration scratch");
-  if (rc) return rc;
+  int rc;
   char* p = (char*)base;
   auto take = [&](size_t bytes) {
     char* r = p;
@@ -379,6 +406,51 @@ int carve_ws(kkm_ctx* c, int k) {
   b.status = (int*)take(4);
   c->k_ws = k;
   return KKM_OK;
+}
+
+// The context's per-update scratch pointers, set aside while
+// kkm_iterate_noalloc lays its own out over the static scratch.
+struct SavedWs {
+  IterBufs ib;
+  int k_ws, iter_ws;
+  float *Xs, *nrm_s, *Epart, *Cpart;
+  int* cs;
+  OtfTables otb;
+  const int* epos;
+  int *counts[2], *clbuf[2], *changed;
+  double* obj;
+};
+
+SavedWs save_ws(const kkm_ctx* c) {
+  return SavedWs{c->ib, c->k_ws, c->iter_ws, c->Xs, c->nrm_s, c->Epart, c->Cpart, c->cs, c->otb, c->epos,
+                 {c->counts[0], c->counts[1]}, {c->clbuf[0], c->clbuf[1]}, c->changed, c->obj};
+}
+
+void restore_ws(kkm_ctx* c, const SavedWs& v) {
+  c->ib = v.ib;
+  c->k_ws = v.k_ws;
+  c->iter_ws = v.iter_ws;
+  c->Xs = v.Xs;
+  c->nrm_s = v.nrm_s;
+  c->Epart = v.Epart;
+  c->Cpart = v.Cpart;
+  c->cs = v.cs;
+  c->otb = v.otb;
+  c->epos = v.epos;
+  c->counts[0] = v.counts[0];
+  c->counts[1] = v.counts[1];
+  c->clbuf[0] = v.clbuf[0];
+  c->clbuf[1] = v.clbuf[1];
+  c->changed = v.changed;
+  c->obj = v.obj;
+}
+
+// Allocate one block and carve it (keeps the accounting to one number).
+int carve_ws(kkm_ctx* c, int k) {
+  void* base = nullptr;
+  int rc = dalloc(c, &base, ws_bytes(c->wsz, k, c->mode), c->ws_allocs, "iteration scratch");
+  if (rc) return rc;
+  return carve_from(c, k, base);
 }
 
 int ensure_ws(kkm_ctx* c, int k, int iters) {
@@ -601,9 +673,13 @@ int kkm_create(kkm_ctx** out, void* hip_stream, size_t mem_budget) {
     if (e != hipSuccess) return fail(nullptr, KKM_ERR_HIP, "hipMemGetInfo: %s", hipGetErrorString(e));
     mem_budget = (size_t)((double)freeb * 0.95);
   }
+  void* scr = nullptr;
+  e = scratch_address(dev, &scr);
+  if (e != hipSuccess) return fail(nullptr, KKM_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
   kkm_ctx* c = new kkm_ctx();
   c->stream = (hipStream_t)hip_stream;
   c->device = dev;
+  c->scratch = scr;
   c->budget = mem_budget;
   *out = c;
   return KKM_OK;
@@ -973,13 +1049,15 @@ int kkm_block_assign(kkm_ctx* c, const float* E, int64_t a0, int64_t a1, int32_t
   return KKM_OK;
 }
 
-int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
-                double* obj_hist) {
+}  // extern "C"
+
+namespace {
+
+// The loop of kkm_iterate on per-update scratch already laid out (c->ib and
+// the id, size and history buffers).
+int iterate_loop(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
+                 double* obj_hist) {
   int rc;
-  if ((rc = check_ready(c, k, max_iter))) return rc;
-  if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
-  if (iters_done) *iters_done = 0;
-  if ((rc = ensure_ws(c, k, max_iter))) return rc;
   if ((rc = label_pass(c, V))) return rc;
   const int* cur = V;
   int t = 0, status = 0;
@@ -1015,6 +1093,53 @@ int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol,
   if ((rc = status_error(c, status))) return rc;
   if (iters_done) *iters_done = t;
   return KKM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kkm_iterate(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
+                double* obj_hist) {
+  int rc;
+  if ((rc = check_ready(c, k, max_iter))) return rc;
+  if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
+  if (iters_done) *iters_done = 0;
+  if ((rc = ensure_ws(c, k, max_iter))) return rc;
+  return iterate_loop(c, V, k, max_iter, tol, iters_done, obj_hist);
+}
+
+int kkm_iterate_noalloc(kkm_ctx* c, int32_t* V, int32_t k, int32_t max_iter, double tol, int32_t* iters_done,
+                        double* obj_hist) {
+  int rc;
+  if ((rc = check_ready(c, k, max_iter))) return rc;
+  if (!V) return fail(c, KKM_ERR_ARG, "V is NULL");
+  if (iters_done) *iters_done = 0;
+  if (!c->scratch) return fail(c, KKM_ERR_STATE, "the static scratch of this device is not mapped");
+  const size_t ws = round_up((int64_t)ws_bytes(c->wsz, k, c->mode), 256);
+  const int cap = std::max(max_iter, 1);
+  const size_t hist = (size_t)cap * 12 + 512;
+  if (ws + hist > KKM_NOALLOC_SCRATCH_BYTES)
+    return fail(c, KKM_ERR_ARG,
+                "this problem (n=%lld, k=%d, %s storage, %d updates) needs %zu bytes of scratch; the static "
+                "scratch holds %zu: use kkm_iterate",
+                (long long)c->wsz.n, k, c->mode == KKM_MODE_PACKED ? "packed" : c->mode == KKM_MODE_RESIDENT ? "full" : "no",
+                max_iter, ws + hist, (size_t)KKM_NOALLOC_SCRATCH_BYTES);
+  // The context's own scratch (if any) is set aside for this call and put
+  // back after it; no launch is bracketed by events (creating one may allocate).
+  const SavedWs saved = save_ws(c);
+  const int32_t timing = c->timing;
+  c->timing = 0;
+  rc = carve_from(c, k, c->scratch);
+  if (!rc) {
+    c->obj = (double*)((char*)c->scratch + ws);
+    c->changed = (int*)((char*)c->obj + (size_t)cap * 8);
+    c->iter_ws = cap;
+    rc = iterate_loop(c, V, k, max_iter, tol, iters_done, obj_hist);
+  }
+  c->timing = timing;
+  restore_ws(c, saved);
+  return rc;
 }
 
 int kkm_step(kkm_ctx* c, const int32_t* cl_in, int32_t k, float* E, float* z, float* D, int32_t* cl_out,

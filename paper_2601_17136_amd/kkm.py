@@ -23,6 +23,7 @@ STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
 KKM_PACKED_FAST_K = 16
+KKM_NOALLOC_SCRATCH_BYTES = 64 << 20
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
           "seed")
 KINDS = {"linear": KKM_LINEAR, "poly": KKM_POLY, "gauss": KKM_GAUSS}
@@ -68,6 +69,7 @@ _SIGS = {
     "kkm_check_iterate_args": ([_i64, _i32, _i32], _i32),
     "kkm_build_kernel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
     "kkm_iterate": ([_vp, _vp, _i32, _i32, _f64, ctypes.POINTER(_i32), _vp], _i32),
+    "kkm_iterate_noalloc": ([_vp, _vp, _i32, _i32, _f64, ctypes.POINTER(_i32), _vp], _i32),
     "kkm_objective": ([_vp, _vp, _i32, ctypes.POINTER(_f64)], _i32),
     "kkm_step": ([_vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(_f64)], _i32),
     "kkm_init_kmeanspp": ([_vp, _i32, _vp, _vp, _vp], _i32),
@@ -202,6 +204,17 @@ def kkm_iterate(ctx, V, k: int, max_iter: int, tol: float = -1.0):
     hist = np.zeros(max(int(max_iter), 1), dtype=np.float64)
     _check(lib().kkm_iterate(ctx, _dev_ptr(V, torch.int32, "V"), int(k), int(max_iter), float(tol),
                              ctypes.byref(it), hist.ctypes.data), ctx)
+    return it.value, hist[:it.value].copy()
+
+
+def kkm_iterate_noalloc(ctx, V, k: int, max_iter: int, tol: float = -1.0):
+    """kkm_iterate on the library's static device scratch (no device allocation
+    in the call).  Returns (iters_done, obj_hist[:iters_done] as numpy fp64)."""
+    import torch
+    it = _i32()
+    hist = np.zeros(max(int(max_iter), 1), dtype=np.float64)
+    _check(lib().kkm_iterate_noalloc(ctx, _dev_ptr(V, torch.int32, "V"), int(k), int(max_iter), float(tol),
+                                     ctypes.byref(it), hist.ctypes.data), ctx)
     return it.value, hist[:it.value].copy()
 
 
