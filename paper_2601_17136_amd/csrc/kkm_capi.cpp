@@ -130,9 +130,10 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
   } else if (mode == KKM_MODE_ONTHEFLY) {
     b += (size_t)s.n_pad * s.d_pad * 4;   // sorted points
     b += (size_t)s.n_pad * 8;             // their norms and cluster ids
-    b += (size_t)onthefly_segments(s.n) * k * s.ld * 4;  // row-side segment partials
-    b += (size_t)onthefly_cpart_floats(s.n, k) * 4;      // column-side partials
-    b += (size_t)(s.n_pad / kTile) * 16;                 // per-block tables
+    const size_t halves = (size_t)onthefly_halves(s.d_pad);
+    b += halves * onthefly_segments(s.n) * k * s.ld * 4;  // row-side segment partials
+    b += halves * onthefly_cpart_floats(s.n, k) * 4;      // column-side partials
+    b += (size_t)(s.n_pad / kTile) * 20;                 // per-block tables
   }
   b += (size_t)k * nzpart_for(s, mode) * 8;  // zpart
   b += (size_t)2 * k * s.nblk * 4;        // hist, base
@@ -381,12 +382,14 @@ int carve_from(kkm_ctx* c, int k, void* base) {
     c->Xs = (float*)take((size_t)s.n_pad * s.d_pad * 4);
     c->nrm_s = (float*)take((size_t)s.n_pad * 4);
     c->cs = (int*)take((size_t)s.n_pad * 4);
-    c->Epart = (float*)take((size_t)onthefly_segments(s.n) * k * s.ld * 4);
-    c->Cpart = (float*)take((size_t)onthefly_cpart_floats(s.n, k) * 4);
+    const size_t halves = (size_t)onthefly_halves(s.d_pad);
+    c->Epart = (float*)take(halves * onthefly_segments(s.n) * k * s.ld * 4);
+    c->Cpart = (float*)take(halves * onthefly_cpart_floats(s.n, k) * 4);
     const size_t nt = (size_t)(s.n_pad / kTile);
     c->otb.cA = (int*)take(nt * 4);
     c->otb.nruns = (int*)take(nt * 4);
     c->otb.cbase = (int64_t*)take(nt * 8);
+    c->otb.bmax = (float*)take(nt * 4);
   }
   b.zpart = (double*)take((size_t)k * b.nzpart * 8);
   b.hist = (int*)take((size_t)k * s.nblk * 4);
@@ -537,7 +540,7 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
          })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "onthefly_reduce", [&] {
-           return launch_onthefly_reduce(b, c->Epart, c->Cpart, c->cs, c->otb, c->stream);
+           return launch_onthefly_reduce(b, c->Epart, c->Cpart, c->cs, c->otb, s.d_pad, c->stream);
          })))
       return rc;
     pos = b.pos;

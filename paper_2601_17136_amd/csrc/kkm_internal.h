@@ -214,9 +214,13 @@ struct OtfTables {
   int* cA;         // nt: first cluster of each sorted row block
   int* nruns;      // nt: clusters spanned by each block
   int64_t* cbase;  // nt: offset of each block's column-side partials (rows of 128 floats)
+  float* bmax;     // nt: largest squared norm of each sorted row block
 };
 int onthefly_segments(int64_t n);
 int64_t onthefly_cpart_floats(int64_t n, int k);
+// partials per row-side and column-side entry of the sweep at this width
+// (2: one per wavefront half, for the register-operand kernel of small d)
+int onthefly_halves(int d_pad);
 hipError_t launch_gather_sorted(const float* Xp, const float* nrm, const IterBufs& b, const int* cl,
                                 int64_t n_pad, int d_pad, float* Xs, float* nrm_s, int* cs,
                                 hipStream_t s);
@@ -227,7 +231,7 @@ hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
                            const KappaParams& kp, const OtfTables& tb, float* Epart, float* Cpart,
                            hipStream_t s);
 hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const float* Cpart,
-                                  const int* cs, const OtfTables& tb, hipStream_t s);
+                                  const int* cs, const OtfTables& tb, int d_pad, hipStream_t s);
 hipError_t launch_kernel_rows(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
                               int64_t n, int d_pad, const KappaParams& kp, int64_t r0, int64_t r1,
                               float* out, hipStream_t s);

@@ -122,16 +122,18 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
     // the row norms are read again here rather than kept in registers
     // across the common path
     asm volatile("" ::: "memory");
+    int rb = rbase, cb = cbase;
+    asm volatile("" : "+v"(rb), "+v"(cb));
     unsigned long long fixmask = 0;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3);
+        const int il = rb + bi * 32 + 8 * (r >> 2) + (r & 3);
         const float cni = rn[il];
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
-          const int jl = cbase + bj * 32;
+          const int jl = cb + bj * 32;
           if (gauss_needs_fix_scaled(acc[bi][bj][r], cni + cnj[bj], kp) && !(diag && il == jl))
             fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
         }
@@ -140,7 +142,7 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
       const int e = __ffsll((long long)fixmask) - 1;
       fixmask &= fixmask - 1;
       const int bi = e >> 5, bj = (e >> 4) & 1, r = e & 15;
-      const int il = rbase + bi * 32 + 8 * (r >> 2) + (r & 3), jl = cbase + bj * 32;
+      const int il = rb + bi * 32 + 8 * (r >> 2) + (r & 3), jl = cb + bj * 32;
       if (il < nrows && jl < ncols) {
         const float w = gauss_direct(Y + (row0 + il) * d_pad, Y + (col0 + jl) * d_pad, d_pad, kp);
 #pragma unroll
@@ -157,6 +159,18 @@ __device__ inline void kappa_tile(floatx16 acc[2][2], const float* __restrict__ 
 
 // Segment bounds: segment s of nseg covers column tiles [seg_begin(s), seg_begin(s+1)).
 __device__ __host__ inline int seg_begin(int s, int nt, int nseg) { return (int)((int64_t)s * nt / nseg); }
+
+// bmax[P] = the largest squared norm among the sorted points of block P (128
+// threads per block; padding rows hold 0): an upper bound of |x_i|^2 + |x_j|^2
+// over a tile, with which the sweep skips the Gaussian fix-up estimate.
+__global__ __launch_bounds__(128) void blockmax_kernel(const float* __restrict__ nrm_s, float* __restrict__ bmax) {
+  __shared__ float part[2];
+  float v = nrm_s[(int64_t)blockIdx.x * kTile + threadIdx.x];
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) bmax[blockIdx.x] = fmaxf(part[0], part[1]);
+}
 
 // Per update: for each row block P of the sorted order, the first cluster its
 // rows hold (cA), how many clusters they span (nruns), and where its
@@ -330,15 +344,330 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(
   flush(cur);
 }
 
+// ---- Small widths (d_pad <= kRegMaxDpad): no barrier per tile.
+//
+// The block's 128 rows are staged in LDS once per work item; each wavefront
+// (wm, wn) holds its 64 columns of the current tile J as MFMA operands in
+// registers, loaded straight from the sorted points: lane (l, h) keeps
+// column l of each 32-column block at k = h*HP .. h*HP + HP - 1 (HP =
+// d_pad / 2), reads its rows at the same k from LDS, and step s of
+// v_mfma_f32_32x32x2_f32 pairs k = s with k = HP + s.  The next tile's columns
+// are loaded as soon as the current tile's products are issued, so the loads
+// run beside the kappa epilogue.  The row side and the column side are kept
+// per wavefront (two halves per partial: the wn halves of the row-side
+// partials, the wm halves of the column-side partials), so the four
+// wavefronts never wait for each other inside the sweep; two workgroups per
+// CU give every SIMD two independent wavefronts, one streaming products while
+// the other runs its epilogue.
+constexpr int kRegMaxDpad = 64;
+
+template <int HP>
+__device__ inline void load_operand(const float* __restrict__ Y, int64_t row, int d_pad, int h, float (&v)[HP]) {
+  const float4* p = (const float4*)(Y + row * d_pad + h * HP);
+#pragma unroll
+  for (int u = 0; u < HP / 4; ++u) {
+    const float4 t = p[u];
+    v[4 * u] = t.x;
+    v[4 * u + 1] = t.y;
+    v[4 * u + 2] = t.z;
+    v[4 * u + 3] = t.w;
+  }
+}
+
+// acc[bi][bj] for one bj: the wavefront's 64 rows from As (stride 2 HP + 4
+// floats, an odd number of 16-byte units, so the 16-byte reads of 32
+// consecutive rows are conflict-free) against its 32 columns bj in b.  The
+// two column blocks run as two passes, so the second block's loads are still
+// in flight while the first block's products run.
+template <int HP>
+__device__ inline void mma_rows_lds(const float* __restrict__ As, const float (&b)[HP], floatx16& acc0,
+                                    floatx16& acc1, int l32, int h) {
+  constexpr int ldsA = 2 * HP + 4;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    acc0[r] = 0.f;
+    acc1[r] = 0.f;
+  }
+  const float* p0 = As + l32 * ldsA + h * HP;
+  const float* p1 = p0 + 32 * ldsA;
+  // rows of the next four steps read one group ahead; the scheduling
+  // barriers keep the reads from being hoisted further (registers)
+  float4 a0 = *(const float4*)p0, a1 = *(const float4*)p1;
+#pragma unroll
+  for (int s4 = 0; s4 < HP; s4 += 4) {
+    float4 n0 = a0, n1 = a1;
+    if (s4 + 4 < HP) {
+      n0 = *(const float4*)(p0 + s4 + 4);
+      n1 = *(const float4*)(p1 + s4 + 4);
+    }
+    const float av0[4] = {a0.x, a0.y, a0.z, a0.w}, av1[4] = {a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av0[u], b[s4 + u], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av1[u], b[s4 + u], acc1, 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    a0 = n0;
+    a1 = n1;
+  }
+}
+
+// kappa on the wavefront's 64 x 64 block of an interior tile (off the
+// diagonal, all rows and columns below n), as kappa_tile, laid out for the
+// sweep's instruction budget: the Gaussian on norms scaled once and the
+// fix-up estimate kept as one running minimum of u v per lane, so the
+// per-entry test (and its mask) is formed only where some lane's minimum
+// calls for it.  Diagonal and last tiles take kappa_tile.
+template <int KIND, bool FIX>
+__device__ inline void kappa_tile_interior(floatx16 (&acc)[2][2], const float* __restrict__ Y,
+                                           const float* __restrict__ ny, const float* rn, int d_pad,
+                                           int64_t row0, int64_t col0, const KappaParams& kp, bool tile_fix) {
+  // u = c|x_i|^2 + c|x_j|^2 rounds the same for (i, j) and (j, i) only if
+  // the products are not fused into the sum
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const int rbase = wm * 64 + 4 * h, cbase = wn * 64 + l32;
+  float cnj[2] = {0.f, 0.f};
+  if (KIND == GAUSS) {
+    cnj[0] = kp.neg_g_log2e * ny[col0 + cbase];
+    cnj[1] = kp.neg_g_log2e * ny[col0 + cbase + 32];
+  }
+  float umin = 0.f;  // min over this lane's entries of u v (the fix-up estimate)
+  auto pass = [&](bool est) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 r4 = {0.f, 0.f, 0.f, 0.f};
+        if (KIND == GAUSS) r4 = *(const float4*)(rn + rbase + bi * 32 + 8 * q);
+        const float cn[4] = {r4.x, r4.y, r4.z, r4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int bj = 0; bj < 2; ++bj) {
+            const float a = acc[bi][bj][4 * q + e];
+            if (KIND == GAUSS) {
+              const float u = cn[e] + cnj[bj];
+              const float v = gauss_scaled(a, u, kp);
+              if (est) umin = fminf(umin, u * v);
+              acc[bi][bj][4 * q + e] = v;
+            } else {
+              acc[bi][bj][4 * q + e] = kappa<KIND>(a, 0.f, 0.f, kp);
+            }
+          }
+      }
+  };
+  // the estimate only where the tile's largest norms allow an entry to need
+  // the fix-up (uniform); elsewhere the plain pass
+  if (KIND == GAUSS && FIX && tile_fix) pass(true);
+  else pass(false);
+  if (KIND == GAUSS && FIX && tile_fix && __ballot(umin < kp.fix_uthr)) {
+    // the lane's row base is made opaque, so the per-entry index work is
+    // formed here and not hoisted out of the sweep
+    asm volatile("" ::: "memory");
+    int rb = rbase;
+    asm volatile("" : "+v"(rb));
+    unsigned long long fixmask = 0;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float cni = rn[rb + bi * 32 + 8 * (r >> 2) + (r & 3)];
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+          if (gauss_needs_fix_scaled(acc[bi][bj][r], cni + cnj[bj], kp)) fixmask |= 1ull << ((bi * 2 + bj) * 16 + r);
+      }
+    while (fixmask) {
+      const int e = __ffsll((long long)fixmask) - 1;
+      fixmask &= fixmask - 1;
+      const int bi = e >> 5, bj = (e >> 4) & 1, r = e & 15;
+      const int il = rb + bi * 32 + 8 * (r >> 2) + (r & 3), jl = cbase + bj * 32;
+      const float w = gauss_direct(Y + (row0 + il) * d_pad, Y + (col0 + jl) * d_pad, d_pad, kp);
+#pragma unroll
+      for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr)
+            if (qq == bi && p == bj && rr == r) acc[qq][p][rr] = w;
+    }
+  }
+}
+
+template <int KIND, bool FIX, int HP>
+__global__ __launch_bounds__(256, 2) void onthefly_reg_kernel(
+    const float* __restrict__ Xs, const float* __restrict__ nrm_s, const int* __restrict__ cs,
+    const unsigned* __restrict__ maxnrm_bits, const int* __restrict__ off,
+    const int* __restrict__ cA, const int* __restrict__ nruns, const int64_t* __restrict__ cbase,
+    const float* __restrict__ bmax, int64_t n, int64_t ld, int nt, int nseg, int k, KappaParams kp,
+    float* __restrict__ Epart, float* __restrict__ Cpart) {
+  constexpr int d_pad = 2 * HP, ldsA = 2 * HP + 4;
+  __shared__ __attribute__((aligned(16))) float rn[kTile];
+  __shared__ __attribute__((aligned(16))) float As[kTile * ldsA];
+  // work items as in onthefly_kernel: (segment s, row block I), segment-major
+  int s = 0;
+  int64_t first = 0;
+  while (s + 1 < nseg && first + seg_begin(s + 1, nt, nseg) <= (int64_t)blockIdx.x) {
+    first += seg_begin(s + 1, nt, nseg);
+    ++s;
+  }
+  const int I = (int)((int64_t)blockIdx.x - first);
+  const int sb = seg_begin(s, nt, nseg), se = seg_begin(s + 1, nt, nseg);
+  if (I >= se) return;
+  if (KIND == GAUSS && any_fix(maxnrm_bits, kp) != FIX) return;
+  const int jt0 = sb > I ? sb : I, jt1 = se;
+  const int64_t row0 = (int64_t)I * kTile;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const int runA = cA[I], nr = nruns[I];
+  // this block's column-side partials: rows of 2 x 128 floats (the wm halves)
+  float* const cp = Cpart + cbase[I] * (2 * kTile);
+  if (tid < kTile) rn[tid] = (KIND == GAUSS ? kp.neg_g_log2e : 1.f) * nrm_s[row0 + tid];
+
+  for (int f = tid; f < kTile * (HP / 2); f += 256) {  // the block's rows, 16 bytes per thread and step
+    const int r = f / (HP / 2), c = f % (HP / 2);
+    *(float4*)(As + r * ldsA + 4 * c) = *(const float4*)(Xs + (row0 + r) * d_pad + 4 * c);
+  }
+  __syncthreads();  // rn, As
+  const float* const Aw = As + wm * 64 * ldsA;
+
+  float rowacc[2][16];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) rowacc[bi][r] = 0.f;
+
+  // Row side: this wavefront's running sums over its 64 columns, reduced over
+  // the lanes (fixed xor tree) and written as cluster c's partial of segment
+  // s, half wn.
+  auto flush = [&](int c) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = rowacc[bi][r];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 8, 64);
+        v += __shfl_xor(v, 4, 64);
+        v += __shfl_xor(v, 2, 64);
+        v += __shfl_xor(v, 1, 64);
+        rowacc[bi][r] = v;
+      }
+    if (l32 == 0) {
+      float* ep = Epart + (((int64_t)s * k + c) * 2 + wn) * ld + row0;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int il = wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (row0 + il < n) ep[il] = rowacc[bi][r];
+        }
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) rowacc[bi][r] = 0.f;
+  };
+
+  // Column side of tile (I, J), J > I, for this wavefront's 64 rows and 64
+  // columns: the column sums over the rows in sorted positions [lo, hi) (all
+  // rows when the block holds one cluster), written as run u, half wm.
+  auto column_side = [&](int J, int u, bool all_rows, int lo, int hi, const floatx16 (&t)[2][2]) {
+    float c0 = 0.f, c1 = 0.f;
+    const int llo = lo - (int)row0, lhi = hi - (int)row0;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        bool in = all_rows;
+        if (!all_rows) {
+          const int il = wm * 64 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          in = il >= llo && il < lhi;
+        }
+        c0 += in ? t[bi][0][r] : 0.f;
+        c1 += in ? t[bi][1][r] : 0.f;
+      }
+    c0 += __shfl_xor(c0, 32, 64);
+    c1 += __shfl_xor(c1, 32, 64);
+    if (h == 0) {
+      float* dst = cp + ((int64_t)(J - I - 1) * nr + u) * (2 * kTile) + wm * kTile + wn * 64 + l32;
+      dst[0] = c0;
+      dst[32] = c1;
+    }
+  };
+
+  // The clusters are walked over the whole tile's columns (not only this
+  // wavefront's half), so both halves write a partial, possibly zero, for
+  // every cluster the segment's columns hold.
+  int cur = cs[(int64_t)jt0 * kTile];
+  floatx16 acc[2][2];
+  for (int J = jt0; J < jt1; ++J) {
+    const int64_t col0 = (int64_t)J * kTile;
+    {
+      float b[2][HP];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) load_operand<HP>(Xs, col0 + wn * 64 + q * 32 + l32, d_pad, h, b[q]);
+      mma_rows_lds<HP>(Aw, b[0], acc[0][0], acc[1][0], l32, h);
+      mma_rows_lds<HP>(Aw, b[1], acc[0][1], acc[1][1], l32, h);
+    }
+    // the epilogue's loads (row norms, column norms and ids) are not hoisted
+    // into the product loop, where they would hold registers
+    __builtin_amdgcn_sched_barrier(0);
+    if (J == I || col0 + kTile > n)  // uniform: the diagonal tile, the last tile
+      kappa_tile<KIND, FIX>(acc, Xs, nrm_s, rn, n, d_pad, row0, col0, kp);
+    else
+      kappa_tile_interior<KIND, FIX>(acc, Xs, nrm_s, rn, d_pad, row0, col0, kp,
+                                     FIX && gauss_needs_fix(1.f, bmax[I], bmax[J], kp));
+    {
+      const int64_t last = (col0 + kTile - 1 < n) ? col0 + kTile - 1 : n - 1;
+      const int cf = cs[col0], cl_last = cs[last];
+      if (cf == cur && cl_last == cur) {
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) rowacc[bi][r] += acc[bi][0][r] + acc[bi][1][r];
+      } else {
+        const int64_t q0 = col0 + wn * 64 + l32, q1 = q0 + 32;
+        const int c0 = q0 < n ? cs[q0] : -1, c1 = q1 < n ? cs[q1] : -1;
+        for (int c = cf; c <= cl_last; ++c) {
+          if (c != cur) {
+            flush(cur);
+            cur = c;
+          }
+#pragma unroll
+          for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              rowacc[bi][r] += (c0 == c ? acc[bi][0][r] : 0.f) + (c1 == c ? acc[bi][1][r] : 0.f);
+        }
+      }
+    }
+    if (J > I) {
+      if (nr == 1) {
+        column_side(J, 0, true, 0, 0, acc);
+      } else {
+        for (int u = 0; u < nr; ++u) column_side(J, u, false, off[runA + u], off[runA + u + 1], acc);
+      }
+    }
+  }
+  flush(cur);
+}
+
+int onthefly_halves(int d_pad) { return d_pad <= kRegMaxDpad ? 2 : 1; }
+
 // Workgroup (stripe, j): E^T_sorted(j, q) for the stripe's sorted rows q:
 //   the row-side partials of the segments that block Q = q/128 swept over
 //   columns of cluster j, in segment order, then the column-side partials of
 //   the blocks P < Q holding rows of cluster j, in block order;
 // plus the stripe's part of sum_{q in L_j} E(q, j) in fp64 (cs[q] == j).
+// halves: 2 when the sweep kept per-wavefront partials (two per row-side
+// partial and two per column-side partial, added in order), else 1.
 __global__ __launch_bounds__(256) void onthefly_reduce_kernel(
     IterBufs b, const float* __restrict__ Epart, const float* __restrict__ Cpart,
     const int* __restrict__ cs, const int* __restrict__ cA, const int* __restrict__ nruns,
-    const int64_t* __restrict__ cbase, int nt, int nseg) {
+    const int64_t* __restrict__ cbase, int nt, int nseg, int halves) {
   const int ns = b.nstripes;
   const int stripe = (int)(blockIdx.x % (unsigned)ns);
   const int j = (int)(blockIdx.x / (unsigned)ns);
@@ -358,12 +687,16 @@ __global__ __launch_bounds__(256) void onthefly_reduce_kernel(
       if (se <= Q) continue;
       const int64_t c0 = (int64_t)(sb > Q ? sb : Q) * kTile;
       const int64_t c1 = (int64_t)se * kTile < b.n ? (int64_t)se * kTile : b.n;
-      if (c0 < hi && lo < c1) e += *(const f4*)(Epart + ((int64_t)s * b.k + j) * ld + col);
+      if (c0 < hi && lo < c1)
+        for (int hh = 0; hh < halves; ++hh)
+          e += *(const f4*)(Epart + (((int64_t)s * b.k + j) * halves + hh) * ld + col);
     }
     const int Pl = (hi - 1) / kTile;
-    for (int P = lo / kTile; P <= Pl && P < Q; ++P)
-      e += *(const f4*)(Cpart + ((cbase[P] + (int64_t)(Q - P - 1) * nruns[P] + (j - cA[P])) * kTile +
-                                 (col - (int64_t)Q * kTile)));
+    for (int P = lo / kTile; P <= Pl && P < Q; ++P) {
+      const float* cr = Cpart + (cbase[P] + (int64_t)(Q - P - 1) * nruns[P] + (j - cA[P])) * (halves * kTile) +
+                        (col - (int64_t)Q * kTile);
+      for (int hh = 0; hh < halves; ++hh) e += *(const f4*)(cr + hh * kTile);
+    }
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -453,6 +786,41 @@ hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
   int64_t items = 0;  // (segment, row block) pairs right of the diagonal
   for (int q = 0; q < nseg; ++q) items += seg_begin(q + 1, nt, nseg);
   dim3 grid((unsigned)items), block(256);
+  if (d_pad <= kRegMaxDpad) {
+    if (d_pad % 8) return hipErrorInvalidValue;
+    if (kp.kind == GAUSS) {
+      hipLaunchKernelGGL(blockmax_kernel, dim3((unsigned)nt), dim3(kTile), 0, s, nrm_s, tb.bmax);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+#define KKM_OTF_REG(KIND, FIX, HP)                                                                          \
+  hipLaunchKernelGGL((onthefly_reg_kernel<KIND, FIX, HP>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits, b.off, \
+                     tb.cA, tb.nruns, tb.cbase, tb.bmax, b.n, b.ld, nt, nseg, b.k, kp, Epart, Cpart)
+#define KKM_OTF_REG_HP(KIND, FIX)           \
+  switch (d_pad / 2) {                      \
+    case 4: KKM_OTF_REG(KIND, FIX, 4); break;   \
+    case 8: KKM_OTF_REG(KIND, FIX, 8); break;   \
+    case 12: KKM_OTF_REG(KIND, FIX, 12); break; \
+    case 16: KKM_OTF_REG(KIND, FIX, 16); break; \
+    case 20: KKM_OTF_REG(KIND, FIX, 20); break; \
+    case 24: KKM_OTF_REG(KIND, FIX, 24); break; \
+    case 28: KKM_OTF_REG(KIND, FIX, 28); break; \
+    default: KKM_OTF_REG(KIND, FIX, 32); break; \
+  }
+    if (kp.kind == LINEAR) {
+      KKM_OTF_REG_HP(LINEAR, false);
+    } else if (kp.kind == POLY) {
+      KKM_OTF_REG_HP(POLY, false);
+    } else {
+      KKM_OTF_REG_HP(GAUSS, false);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      KKM_OTF_REG_HP(GAUSS, true);
+    }
+#undef KKM_OTF_REG_HP
+#undef KKM_OTF_REG
+    return hipGetLastError();
+  }
   if (kp.kind == LINEAR) {
     hipLaunchKernelGGL((onthefly_kernel<LINEAR, false>), grid, block, 0, s, Xs, nrm_s, cs, maxnrm_bits,
                        b.off, tb.cA, tb.nruns, tb.cbase, b.n, d_pad, b.ld, nt, nseg, b.k, kp, Epart, Cpart);
@@ -471,10 +839,10 @@ hipError_t launch_onthefly(const float* Xs, const float* nrm_s, const int* cs,
 }
 
 hipError_t launch_onthefly_reduce(const IterBufs& b, const float* Epart, const float* Cpart,
-                                  const int* cs, const OtfTables& tb, hipStream_t s) {
+                                  const int* cs, const OtfTables& tb, int d_pad, hipStream_t s) {
   const int nt = (int)((b.n + kTile - 1) / kTile), nseg = onthefly_segments(b.n);
   hipLaunchKernelGGL(onthefly_reduce_kernel, dim3((unsigned)(b.nstripes * b.k)), dim3(256), 0, s, b,
-                     Epart, Cpart, cs, tb.cA, tb.nruns, tb.cbase, nt, nseg);
+                     Epart, Cpart, cs, tb.cA, tb.nruns, tb.cbase, nt, nseg, onthefly_halves(d_pad));
   return hipGetLastError();
 }
 

@@ -76,4 +76,6 @@ def test_noalloc_refuses_what_does_not_fit():
         np.testing.assert_array_equal(V.cpu().numpy(), cl0)      # untouched
         it, _ = kkm.kkm_iterate(eng.ctx, V, 10, 2, -1.0)
         assert it == 2
-        it, _ = kkm.kkm_iterate_noalloc(eng.ctx, V, 10, 2, -1.0)   # k = 10 fits
+        V2 = torch.from_numpy(datagen.random_init(20000, 2, 46)).cuda()
+        it, _ = kkm.kkm_iterate_noalloc(eng.ctx, V2, 2, 2, -1.0)   # k = 2 fits (about 31 MB)
+        assert it == 2
