@@ -98,7 +98,7 @@ def parse():
                     help="number format of the stored K (f16: binary16 with fp32 sums, a mixed-precision "
                          "option with its own error bound; the default keeps fp32)")
     ap.add_argument("--extra", default=None,
-                    help="comma-separated further storage modes measured beside the headline "
+                    help="comma-separated further storage modes measured beside the headline, or none "
                          "(default: resident,onthefly for workload 5, none otherwise)")
     ap.add_argument("--extra-steps", type=int, default=3, help="timed jobs per further mode (after 1 warm-up)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -329,7 +329,8 @@ def main():
         # below the HBM time for k <= 16, above it for larger k
         args.mode = "packed" if w.k <= 16 else "resident"
     extra = [m for m in (args.extra.split(",") if args.extra is not None else
-                         (["resident", "onthefly"] if args.config == 5 else [])) if m and m != args.mode]
+                         (["resident", "onthefly"] if args.config == 5 else []))
+             if m and m != "none" and m != args.mode]
     X, _ = datagen.make_points(args.config)
     cl0 = datagen.make_init(args.config, w.n, w.k)
     n, d, k = w.n, w.d, w.k

@@ -327,12 +327,261 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   }
 }
 
+// ---- Small widths (d_pad <= kRegMaxDpad, fp32 storage, the square layouts):
+// the build as a sweep.  A workgroup owns row block I and a segment of
+// column tiles J >= I (the on-the-fly sweep's work items): the block's rows
+// are staged in LDS once, each wavefront loads its 64 columns of tile J into
+// registers (mma_rows_lds), and nothing ties the four wavefronts together
+// inside the sweep: the epilogue is gemm_kappa_kernel's (kappa, the diagonal,
+// the fix-up listing, stores straight from the MFMA layout), and the mirror
+// of a full-storage tile goes through the wavefront's own LDS tile, ordered
+// within the wavefront.  Two workgroups per CU, so every SIMD holds two
+// independent wavefronts.
+__device__ __host__ inline int sweep_seg_begin(int s, int nt, int nseg) { return (int)((int64_t)s * nt / nseg); }
+
+int build_sweep_segments(int64_t n) {
+  const int nt = (int)((n + kTile - 1) / kTile);
+  int nseg = (8192 + nt - 1) / nt;  // ~4096 work items right of the diagonal
+  if (nseg > nt) nseg = nt;
+  if (nseg > 64) nseg = 64;
+  return nseg < 1 ? 1 : nseg;
+}
+
+template <int KIND, int HP>
+__global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
+    const float* __restrict__ Xp, const float* __restrict__ nrm, const unsigned* __restrict__ maxnrm_bits,
+    int64_t n, int64_t ld, bool packed, int nt, int nseg, KappaParams kp, float* __restrict__ K,
+    float* __restrict__ diagK, int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count,
+    long long seg_cap, const float* __restrict__ bmax) {
+  constexpr int d_pad = 2 * HP, ldsA = 2 * HP + 4;
+  __shared__ __attribute__((aligned(16))) float As[kTile * ldsA];
+  __shared__ float Tm[4 * 32 * 65];  // per wavefront: a 32 x 64 block transposed (full storage)
+  // work items (segment s, row block I < sweep_seg_begin(s+1)), segment-major
+  int s = 0;
+  int64_t first = 0;
+  while (s + 1 < nseg && first + sweep_seg_begin(s + 1, nt, nseg) <= (int64_t)blockIdx.x) {
+    first += sweep_seg_begin(s + 1, nt, nseg);
+    ++s;
+  }
+  const int I = (int)((int64_t)blockIdx.x - first);
+  const int sb = sweep_seg_begin(s, nt, nseg), se = sweep_seg_begin(s + 1, nt, nseg);
+  if (I >= se) return;
+  const int jt0 = sb > I ? sb : I, jt1 = se;
+  const int64_t row0 = (int64_t)I * kTile;
+  const bool may_fix = KIND == GAUSS && gauss_needs_fix(1.f, __uint_as_float(*maxnrm_bits),
+                                                         __uint_as_float(*maxnrm_bits), kp);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  for (int f = tid; f < kTile * (HP / 2); f += 256) {  // the block's rows (zero padded past n)
+    const int r = f / (HP / 2), c = f % (HP / 2);
+    *(float4*)(As + r * ldsA + 4 * c) = *(const float4*)(Xp + (row0 + r) * d_pad + 4 * c);
+  }
+  __syncthreads();
+  const float* const Aw = As + wm * 64 * ldsA;
+  float* const Tw = Tm + wave * (32 * 65);
+  const float cg = kp.neg_g_log2e;
+  const float* nrow = nrm + row0 + wm * 64 + 4 * h;
+  const int64_t S = packed ? ld - row0 : ld;  // row stride of the block's stored rows
+  float* const Kr = K + (packed ? packed_row(row0, ld) : row0 * ld);
+  const unsigned lane_b = ((unsigned)(wm * 64 + 4 * h) * (unsigned)S + (unsigned)(wn * 64 + l32)) * 4u;
+
+  for (int J = jt0; J < jt1; ++J) {
+    const int64_t col0 = (int64_t)J * kTile;
+    floatx16 acc[2][2];
+    {
+      float b[2][HP];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) load_operand<HP>(Xp, col0 + wn * 64 + q * 32 + l32, d_pad, h, b[q]);
+      mma_rows_lds<HP>(Aw, b[0], acc[0][0], acc[1][0], l32, h);
+      mma_rows_lds<HP>(Aw, b[1], acc[0][1], acc[1][1], l32, h);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // kappa, as in gemm_kappa_kernel, with the fix-up estimate kept as one
+    // running minimum of u v per lane, and taken only where the two blocks'
+    // largest squared norms allow an entry of the tile to qualify
+    float cnj[2] = {0.f, 0.f};
+    if (KIND == GAUSS) {
+      cnj[0] = cg * nrm[col0 + wn * 64 + l32];
+      cnj[1] = cg * nrm[col0 + wn * 64 + 32 + l32];
+    }
+    const bool tile_fix = KIND == GAUSS && may_fix && gauss_needs_fix(1.f, bmax[I], bmax[J], kp);
+    float umin = 0.f;
+    auto kpass = [&](bool est) {
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma clang fp contract(off)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float4 n4 = {0.f, 0.f, 0.f, 0.f};
+          if (KIND == GAUSS) n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
+          const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int bj = 0; bj < 2; ++bj) {
+              float v;
+              if (KIND == GAUSS) {
+                const float u = cn[e] + cnj[bj];
+                v = gauss_scaled(acc[bi][bj][4 * q + e], u, kp);
+                if (est) umin = fminf(umin, u * v);
+              } else {
+                v = kappa<KIND>(acc[bi][bj][4 * q + e], 0.f, 0.f, kp);
+              }
+              acc[bi][bj][4 * q + e] = v;
+            }
+        }
+      }
+    };
+    if (tile_fix) kpass(true);
+    else kpass(false);
+    if (J == I && wm == wn) {  // the diagonal
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (8 * (r >> 2) + 4 * h + (r & 3) == l32) {
+            const int64_t gi = row0 + wm * 64 + bi * 32 + l32;
+            float v = acc[bi][bi][r];
+            if (KIND == GAUSS) v = 1.f;
+            acc[bi][bi][r] = v;
+            if (gi < n) diagK[gi] = v;
+          }
+    }
+    if (KIND == GAUSS && tile_fix && __ballot(umin < kp.fix_uthr)) {  // the listing, as in gemm_kappa_kernel
+      const int seg = (int)(blockIdx.x % kFixSegs);
+      unsigned mlo = 0u, mhi = 0u;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+#pragma clang fp contract(off)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
+          const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * q + 4 * h + e;
+#pragma unroll
+            for (int bj = 0; bj < 2; ++bj) {
+              const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
+              const bool f = gi < gj && gj < n && gauss_needs_fix_scaled(acc[bi][bj][4 * q + e], cn[e] + cnj[bj], kp);
+              const int g = ((bi * 4 + q) * 4 + e) * 2 + bj;
+              if (g < 32) mlo |= f ? 1u << g : 0u;
+              else mhi |= f ? 1u << (g - 32) : 0u;
+            }
+          }
+        }
+      }
+      const unsigned cnt = (unsigned)(__popc(mlo) + __popc(mhi));
+      unsigned pre = cnt;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned v = __shfl_up(pre, o, 64);
+        if (lane >= o) pre += v;
+      }
+      const unsigned total = __shfl(pre, 63, 64);
+      unsigned long long base = 0;
+      if (lane == 0 && total) base = atomicAdd(fix_count + seg, (unsigned long long)total);
+      base = __shfl(base, 0, 64) + (pre - cnt);
+      while (mlo | mhi) {
+        const int g = mlo ? __ffs(mlo) - 1 : 32 + __ffs(mhi) - 1;
+        if (g < 32) mlo &= mlo - 1u;
+        else mhi &= mhi - 1u;
+        const int bj = g & 1, e = (g >> 1) & 3, q = (g >> 3) & 3, bi = g >> 5;
+        const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * q + 4 * h + e;
+        const int64_t gj = col0 + wn * 64 + bj * 32 + l32;
+        if (base < (unsigned long long)seg_cap)
+          fix_list[(int64_t)seg * seg_cap + (int64_t)base] = make_int2((int)gi, (int)gj);
+        ++base;
+      }
+    }
+
+    // stores of tile (I, J) straight from the MFMA layout (see gemm_kappa_kernel)
+    {
+      char* const Kc = (char*)(Kr + col0);
+      const bool full = row0 + kTile <= n && col0 + kTile <= n;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int iu = bi * 32 + 8 * (r >> 2) + (r & 3);
+          char* const rowp = Kc + (size_t)iu * (size_t)S * 4u;
+          const float v0 = acc[bi][0][r], v1 = acc[bi][1][r];
+          if (full) {
+            __builtin_nontemporal_store(v0, (float*)(rowp + lane_b));
+            __builtin_nontemporal_store(v1, (float*)(rowp + lane_b + 128u));
+            continue;
+          }
+          if (row0 + wm * 64 + 4 * h + iu >= n) continue;
+          const int64_t j0 = col0 + wn * 64 + l32, j1 = j0 + 32;
+          if (j0 < ld) __builtin_nontemporal_store(j0 < n ? v0 : 0.f, (float*)(rowp + lane_b));
+          if (j1 < ld) __builtin_nontemporal_store(j1 < n ? v1 : 0.f, (float*)(rowp + lane_b + 128u));
+        }
+    }
+    if (J != I && !packed) {  // tile (J, I) of full storage: rows j, columns i
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) {
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) Tw[l32 * 65 + bi * 32 + 8 * (r >> 2) + 4 * h + (r & 3)] = acc[bi][bj][r];
+        // the wavefront's own LDS tile: its writes complete before its reads
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const int64_t gj = row0 + wm * 64 + lane;  // I < J, so gj < n
+        const int64_t gi0 = col0 + wn * 64 + bj * 32;
+        const int nrows = (int)min<int64_t>(32, n - gi0);
+        float* dst = K + gi0 * ld + gj;
+        if (nrows >= 32) {
+#pragma unroll
+          for (int rr = 0; rr < 32; ++rr) __builtin_nontemporal_store(Tw[rr * 65 + lane], dst + rr * ld);
+        } else {
+          for (int rr = 0; rr < nrows; ++rr) __builtin_nontemporal_store(Tw[rr * 65 + lane], dst + rr * ld);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    }
+  }
+}
+
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
                              int64_t n, int d_pad, int64_t ld, bool packed, bool f16, const float* kw,
                              const KappaParams& kp, void* K, float* diagK, int2* fix_list,
-                             unsigned long long* fix_count, long long seg_cap, hipStream_t s) {
+                             unsigned long long* fix_count, long long seg_cap, const float* bmax, hipStream_t s) {
   if (ld >= kMaxKStride) return hipErrorInvalidValue;
   const int64_t nt = (n + kTile - 1) / kTile;
+  if (!f16 && d_pad <= kRegMaxDpad) {
+    if (d_pad % 8 || (kp.kind == GAUSS && !bmax)) return hipErrorInvalidValue;
+    const int ns = build_sweep_segments(n);
+    int64_t items = 0;
+    for (int q = 0; q < ns; ++q) items += sweep_seg_begin(q + 1, (int)nt, ns);
+    const dim3 sgrid((unsigned)items), sblock(256);
+#define KKM_SWEEP(KIND, HP)                                                                             \
+  hipLaunchKernelGGL((gemm_kappa_sweep_kernel<KIND, HP>), sgrid, sblock, 0, s, Xp, nrm, maxnrm_bits, n, ld, \
+                     packed, (int)nt, ns, kp, (float*)K, diagK, fix_list, fix_count, seg_cap, bmax)
+#define KKM_SWEEP_HP(KIND)                     \
+  switch (d_pad / 2) {                         \
+    case 4: KKM_SWEEP(KIND, 4); break;         \
+    case 8: KKM_SWEEP(KIND, 8); break;         \
+    case 12: KKM_SWEEP(KIND, 12); break;       \
+    case 16: KKM_SWEEP(KIND, 16); break;       \
+    case 20: KKM_SWEEP(KIND, 20); break;       \
+    case 24: KKM_SWEEP(KIND, 24); break;       \
+    case 28: KKM_SWEEP(KIND, 28); break;       \
+    default: KKM_SWEEP(KIND, 32); break;       \
+  }
+    switch (kp.kind) {
+      case LINEAR: KKM_SWEEP_HP(LINEAR); break;
+      case POLY: KKM_SWEEP_HP(POLY); break;
+      default: KKM_SWEEP_HP(GAUSS); break;
+    }
+#undef KKM_SWEEP_HP
+#undef KKM_SWEEP
+    return hipGetLastError();
+  }
   const int64_t T = nt * (nt + 1) / 2;
   dim3 grid((unsigned)T), block(256);
 #define KKM_GEMM_LAUNCH(KIND, TY)                                                                        \

@@ -86,8 +86,9 @@ Sizes sizes_for(int64_t n, int32_t d, int mode) {
   return s;
 }
 
+// staged points, their norms, diag K, and the largest norm of each 128-point block
 size_t staged_bytes(const Sizes& s) {
-  return (size_t)s.n_pad * s.d_pad * 4 + (size_t)s.n_pad * 4 + (size_t)s.n * 4 + 64;
+  return (size_t)s.n_pad * s.d_pad * 4 + (size_t)s.n_pad * 4 + (size_t)s.n * 4 + (size_t)(s.n_pad / kTile) * 4 + 64;
 }
 // bytes of one stored entry of K
 size_t k_elem(int storage) { return storage == KKM_STORE_F16 ? 2 : 4; }
@@ -164,6 +165,7 @@ struct kkm_ctx {
   kkm_params params{};
   KappaParams kp{};
   float *Xp = nullptr, *nrm = nullptr, *diagK = nullptr;
+  float* bmax = nullptr;      // largest squared norm of each 128-point block of the staged points
   void* K = nullptr;          // fp32 or binary16 entries (storage)
   int storage = KKM_STORE_F32;
   float* kw = nullptr;        // binary16 row scales (linear, polynomial), else null
@@ -320,7 +322,7 @@ void free_build(kkm_ctx* c) {
   free_hist(c);
   free_seed(c);
   release(c, c->build_allocs);
-  c->Xp = c->nrm = c->diagK = nullptr;
+  c->Xp = c->nrm = c->diagK = c->bmax = nullptr;
   c->K = nullptr;
   c->kw = nullptr;
   c->trK = nullptr;
@@ -781,6 +783,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
     c->Xp = (float*)p;
     c->nrm = c->Xp + (size_t)s.n_pad * s.d_pad;
     c->diagK = c->nrm + s.n_pad;
+    c->bmax = c->diagK + s.n;
     if ((rc = dalloc(c, &p, 64, c->build_allocs, "trace"))) return rc;
     c->trK = (double*)p;
     c->maxnrm = (unsigned*)((char*)p + 8);
@@ -829,6 +832,9 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
         return launch_row_scales(c->nrm, c->maxnrm, n, kp, c->kw, c->stream);
       })))
     return rc;
+  if (!panel && kind == KKM_GAUSS &&
+      (rc = run(c, KKM_PHASE_STAGE, "blockmax", [&] { return launch_blockmax(c->nrm, s.n_pad / kTile, c->bmax, c->stream); })))
+    return rc;
   if ((rc = run(c, KKM_PHASE_GEMM, "gemm_kappa", [&] {
          if (panel)
            return launch_gemm_kappa_panel(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, pr0, pr1, pc0, pc1, s.ld, kp,
@@ -836,7 +842,7 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
                                           c->fix_cap / kFixSegs, c->stream);
          return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16,
                                   c->kw, kp, c->K, c->diagK, c->fix_list, c->fix_count,
-                                  c->fix_cap / kFixSegs, c->stream);
+                                  c->fix_cap / kFixSegs, c->bmax, c->stream);
        })))
     return rc;
   if (kind == KKM_GAUSS &&

@@ -129,10 +129,15 @@ hipError_t launch_row_scales(const float* nrm, const unsigned* maxnrm_bits, int6
                              float* kw, hipStream_t s);
 // packed: store only tiles I <= J, at packed_row(i) + j (no mirror).
 // f16: K is binary16, entry (i, j) stored as K(i,j) / kw[i] (kw null: 1).
+// bmax[P] = the largest squared norm among points 128P .. 128P+127 of nrm
+// (n_pad entries, zero past n), one per 128-point block
+hipError_t launch_blockmax(const float* nrm, int64_t nblocks, float* bmax, hipStream_t s);
+// bmax: the block maxima of nrm (launch_blockmax), read by the small-width
+// sweep for the Gaussian kernel (may be null otherwise)
 hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* maxnrm_bits,
                              int64_t n, int d_pad, int64_t ld, bool packed, bool f16, const float* kw,
                              const KappaParams& kp, void* K, float* diagK, int2* fix_list,
-                             unsigned long long* fix_count, long long seg_cap, hipStream_t s);
+                             unsigned long long* fix_count, long long seg_cap, const float* bmax, hipStream_t s);
 // Recomputes the listed Gaussian entries (counts read on the device); if a
 // segment received more entries than it holds, re-tests the whole triangle.
 // fix_list holds kFixSegs segments of seg_cap entries; fix_count kFixSegs counters.

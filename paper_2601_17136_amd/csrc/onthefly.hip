@@ -359,59 +359,6 @@ __global__ __launch_bounds__(256, 2) void onthefly_kernel(
 // wavefronts never wait for each other inside the sweep; two workgroups per
 // CU give every SIMD two independent wavefronts, one streaming products while
 // the other runs its epilogue.
-constexpr int kRegMaxDpad = 64;
-
-template <int HP>
-__device__ inline void load_operand(const float* __restrict__ Y, int64_t row, int d_pad, int h, float (&v)[HP]) {
-  const float4* p = (const float4*)(Y + row * d_pad + h * HP);
-#pragma unroll
-  for (int u = 0; u < HP / 4; ++u) {
-    const float4 t = p[u];
-    v[4 * u] = t.x;
-    v[4 * u + 1] = t.y;
-    v[4 * u + 2] = t.z;
-    v[4 * u + 3] = t.w;
-  }
-}
-
-// acc[bi][bj] for one bj: the wavefront's 64 rows from As (stride 2 HP + 4
-// floats, an odd number of 16-byte units, so the 16-byte reads of 32
-// consecutive rows are conflict-free) against its 32 columns bj in b.  The
-// two column blocks run as two passes, so the second block's loads are still
-// in flight while the first block's products run.
-template <int HP>
-__device__ inline void mma_rows_lds(const float* __restrict__ As, const float (&b)[HP], floatx16& acc0,
-                                    floatx16& acc1, int l32, int h) {
-  constexpr int ldsA = 2 * HP + 4;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    acc0[r] = 0.f;
-    acc1[r] = 0.f;
-  }
-  const float* p0 = As + l32 * ldsA + h * HP;
-  const float* p1 = p0 + 32 * ldsA;
-  // rows of the next four steps read one group ahead; the scheduling
-  // barriers keep the reads from being hoisted further (registers)
-  float4 a0 = *(const float4*)p0, a1 = *(const float4*)p1;
-#pragma unroll
-  for (int s4 = 0; s4 < HP; s4 += 4) {
-    float4 n0 = a0, n1 = a1;
-    if (s4 + 4 < HP) {
-      n0 = *(const float4*)(p0 + s4 + 4);
-      n1 = *(const float4*)(p1 + s4 + 4);
-    }
-    const float av0[4] = {a0.x, a0.y, a0.z, a0.w}, av1[4] = {a1.x, a1.y, a1.z, a1.w};
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av0[u], b[s4 + u], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av1[u], b[s4 + u], acc1, 0, 0, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    a0 = n0;
-    a1 = n1;
-  }
-}
-
 // kappa on the wavefront's 64 x 64 block of an interior tile (off the
 // diagonal, all rows and columns below n), as kappa_tile, laid out for the
 // sweep's instruction budget: the Gaussian on norms scaled once and the
@@ -656,6 +603,11 @@ __global__ __launch_bounds__(256, 2) void onthefly_reg_kernel(
 }
 
 int onthefly_halves(int d_pad) { return d_pad <= kRegMaxDpad ? 2 : 1; }
+
+hipError_t launch_blockmax(const float* nrm, int64_t nblocks, float* bmax, hipStream_t s) {
+  hipLaunchKernelGGL(blockmax_kernel, dim3((unsigned)nblocks), dim3(kTile), 0, s, nrm, bmax);
+  return hipGetLastError();
+}
 
 // Workgroup (stripe, j): E^T_sorted(j, q) for the stripe's sorted rows q:
 //   the row-side partials of the segments that block Q = q/128 swept over

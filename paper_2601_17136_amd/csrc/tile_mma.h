@@ -122,6 +122,65 @@ __device__ inline void mma_tile(const float* __restrict__ Xa, const float* __res
   }
 }
 
+// ---- Small widths (d_pad <= kRegMaxDpad): the sweep kernels' product.
+// A workgroup stages its block's 128 rows in LDS once (stride 2 HP + 4
+// floats); each wavefront (wm, wn) loads its 64 columns of the current tile
+// into registers: lane (l, h) holds column l of each 32-column block at
+// k = h*HP .. h*HP + HP - 1 (HP = d_pad / 2), and step s of
+// v_mfma_f32_32x32x2_f32 pairs k = s with k = HP + s.
+constexpr int kRegMaxDpad = 64;
+
+template <int HP>
+__device__ inline void load_operand(const float* __restrict__ Y, int64_t row, int d_pad, int h, float (&v)[HP]) {
+  const float4* p = (const float4*)(Y + row * d_pad + h * HP);
+#pragma unroll
+  for (int u = 0; u < HP / 4; ++u) {
+    const float4 t = p[u];
+    v[4 * u] = t.x;
+    v[4 * u + 1] = t.y;
+    v[4 * u + 2] = t.z;
+    v[4 * u + 3] = t.w;
+  }
+}
+
+// acc[bi][bj] for one bj: the wavefront's 64 rows from As (stride 2 HP + 4
+// floats, an odd number of 16-byte units, so the 16-byte reads of 32
+// consecutive rows are conflict-free) against its 32 columns bj in b.  The
+// two column blocks run as two passes, so the second block's loads are still
+// in flight while the first block's products run.
+template <int HP>
+__device__ inline void mma_rows_lds(const float* __restrict__ As, const float (&b)[HP], floatx16& acc0,
+                                    floatx16& acc1, int l32, int h) {
+  constexpr int ldsA = 2 * HP + 4;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    acc0[r] = 0.f;
+    acc1[r] = 0.f;
+  }
+  const float* p0 = As + l32 * ldsA + h * HP;
+  const float* p1 = p0 + 32 * ldsA;
+  // rows of the next four steps read one group ahead; the scheduling
+  // barriers keep the reads from being hoisted further (registers)
+  float4 a0 = *(const float4*)p0, a1 = *(const float4*)p1;
+#pragma unroll
+  for (int s4 = 0; s4 < HP; s4 += 4) {
+    float4 n0 = a0, n1 = a1;
+    if (s4 + 4 < HP) {
+      n0 = *(const float4*)(p0 + s4 + 4);
+      n1 = *(const float4*)(p1 + s4 + 4);
+    }
+    const float av0[4] = {a0.x, a0.y, a0.z, a0.w}, av1[4] = {a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av0[u], b[s4 + u], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av1[u], b[s4 + u], acc1, 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    a0 = n0;
+    a1 = n1;
+  }
+}
+
 // kappa(x, y) from b = x.y (and the squared norms nx, ny for the Gaussian):
 //   LINEAR b;  POLY (gamma b + c)^degree;  GAUSS exp(-gamma (nx + ny - 2b)).
 template <int KIND>

@@ -99,7 +99,9 @@ def test_f16_step(oracle, name, mode):
     with Engine(X, kind, g, c, p, mode=mode) as eng32:
         diag32 = eng32.diag()
     assert info["storage"] == 1
-    np.testing.assert_array_equal(diag16, diag32)
+    # diag K stays fp32 in both formats; the two builds may sum x.x in another
+    # order (the small-width fp32 build runs a different product loop)
+    np.testing.assert_allclose(diag16, diag32, rtol=1e-5, atol=1e-6 * float(np.abs(diag32).max()))
     Kref = kern.matrix(X)
     w = row_scales(X, kind, g, c, p)
     rows = np.arange(n)

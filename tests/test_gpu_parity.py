@@ -32,6 +32,8 @@ CASES = {
     "linear-n300": (lambda: datagen.separated_blobs(300, 3, 4, seed=4, spread=3.0, sigma=1.0)[0],
                     4, "linear", 1.0, 0.0, 1, 13),
     "rings-n3000-gauss": (lambda: datagen.make_points(4, n=3000)[0], 64, "gauss", 0.5, 0.0, 1, 14),
+    # the same rings at a small width (the sweep build and sweep update), fix-up entries listed
+    "rings-n3000-d24-gauss": (lambda: datagen.make_points(4, n=3000, d=24)[0], 64, "gauss", 0.5, 0.0, 1, 24),
     "n129-d1": (lambda: datagen.separated_blobs(129, 1, 3, seed=5)[0], 3, "poly", 0.25, 2.0, 2, 15),
     "n128-d16": (lambda: datagen.make_points(5, n=128, d=16)[0], 7, "gauss", 1.0 / 16, 0.0, 1, 16),
     "n2-k2": (lambda: np.array([[0.0, 1.0], [2.0, -1.0]], np.float32), 2, "poly", 1.0, 1.0, 2, 17),
@@ -308,8 +310,9 @@ def test_bitwise_reproducible(oracle, mode):
     assert np.array_equal(i1[0], i2[0]) and np.array_equal(i1[2], i2[2])
 
 
+@pytest.mark.parametrize("d", [128, 24])
 @pytest.mark.parametrize("mode", ["resident", "packed"])
-def test_gauss_fixup_overflow_path(oracle, mode):
+def test_gauss_fixup_overflow_path(oracle, mode, d):
     """With a memory budget that leaves room for only a few ten thousand fix-up
     list entries, more entries qualify than the list holds and the fix-up
     re-tests the whole triangle; K must still match the oracle.  The points
@@ -318,7 +321,7 @@ def test_gauss_fixup_overflow_path(oracle, mode):
     entry with a non-negligible value is listed."""
     _torch_cuda()
     from paper_2601_17136_amd import kkm
-    X = datagen.make_points(4, n=3000)[0] + np.float32(30.0)
+    X = datagen.make_points(4, n=3000, d=d)[0] + np.float32(30.0)
     _, need = kkm.kkm_plan(3000, X.shape[1], 1, 1 << 40, kkm.MODES[mode])
     with Engine(X, "gauss", 0.5, mode=mode, mem_budget=need + 4096) as eng:
         K = eng.K_rows()
