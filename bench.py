@@ -31,18 +31,28 @@ METRIC = "clustering iters/sec + K-build TFLOP/s, % of HBM / MFMA peak, 1 GPU"
 # HBM bytes per launch from two rocprofv3 counter runs (FETCH_SIZE, then
 # WRITE_SIZE; KiB per dispatch) on a workload, scaled by what the same
 # counters read for a plain 1 GiB device copy (fetch x1.9999, write x1.0).
-# Reported only while the kernel's sources still hash to what was counted.
+# Reported only while the kernel's sources still hash to what was counted
+# (the counter summaries are profiles/pmc_traffic_*).
 FETCH_SCALE, WRITE_SCALE = 1.9999, 1.0
 TRAFFIC = {
+    # workload 2 (n=20000, d=784)
     ("spmm_sym", 2, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 397405.5, 21345.2),
     ("spmm_sym", 2, "packed-f16"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 198963.7, 21344.9),
-    ("gemm_kappa", 2, "packed"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                  ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2521025.0, 793823.0),
-    ("gemm_kappa", 2, "packed-f16"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                      ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2504742.1, 396951.0),
     ("spmm_onehot", 2, "resident"): (("csrc/cluster_ops.hip",), ("ffc98cf809a2ba97",), 782834.6, 1578.0),
-    ("gemm_kappa", 2, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
-                                    ("1c04cbe5dc19deb6", "21ea801568c098f4"), 2506375.9, 1565078.8),
+    # workload 3 (n=60000, d=780)
+    ("spmm_sym", 3, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 3528453.121, 93746.717),
+    ("spmm_onehot", 3, "resident"): (("csrc/cluster_ops.hip",), ("ffc98cf809a2ba97",), 7035962.829, 14074.69),
+    ("gemm_kappa", 3, "packed"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
+                                  ("660210cbc993ebea", "366f902efcd9e5e8"), 22315518.0, 7053978.625),
+    ("gemm_kappa", 3, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
+                                    ("660210cbc993ebea", "366f902efcd9e5e8"), 22349755.062, 14070234.5),
+    # workload 5 (n=200000, d=54)
+    ("spmm_sym", 5, "packed"): (("csrc/spmm_sym.hip",), ("7d08b0ed34741ecd",), 39122976.645, 886700.217),
+    ("spmm_onehot", 5, "resident"): (("csrc/cluster_ops.hip",), ("ffc98cf809a2ba97",), 78128224.638, 153234.375),
+    ("gemm_kappa", 5, "packed"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
+                                  ("660210cbc993ebea", "366f902efcd9e5e8"), 2961565.0, 78291487.594),
+    ("gemm_kappa", 5, "resident"): (("csrc/gemm_kappa.hip", "csrc/tile_mma.h"),
+                                    ("660210cbc993ebea", "366f902efcd9e5e8"), 3548282.812, 156316685.938),
 }
 
 
