@@ -34,6 +34,12 @@ CASES = {
     "rings-n3000-gauss": (lambda: datagen.make_points(4, n=3000)[0], 64, "gauss", 0.5, 0.0, 1, 14),
     # the same rings at a small width (the sweep build and sweep update), fix-up entries listed
     "rings-n3000-d24-gauss": (lambda: datagen.make_points(4, n=3000, d=24)[0], 64, "gauss", 0.5, 0.0, 1, 24),
+    # widths above 64: the sweep build's contraction in two chunks (second chunk
+    # of half-width 32, 20 and 4), ragged row tails
+    "rings-n2000-d120-gauss": (lambda: datagen.make_points(4, n=2000, d=120)[0], 16, "gauss", 0.5, 0.0, 1, 25),
+    "d100-n1300-poly": (lambda: datagen.make_points(2, n=1300, d=100)[0], 6, "poly", 0.01, 1.0, 2, 26),
+    "d72-n700-linear": (lambda: datagen.separated_blobs(700, 72, 5, seed=7, spread=2.0, sigma=1.0)[0],
+                        5, "linear", 1.0, 0.0, 1, 27),
     "n129-d1": (lambda: datagen.separated_blobs(129, 1, 3, seed=5)[0], 3, "poly", 0.25, 2.0, 2, 15),
     "n128-d16": (lambda: datagen.make_points(5, n=128, d=16)[0], 7, "gauss", 1.0 / 16, 0.0, 1, 16),
     "n2-k2": (lambda: np.array([[0.0, 1.0], [2.0, -1.0]], np.float32), 2, "poly", 1.0, 1.0, 2, 17),
