@@ -123,6 +123,7 @@ size_t ws_bytes(const Sizes& s, int k, int mode) {
   }
   if (mode == KKM_MODE_PACKED) {
     b += (size_t)nseg_for(s, k) * k * qmax * chunk_len_for(s, mode) * 4;  // Ecp: column-side partials
+    b += (size_t)k * s.n * 4;                // Ecol
     b += (size_t)qmax * 4;                   // chunk start columns
     b += (size_t)qmax * chunk_len_for(s, mode) * 4;  // chunk-major member table
     b += (size_t)(s.n_pad / kTile) * ((k + 15) / 16) * 64 * 4;  // one-hot bits per column tile
@@ -381,6 +382,7 @@ int carve_from(kkm_ctx* c, int k, void* base) {
     b.bseg = sym_seg_for(s.n, k);
     b.nseg = nseg_for(s, k);
     b.Ecp = (float*)take((size_t)b.nseg * k * qmax * b.chunk_len * 4);
+    b.Ecol = (float*)take((size_t)k * s.n * 4);
     b.chunk_c0 = (int*)take((size_t)qmax * 4);
     b.nlb = (k + 15) / 16;
     b.crow = (int*)take((size_t)qmax * b.chunk_len * 4);
@@ -534,6 +536,8 @@ int one_update(kkm_ctx* c, int t, const int* cur, int* nxt, float* z_out, float*
       return rc;
   } else if (c->mode == KKM_MODE_PACKED) {
     if ((rc = run(c, KKM_PHASE_SPMM, "spmm_sym", [&] { return launch_spmm_sym(c->K, b, c->stream); })))
+      return rc;
+    if ((rc = run(c, KKM_PHASE_REDUCE, "ecol_sum", [&] { return launch_ecol_sum(b, c->stream); })))
       return rc;
     if ((rc = run(c, KKM_PHASE_REDUCE, "spmm_reduce_sym", [&] { return launch_spmm_reduce_sym(b, cur, c->stream); })))
       return rc;

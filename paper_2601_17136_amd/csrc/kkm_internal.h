@@ -101,6 +101,7 @@ struct IterBufs {
   int nt, nseg, bseg;   // column tiles (ld / kTile); column segments of bseg tiles
   float* Ecp;           // nseg x k x (qmax * chunk_len): column-side partials per segment,
                         // at chunk-major positions (member t of chunk q at q * chunk_len + t)
+  float* Ecol;          // k x n: column-side sums, by point index
   int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
                         // start), written by the scatter; null when K is not packed
   int* crow;            // qmax x chunk_len: point index of member t of chunk q at
@@ -203,9 +204,10 @@ hipError_t launch_spmm_reduce(const IterBufs& b, const int* cl, hipStream_t s);
 // packed K (upper block triangle)
 // needs the scatter's crow and mskg for the current ids
 hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s);
+hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s);
 // E^T from the chunk partials (each starting at its chunk's first stored
-// column) plus each point's column-side partials over the segments (found
-// from the scatter's sorted positions); zpart per kSymRedStripe columns.
+// column) plus the column-side sums Ecol (by point index); zpart per
+// kSymRedStripe columns.
 hipError_t launch_spmm_reduce_sym(const IterBufs& b, const int* cl, hipStream_t s);
 hipError_t launch_packed_rows(const void* Kp, bool f16, const float* kw, int64_t n, int64_t ld, int64_t r0,
                               int64_t r1, float* out, hipStream_t s);

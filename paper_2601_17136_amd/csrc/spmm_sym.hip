@@ -29,9 +29,9 @@
 // order and each column tile's one-hot bits, so a workgroup's prologue is a
 // single round trip of independent loads.  The column-side sums of a row stay
 // in the accumulators for the whole segment and go to Ecp[sg] at the row's
-// chunk-major position; spmm_reduce_sym_kernel adds the segments of each
-// point and the chunks' row-side partials into E^T.  Fixed orders
-// throughout, so the result is bitwise reproducible.
+// chunk-major position; ecol_sum_kernel adds the segments into Ecol at each
+// row's point index, and spmm_reduce_sym_kernel adds them into E^T.  Fixed
+// orders throughout, so the result is bitwise reproducible.
 #include "kkm_internal.h"
 
 #include <algorithm>
@@ -295,14 +295,38 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       }
 }
 
-// Workgroup (stripe of kSymRedStripe columns, cluster j).  First, each
-// thread adds the column-side sums of one point of the stripe (member u of
-// chunk q, found from its sorted position) over the segments that hold its
-// row's stored columns, in segment order.  Then cluster j's many short
-// chunks are split into four fixed quarters, one per wavefront, each summed
-// in chunk order (a chunk's partial starts at its first stored column), and
-// the quarters are added in order, with the column-side sums, into E^T and
-// the stripe's part of sum_{i in L_j} E(i, j).
+// Ecol[j][i] = the column-side sums of point i (member u of chunk q) over
+// the segments that hold its row's stored columns, in order.  One output per
+// thread: (chunk, label, member) over ecol_wgs(b) workgroups per chunk.
+__device__ __host__ inline int ecol_wgs(const IterBufs& b) { return (b.k * b.chunk_len + 255) / 256; }
+__global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
+  const int per = ecol_wgs(b), cl = b.chunk_len;
+  const int q = (int)(blockIdx.x / (unsigned)per), part = (int)(blockIdx.x % (unsigned)per);
+  const int t = part * 256 + (int)threadIdx.x;
+  const int j = t / cl, u = t % cl;
+  const int* cr = b.crow + (int64_t)q * cl;
+  const int i0 = cr[0], row = cr[u];
+  if (i0 < 0 || j >= b.k || row < 0) return;
+  const int s0 = i0 / kTile / b.bseg, last = b.nseg - 1;
+  const int64_t ecs = (int64_t)b.qmax * cl, seg_stride = (int64_t)b.k * ecs;
+  const float* e = b.Ecp + (int64_t)j * ecs + (int64_t)q * cl + u;
+  float acc = 0.f;
+  for (int sg = s0; sg <= last; sg += 8) {  // eight loads in flight, added in order
+    float v[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) v[x] = e[min(sg + x, last) * seg_stride];
+#pragma unroll
+    for (int x = 0; x < 8; ++x)
+      if (sg + x <= last) acc += v[x];
+  }
+  b.Ecol[(int64_t)j * b.n + row] = acc;
+}
+
+// Workgroup (stripe of kSymRedStripe columns, cluster j).  Cluster j's many
+// short chunks are split into four fixed quarters, one per wavefront, each
+// summed in chunk order (a chunk's partial starts at its first stored
+// column), and the quarters are added in order.  Then the column-side sums
+// of the stripe's rows, and the stripe's part of sum_{i in L_j} E(i, j).
 __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const int* __restrict__ cl) {
   const int ns = b.nzpart;
   const int stripe = (int)(blockIdx.x % (unsigned)ns), j = (int)(blockIdx.x / (unsigned)ns);
@@ -310,34 +334,19 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
   if (qa == qb) return;  // empty cluster: E^T(j, .) and z_j are never read
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   __shared__ f4 part[4][64];
-  __shared__ float ecl[kSymRedStripe];
   const int64_t ld = b.ld, n = b.n;
   const int64_t col = (int64_t)stripe * kSymRedStripe + 4 * lane;
-  {
-    const int64_t x = (int64_t)stripe * kSymRedStripe + tid;
-    const int cx = x < n ? cl[x] : -1;
-    float acc = 0.f;
-    if ((unsigned)cx < (unsigned)b.k) {  // ids out of range are reported by the scatter
-      const int len = b.chunk_len;
-      const int64_t u = (int64_t)b.qfirst[cx] * len + (b.pos[x] - b.off[cx]);  // chunk-major position
-      const int s0 = b.chunk_c0[u / len] / kTile / b.bseg, last = b.nseg - 1;
-      const int64_t ecs = (int64_t)b.qmax * len, seg_stride = (int64_t)b.k * ecs;
-      const float* e = b.Ecp + (int64_t)j * ecs + u;
-      for (int sg = s0; sg <= last; sg += 8) {  // eight loads in flight, added in order
-        float v[8];
-#pragma unroll
-        for (int y = 0; y < 8; ++y) v[y] = e[min(sg + y, last) * seg_stride];
-#pragma unroll
-        for (int y = 0; y < 8; ++y)
-          if (sg + y <= last) acc += v[y];
-      }
-    }
-    ecl[tid] = acc;
-  }
+  // the column-side sums and ids of the stripe's points, for wavefront 0's
+  // epilogue, are loaded before the chunk loop
+  float ec[4];
   int cc[4];
   if (w == 0) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) cc[c] = cl[min(col + c, n - 1)];
+    for (int c = 0; c < 4; ++c) {
+      const int64_t x = min(col + c, n - 1);
+      ec[c] = b.Ecol[(int64_t)j * n + x];
+      cc[c] = cl[x];
+    }
   }
   const int per = (qb - qa + 3) / 4;
   const int q0 = qa + w * per, q1 = min(qb, q0 + per);
@@ -367,7 +376,7 @@ __global__ __launch_bounds__(256) void spmm_reduce_sym_kernel(IterBufs b, const 
     e = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-      if (col + c < n) e[c] += ecl[4 * lane + c];
+      if (col + c < n) e[c] += ec[c];
     *(f4*)(b.Et + (int64_t)j * ld + col) = e;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -423,6 +432,11 @@ hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
     default: return hipErrorInvalidValue;  // k > kSymMaxK is rejected before launch
   }
 #undef KKM_SYM_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_ecol_sum(const IterBufs& b, hipStream_t s) {
+  hipLaunchKernelGGL(ecol_sum_kernel, dim3((unsigned)((int64_t)b.qmax * ecol_wgs(b))), dim3(256), 0, s, b);
   return hipGetLastError();
 }
 
