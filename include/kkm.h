@@ -177,7 +177,11 @@ const char *kkm_last_warning(const kkm_ctx *ctx);
 
 /* Pure host planning, no HIP call.  Picks the mode for a problem and the
  * device bytes it needs (K, staged points, per-iteration scratch for k
- * clusters).  requested_mode: kkm_mode; AUTO resolves by the budget and k
+ * clusters).  A context created with that many bytes builds and iterates:
+ * the Gaussian build's fix-up list takes up to a quarter of the room the
+ * budget leaves, and the first iteration that needs that room frees it
+ * (after one synchronisation to read its counts), so it is not counted
+ * here.  requested_mode: kkm_mode; AUTO resolves by the budget and k
  * as a build with k_hint = k does (see kkm_mode).
  * storage: kkm_storage of K (sizes K and the row scales).
  * Errors: KKM_ERR_ARG (bad sizes or storage, or PACKED with

@@ -236,9 +236,9 @@ int dalloc(kkm_ctx* c, void** p, size_t bytes, std::vector<Alloc>& owner, const 
     return fail(c, KKM_ERR_OOM, "%s needs %zu bytes; %zu of the %zu-byte budget already held", what,
                 bytes, c->held, c->budget);
   // Large buffers (K and its panels) are asked for as physically contiguous
-  // memory first: the streaming SpMM over such a buffer runs a few % faster and
-  // with less spread between allocations than over one of scattered pages.
-  // Ordinary device memory is the fallback.
+  // memory first: the streaming SpMM over K measured a few % faster on such
+  // memory than on memory from hipMalloc.  Ordinary device memory is the
+  // fallback.
   hipError_t e = hipErrorOutOfMemory;
   if (bytes >= kContiguousMinBytes) {
     e = hipExtMallocWithFlags(p, bytes, hipDeviceMallocContiguous);
@@ -462,6 +462,32 @@ void restore_ws(kkm_ctx* c, const SavedWs& v) {
 }
 
 // Allocate one block and carve it (keeps the accounting to one number).
+// Frees the Gaussian fix-up list of a finished build, after reading its
+// counts (the one synchronisation this adds): a budget sized by kkm_plan
+// (K, staged points, iteration scratch) has no room for both.
+int release_fix_list(kkm_ctx* c) {
+  if (!c->fix_list) return KKM_OK;
+  if (c->fixups < 0) {
+    unsigned long long cnt[kFixSegs] = {0};
+    HIP_TRY(c, hipMemcpyAsync(cnt, c->fix_count, sizeof cnt, hipMemcpyDeviceToHost, c->stream), "read fix-up counts");
+    HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");
+    int64_t tot = 0;
+    for (int q = 0; q < kFixSegs; ++q) tot += (int64_t)cnt[q];
+    c->fixups = tot;
+  }
+  std::vector<Alloc>& v = c->build_allocs;
+  for (size_t i = 0; i < v.size(); ++i)
+    if (v[i].p == (void*)c->fix_list) {
+      (void)hipFree(v[i].p);
+      c->held -= std::min(c->held, v[i].bytes);
+      v.erase(v.begin() + (ptrdiff_t)i);
+      break;
+    }
+  c->fix_list = nullptr;
+  c->fix_count = nullptr;
+  return KKM_OK;
+}
+
 int carve_ws(kkm_ctx* c, int k) {
   void* base = nullptr;
   int rc = dalloc(c, &base, ws_bytes(c->wsz, k, c->mode), c->ws_allocs, "iteration scratch");
@@ -472,6 +498,11 @@ int carve_ws(kkm_ctx* c, int k) {
 int ensure_ws(kkm_ctx* c, int k, int iters) {
   if (c->k_ws != k) {
     free_ws(c);
+    const size_t need = ws_bytes(c->wsz, k, c->mode) + (size_t)std::max(iters, 64) * 12 + 512;
+    if (c->held + need > c->budget) {
+      int rc = release_fix_list(c);
+      if (rc) return rc;
+    }
     int rc = carve_ws(c, k);
     if (rc) return rc;
   }
@@ -807,18 +838,22 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
       if ((rc = dalloc(c, &p, (size_t)n * 4, c->build_allocs, "row scales"))) return rc;
       c->kw = (float*)p;
     }
-    if (kind == KKM_GAUSS && stores_k) {
-      const long long upper = panel ? (long long)((pr1 - pr0) * (pc1 - pc0)) : (long long)(n * (n - 1) / 2);
-      long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
-      const size_t room = c->budget > c->held ? c->budget - c->held : 0;
-      cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
-      cap = std::max<long long>(cap / kFixSegs, 1) * kFixSegs;
-      if ((rc = dalloc(c, &p, (size_t)cap * sizeof(int2) + kFixSegs * 8, c->build_allocs, "fix-up list")))
-        return rc;
-      c->fix_list = (int2*)p;
-      c->fix_count = (unsigned long long*)((char*)p + (size_t)cap * sizeof(int2));
-      c->fix_cap = cap;
-    }
+  }
+  // The Gaussian fix-up list takes up to a quarter of the room the budget
+  // leaves.  It is needed only while building: the first iteration scratch
+  // that does not fit beside it releases it (release_fix_list), and a
+  // rebuild then makes it again here.
+  if (kind == KKM_GAUSS && (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) && !c->fix_list) {
+    const long long upper = panel ? (long long)((pr1 - pr0) * (pc1 - pc0)) : (long long)(n * (n - 1) / 2);
+    long long cap = std::min<long long>(upper, std::max<long long>(1LL << 20, 512LL * n));
+    const size_t room = c->budget > c->held ? c->budget - c->held : 0;
+    cap = std::min<long long>(cap, (long long)(room / 4 / sizeof(int2)));
+    cap = std::max<long long>(cap / kFixSegs, 1) * kFixSegs;
+    if ((rc = dalloc(c, &p, (size_t)cap * sizeof(int2) + kFixSegs * 8, c->build_allocs, "fix-up list")))
+      return rc;
+    c->fix_list = (int2*)p;
+    c->fix_count = (unsigned long long*)((char*)p + (size_t)cap * sizeof(int2));
+    c->fix_cap = cap;
   }
   if ((rc = run(c, KKM_PHASE_STAGE, "zero", [&] { return launch_zero_ints((int*)c->maxnrm, 1, c->stream); })))
     return rc;
