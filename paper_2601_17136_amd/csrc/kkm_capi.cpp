@@ -461,7 +461,6 @@ void restore_ws(kkm_ctx* c, const SavedWs& v) {
   c->obj = v.obj;
 }
 
-// Allocate one block and carve it (keeps the accounting to one number).
 // Frees the Gaussian fix-up list of a finished build, after reading its
 // counts (the one synchronisation this adds): a budget sized by kkm_plan
 // (K, staged points, iteration scratch) has no room for both.
@@ -488,6 +487,7 @@ int release_fix_list(kkm_ctx* c) {
   return KKM_OK;
 }
 
+// Allocate one block and carve it (keeps the accounting to one number).
 int carve_ws(kkm_ctx* c, int k) {
   void* base = nullptr;
   int rc = dalloc(c, &base, ws_bytes(c->wsz, k, c->mode), c->ws_allocs, "iteration scratch");
