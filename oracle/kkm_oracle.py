@@ -20,7 +20,7 @@ Naming.  The paper's point matrix P is ``X`` here.  Its assignment matrix V
     with it D is the true squared feature-space distance),
   * ``J(cl)   = sum_i D[i, cl(i)] = tr K - sum_j |L_j| z[j]``.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
   * an empty cluster j has D[:, j] = +inf (never chosen) and z[j] = 0;
   * the argmin takes the lowest index among equal minima, and is decided on D
     rounded to single precision, the precision the paper computes in
