@@ -31,13 +31,18 @@ constexpr int kBlk = 256;
 // chunk of at most 16 W sorted rows of one cluster (one 16-row MFMA group per
 // wavefront) and a segment of S column tiles.  Up to kSymSmallN points,
 // W = 4 and S = 8: small problems need many workgroups to fill the GPU
-// evenly.  Above, W = 8 and (for k <= 16) S = 16: taller chunks halve the
+// evenly; up to kSymTinyN points (with k <= 16) S = 2, since 8-tile segments
+// leave most CUs idle there (2000 points: 18.8 -> 11.4 us per SpMM).  Above
+// kSymSmallN, W = 8 and (for k <= 16) S = 16: taller chunks halve the
 // partial sums, and longer segments spread each workgroup's start (row
 // addresses far apart in a K of tens of GB) over more tiles.  kSymMaxK
 // bounds the one-hot MFMA label blocks (16 labels each) a wavefront carries.
-constexpr int64_t kSymSmallN = 40000;
+constexpr int64_t kSymSmallN = 40000, kSymTinyN = 4096;
 inline int sym_chunk_for(int64_t n) { return n <= kSymSmallN ? 64 : 128; }
-inline int sym_seg_for(int64_t n, int k) { return n > kSymSmallN && k <= 16 ? 16 : 8; }
+inline int sym_seg_for(int64_t n, int k) {
+  if (k <= 16) return n <= kSymTinyN ? 2 : n > kSymSmallN ? 16 : 8;
+  return 8;
+}
 constexpr int kSymMaxK = 64;
 constexpr int kSymRedStripe = 256;  // columns per workgroup of the packed reduction
 

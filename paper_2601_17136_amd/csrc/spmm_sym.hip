@@ -418,12 +418,13 @@ hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
                          (const float*)Kp, b);                                                           \
   } while (0)
   if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
-  if (b.bseg != 8 && !(b.bseg == 16 && nb == 1 && b.chunk_len == 128)) return hipErrorInvalidValue;
   const bool tall = b.chunk_len == 128;
+  if (b.bseg != 8 && !(nb == 1 && ((b.bseg == 16 && tall) || (b.bseg == 2 && !tall)))) return hipErrorInvalidValue;
   switch (nb) {
     case 1:
       if (b.bseg == 16) KKM_SYM_LAUNCH(1, 8, 16);
       else if (tall) KKM_SYM_LAUNCH(1, 8, 8);
+      else if (b.bseg == 2) KKM_SYM_LAUNCH(1, 4, 2);
       else KKM_SYM_LAUNCH(1, 4, 8);
       break;
     case 2: if (tall) KKM_SYM_LAUNCH(2, 8, 8); else KKM_SYM_LAUNCH(2, 4, 8); break;
