@@ -40,6 +40,11 @@ CASES = {
     "d100-n1300-poly": (lambda: datagen.make_points(2, n=1300, d=100)[0], 6, "poly", 0.01, 1.0, 2, 26),
     "d72-n700-linear": (lambda: datagen.separated_blobs(700, 72, 5, seed=7, spread=2.0, sigma=1.0)[0],
                         5, "linear", 1.0, 0.0, 1, 27),
+    # the packed SpMM's segment length changes at 4096 points (k <= 16): the last
+    # size with 2-tile segments (and the largest label count they take), and one
+    # just above it with a ragged tail
+    "n4096-k16-gauss": (lambda: datagen.make_points(2, n=4096, d=20)[0], 16, "gauss", 1.0 / 20, 0.0, 1, 28),
+    "n4500-k12-poly": (lambda: datagen.make_points(2, n=4500, d=20)[0], 12, "poly", 0.05, 1.0, 2, 29),
     "n129-d1": (lambda: datagen.separated_blobs(129, 1, 3, seed=5)[0], 3, "poly", 0.25, 2.0, 2, 15),
     "n128-d16": (lambda: datagen.make_points(5, n=128, d=16)[0], 7, "gauss", 1.0 / 16, 0.0, 1, 16),
     "n2-k2": (lambda: np.array([[0.0, 1.0], [2.0, -1.0]], np.float32), 2, "poly", 1.0, 1.0, 2, 17),
