@@ -335,9 +335,11 @@ def main():
 
     w = datagen.WORKLOADS[args.config]
     if args.mode is None:
-        # the packed SpMM's column side costs one MFMA per 16 labels per entry:
-        # below the HBM time for k <= 16, above it for larger k
-        args.mode = "packed" if w.k <= 16 else "resident"
+        # the mode the library's planner (AUTO) picks for this workload on one
+        # MI355X's memory (288 GB less 5%)
+        m, _ = kkm.kkm_plan(w.n, w.d, w.k, kkm.KINDS[w.kind], int(0.95 * (288 << 30)), kkm.KKM_MODE_AUTO,
+                            kkm.STORAGES[args.storage])
+        args.mode = {v: name for name, v in kkm.MODES.items()}[m]
     extra = [m for m in (args.extra.split(",") if args.extra is not None else
                          (["resident", "onthefly"] if args.config == 5 else []))
              if m and m != "none" and m != args.mode]

@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 6
+#define KKM_ABI_VERSION 7
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -67,10 +67,15 @@ typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
  * KKM_PACKED_MAX_K clusters; it is the fastest mode for small k.  ONTHEFLY
  * never stores K: every iteration recomputes its tiles and folds them
  * straight into E, which is the paper's single-GPU sliding-window baseline
- * (Section VI-D) done tile by tile.  AUTO picks by the memory budget and
- * the cluster count the caller announces in kkm_params.k_hint:
- *   k_hint in 1..KKM_PACKED_FAST_K: PACKED if it fits (measured fastest for
- *     k <= 16 on every workload of n >= 20000), else as below;
+ * (Section VI-D) done tile by tile.  AUTO picks by the memory budget, the
+ * kernel, the storage and the cluster count the caller announces in
+ * kkm_params.k_hint:
+ *   k_hint in 1..KKM_PACKED_MAX_K with F16 storage or the Gaussian kernel,
+ *   or in 1..KKM_PACKED_FAST_K otherwise: PACKED if it fits, else as below.
+ *     PACKED's per-label column side runs on the binary16 matrix cores for a
+ *     binary16 K and for the Gaussian's fp32 K (whose entries, all in [0, 1],
+ *     it takes as two binary16 parts), on the fp32 ones otherwise; measured
+ *     fastest in these ranges at n = 20000 .. 200000;
  *   otherwise: RESIDENT if it fits, else PACKED if it fits (and k_hint is 0
  *     or at most KKM_PACKED_MAX_K), else ONTHEFLY.
  * A kkm_iterate with more than KKM_PACKED_MAX_K clusters on a K that AUTO
@@ -82,7 +87,7 @@ typedef enum kkm_mode {
   KKM_MODE_PACKED = 3
 } kkm_mode;
 #define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
-#define KKM_PACKED_FAST_K 16 /* AUTO stores PACKED for a k_hint up to this */
+#define KKM_PACKED_FAST_K 32 /* AUTO stores an fp32 linear or polynomial K PACKED for a k_hint up to this */
 #define KKM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20) /* static scratch of kkm_iterate_noalloc, per GPU */
 
 /* Number format of a stored K (RESIDENT or PACKED; ONTHEFLY stores nothing
@@ -181,14 +186,15 @@ const char *kkm_last_warning(const kkm_ctx *ctx);
  * the Gaussian build's fix-up list takes up to a quarter of the room the
  * budget leaves, and the first iteration that needs that room frees it
  * (after one synchronisation to read its counts), so it is not counted
- * here.  requested_mode: kkm_mode; AUTO resolves by the budget and k
- * as a build with k_hint = k does (see kkm_mode).
+ * here.  kind: kkm_kind of the kernel to be built.  requested_mode:
+ * kkm_mode; AUTO resolves by the budget, kind, storage and k as a build
+ * with k_hint = k does (see kkm_mode).
  * storage: kkm_storage of K (sizes K and the row scales).
- * Errors: KKM_ERR_ARG (bad sizes or storage, or PACKED with
+ * Errors: KKM_ERR_ARG (bad sizes, kind or storage, or PACKED with
  * k > KKM_PACKED_MAX_K), KKM_ERR_OOM (even the on-the-fly mode does not fit,
  * or the requested storing mode does not). */
-int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode, int32_t storage,
-             int32_t *mode_out, size_t *bytes_out);
+int kkm_plan(int64_t n, int32_t d, int32_t k, int32_t kind, size_t mem_budget, int32_t requested_mode,
+             int32_t storage, int32_t *mode_out, size_t *bytes_out);
 
 /* Host-only argument checks that the entry points apply first; exported so
  * they can be exercised without a GPU.  Return KKM_OK or KKM_ERR_ARG;

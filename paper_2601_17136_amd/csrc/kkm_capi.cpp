@@ -349,6 +349,12 @@ void free_build(kkm_ctx* c) {
   c->panel_e = false;
 }
 
+// The packed SpMM's column side may take each fp32 entry as two binary16
+// parts only where every entry lies in [0, 1]: the Gaussian kernel.
+bool split_column_side(const kkm_ctx* c) {
+  return c->mode == KKM_MODE_PACKED && c->storage == KKM_STORE_F32 && c->kind == KKM_GAUSS;
+}
+
 // Lay the per-update scratch for k clusters out over base (ws_bytes of it)
 // and clear what must start at zero.
 int carve_from(kkm_ctx* c, int k, void* base) {
@@ -376,6 +382,7 @@ int carve_from(kkm_ctx* c, int k, void* base) {
   b.ncol = c->pc1 > 0 ? c->pc1 - c->pc0 : s.n;
   b.trK = c->trK;
   b.kf16 = c->storage == KKM_STORE_F16;
+  b.ksplit = split_column_side(c);
   b.kw = c->kw;
   b.Et = (float*)take((size_t)k * s.ld * 4);
   if (c->mode == KKM_MODE_RESIDENT || c->mode == KKM_MODE_PACKED) {
@@ -521,6 +528,7 @@ int ensure_ws(kkm_ctx* c, int k, int iters) {
   b.trK = c->trK;
   b.kw = c->kw;
   b.kf16 = c->storage == KKM_STORE_F16;
+  b.ksplit = split_column_side(c);
   if (c->iter_ws < iters || !c->obj) {
     free_hist(c);
     int cap = std::max(iters, 64);
@@ -614,18 +622,26 @@ int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
 // The mode AUTO resolves to, and the device bytes of a mode.  k_known: k is
 // the cluster count the loop will run with; otherwise (a build without a
 // hint) k only sizes the scratch and the mode is picked without it.
-//   AUTO with k known: PACKED when k <= KKM_PACKED_FAST_K and it fits (it
+//   AUTO with k known: PACKED when k is at most packed_fast_k and it fits (it
 //   streams half the bytes per update, and its per-label column side stays
-//   below the HBM time up to 16 labels); else RESIDENT when it fits; else
-//   PACKED when k <= KKM_PACKED_MAX_K and it fits; else ONTHEFLY.
+//   below the HBM time up to that many labels); else RESIDENT when it fits;
+//   else PACKED when k <= KKM_PACKED_MAX_K and it fits; else ONTHEFLY.
 //   AUTO with k unknown: RESIDENT, else PACKED, else ONTHEFLY, whichever
 //   fits first.
 // ONTHEFLY is picked only when no stored K fits: at every width measured
 // (d >= 54) a stored K is at least as fast per update.
-int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, size_t mem_budget, int32_t requested_mode,
-              int32_t storage, int32_t* mode_out, size_t* bytes_out) {
+int packed_fast_k(int32_t kind, int32_t storage) {
+  // the column side on the binary16 matrix cores (binary16 K, or the fp32
+  // Gaussian split in two binary16 parts) stays fastest up to the packed
+  // storage's limit; on the fp32 ones up to KKM_PACKED_FAST_K labels
+  return storage == KKM_STORE_F16 || kind == KKM_GAUSS ? KKM_PACKED_MAX_K : KKM_PACKED_FAST_K;
+}
+int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, int32_t kind, size_t mem_budget,
+              int32_t requested_mode, int32_t storage, int32_t* mode_out, size_t* bytes_out) {
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
     return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
+  if (kind != KKM_LINEAR && kind != KKM_POLY && kind != KKM_GAUSS)
+    return fail(nullptr, KKM_ERR_ARG, "bad kind=%d", kind);
   if (requested_mode < KKM_MODE_AUTO || requested_mode > KKM_MODE_PACKED)
     return fail(nullptr, KKM_ERR_ARG, "bad mode=%d", requested_mode);
   if (requested_mode == KKM_MODE_PACKED && k_known && k > KKM_PACKED_MAX_K)
@@ -633,13 +649,13 @@ int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, size_t mem_budget, 
   if (storage != KKM_STORE_F32 && storage != KKM_STORE_F16) return fail(nullptr, KKM_ERR_ARG, "bad storage=%d", storage);
   auto need_for = [&](int m) {
     const Sizes s = sizes_for(n, d, m);
-    const size_t scales = row_scaled(m, storage, KKM_POLY) ? (size_t)n * 4 + 256 : 0;
+    const size_t scales = row_scaled(m, storage, kind) ? (size_t)n * 4 + 256 : 0;
     return staged_bytes(s) + ws_bytes(s, k, m) + 4096 + k_bytes(s, m, storage) + scales;
   };
   auto fits = [&](int m) { return need_for(m) <= mem_budget; };
   int mode = requested_mode;
   if (mode == KKM_MODE_AUTO) {
-    if (k_known && k <= KKM_PACKED_FAST_K && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
+    if (k_known && k <= packed_fast_k(kind, storage) && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
     else if (fits(KKM_MODE_RESIDENT)) mode = KKM_MODE_RESIDENT;
     else if ((!k_known || k <= KKM_PACKED_MAX_K) && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
     else mode = KKM_MODE_ONTHEFLY;
@@ -705,12 +721,12 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter) {
   return KKM_OK;
 }
 
-int kkm_plan(int64_t n, int32_t d, int32_t k, size_t mem_budget, int32_t requested_mode, int32_t storage,
-             int32_t* mode_out, size_t* bytes_out) {
+int kkm_plan(int64_t n, int32_t d, int32_t k, int32_t kind, size_t mem_budget, int32_t requested_mode,
+             int32_t storage, int32_t* mode_out, size_t* bytes_out) {
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
     return fail(nullptr, KKM_ERR_ARG, "bad sizes n=%lld d=%d", (long long)n, d);
   if (k < 1 || k > KKM_MAX_K || (int64_t)k > n) return fail(nullptr, KKM_ERR_ARG, "bad k=%d", k);
-  return plan_impl(n, d, k, true, mem_budget, requested_mode, storage, mode_out, bytes_out);
+  return plan_impl(n, d, k, true, kind, mem_budget, requested_mode, storage, mode_out, bytes_out);
 }
 
 int kkm_create(kkm_ctx** out, void* hip_stream, size_t mem_budget) {
@@ -775,8 +791,8 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
     for (const Alloc& a : c->hist_allocs) held_by_build += a.bytes;
     const size_t budget_left = c->budget - std::min(c->budget, c->held - std::min(c->held, held_by_build));
     const int32_t kh = std::min<int64_t>(params->k_hint, n);
-    if (plan_impl(n, d, kh > 0 ? kh : 1, kh > 0, budget_left, params->mode, params->storage, &mode, &need) !=
-        KKM_OK)
+    if (plan_impl(n, d, kh > 0 ? kh : 1, kh > 0, kind, budget_left, params->mode, params->storage, &mode,
+                  &need) != KKM_OK)
       return fail(c, KKM_ERR_OOM, "%s", g_noctx_err.c_str());
   }
   HIP_TRY(c, hipStreamSynchronize(c->stream), "synchronize");

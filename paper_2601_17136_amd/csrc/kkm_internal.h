@@ -29,19 +29,28 @@ constexpr int kBlk = 256;
 
 // Packed (upper block triangle) SpMM: a workgroup of W wavefronts takes a
 // chunk of at most 16 W sorted rows of one cluster (one 16-row MFMA group per
-// wavefront) and a segment of S column tiles.  Up to kSymSmallN points,
-// W = 4 and S = 8: small problems need many workgroups to fill the GPU
-// evenly; up to kSymTinyN points (with k <= 16) S = 2, since 8-tile segments
-// leave most CUs idle there (2000 points: 18.8 -> 11.4 us per SpMM).  Above
-// kSymSmallN, W = 8 and (for k <= 16) S = 16: taller chunks halve the
-// partial sums, and longer segments spread each workgroup's start (row
-// addresses far apart in a K of tens of GB) over more tiles.  kSymMaxK
-// bounds the one-hot MFMA label blocks (16 labels each) a wavefront carries.
+// wavefront) and a segment of S column tiles.  Up to kSymSmallN points W = 4,
+// above it W = 8 (taller chunks halve the partial sums).  S by problem size:
+//                          k <= 16   k > 16
+//   n <= kSymTinyN            2         8
+//   n <= kSymSmallN           8        16
+//   n >  kSymSmallN          16        32
+// Small problems need many workgroups to fill the GPU evenly (2000 points,
+// k = 8: 18.8 us per SpMM at S = 8, 11.4 at S = 2).  Longer segments spread
+// each workgroup's start (row addresses far apart in a K of tens of GB) over
+// more tiles, and each workgroup writes k column-side sums per row of its
+// chunk for its segment, which the next kernel reads back: with more labels
+// these partials and the epilogue weigh more against the tiles streamed
+// (200000 points, k = 64, binary16 column side: 17.0 ms per SpMM at S = 8,
+// 15.6 at 16, 13.6 at 32; 20000 points, k = 64: S = 16 beats 8 and 32).
+// kSymMaxK bounds the one-hot MFMA label blocks (16 labels each) a wavefront
+// carries.
 constexpr int64_t kSymSmallN = 40000, kSymTinyN = 4096;
 inline int sym_chunk_for(int64_t n) { return n <= kSymSmallN ? 64 : 128; }
 inline int sym_seg_for(int64_t n, int k) {
-  if (k <= 16) return n <= kSymTinyN ? 2 : n > kSymSmallN ? 16 : 8;
-  return 8;
+  if (n <= kSymTinyN) return k <= 16 ? 2 : 8;
+  if (n <= kSymSmallN) return k <= 16 ? 8 : 16;
+  return k <= 16 ? 16 : 32;
 }
 constexpr int kSymMaxK = 64;
 constexpr int kSymRedStripe = 256;  // columns per workgroup of the packed reduction
@@ -120,6 +129,9 @@ struct IterBufs {
   // stored K in binary16: entry (i, j) holds K(i,j) / kw[i] (kw null: 1)
   int kf16;
   const float* kw;
+  // fp32 K whose entries lie in [0, 1] (the Gaussian): the packed SpMM's
+  // column side may split each entry into two binary16 parts
+  int ksplit;
 };
 
 // binary16 storage of K

@@ -9,8 +9,16 @@
 // the row side is a plain column sum over the chunk, as in the full-storage
 // SpMM.  The column side needs, for every row, its entries summed per label
 // of their column: a product with the one-hot matrix of the column labels,
-// which runs on the fp32 matrix cores (v_mfma_f32_16x16x4_f32, 16 labels per
-// block, exact: every product is 0 or the entry itself).
+// which runs on the matrix cores with 16 labels per block, exact in its
+// products (each is 0 or the entry itself):
+//  - fp32 K in general: v_mfma_f32_16x16x4_f32, 4 columns per instruction;
+//  - binary16 K: v_mfma_f32_16x16x16_f16, 16 columns per instruction;
+//  - fp32 K with every entry in [0, 1] (the Gaussian): each entry as the sum
+//    of two binary16 values, hi = its rounding and lo = the rest rounded, on
+//    v_mfma_f32_16x16x16_f16: 16 columns per two instructions, and hi + lo
+//    within 2^-22 of the entry relative to it (2^-25 absolute below binary16's
+//    normal range; the row's own diagonal entry is 1), sums in fp32.  At
+//    k = 64 this takes the column side from above the HBM time to below it.
 //
 // Workgroup (chunk q, segment sg): NW wavefronts (4 or 8), one 16-row group
 // each, over the column tiles of segment sg (BSEG tiles) that the chunk's
@@ -51,10 +59,11 @@ namespace {
 // KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
 // binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
 // when a tile is consumed, so everything after the loads is the same.
-template <int NB, int NW, int BSEG, typename KT>
+template <int NB, int NW, int BSEG, typename KT, bool SPLIT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const KT* __restrict__ Kp, IterBufs b) {
   constexpr bool kHalf = sizeof(KT) == 2;
+  static_assert(!(SPLIT && kHalf), "the split column side is for fp32 K");
   using BufT = typename std::conditional<kHalf, h4, f4>::type;
   constexpr int R = 16 * NW, NT = 64 * NW;
   // With one label block the whole 16 x 128 block is staged at once; with
@@ -100,7 +109,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
   __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
-  __shared__ h4 onehot[kHalf ? 16 : 1];  // the 4 bits of a nibble as binary16 0 / 1
+  __shared__ h4 onehot[kHalf || SPLIT ? 16 : 1];  // the 4 bits of a nibble as binary16 0 / 1
 
   const int I0 = i0 / kTile;
   const int J_lo = max(Js, I0), J_hi = Je;
@@ -148,7 +157,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   BufT bb[8];
   if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
-  if (kHalf && tid < 16)
+  if ((kHalf || SPLIT) && tid < 16)
     onehot[tid] = h4{(_Float16)(tid & 1), (_Float16)((tid >> 1) & 1), (_Float16)((tid >> 2) & 1),
                      (_Float16)((tid >> 3) & 1)};
 #pragma unroll
@@ -196,13 +205,27 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
         const int g = g0 + gg;
         f4 v = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
         if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
+        if constexpr (SPLIT) {
+          // entries in [0, 1] as a sum of two binary16 values (hi, and the
+          // rest rounded: within 2^-22 relative); 16 columns per instruction
+          // and label block, exact 0/1 products, fp32 sums
+          const h4 hi = __builtin_convertvector(v, h4);
+          const h4 lo = __builtin_convertvector(v - __builtin_convertvector(hi, f4), h4);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
-            const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
+            const h4 a = onehot[(msk[nb] >> (4 * g)) & 15u];
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, hi, D[nb], 0, 0, 0);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, lo, D[nb], 0, 0, 0);
           }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
+              D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
+            }
+        }
       }
     };
     if constexpr (kHalf) {
@@ -411,27 +434,33 @@ hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
 #define KKM_SYM_LAUNCH(NB, NW, S)                                                                        \
   do {                                                                                                   \
     if (b.kf16)                                                                                          \
-      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, half_t>), dim3(grid), dim3(64 * NW), 0, s,            \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, half_t, false>), dim3(grid), dim3(64 * NW), 0, s,     \
                          (const half_t*)Kp, b);                                                          \
+    else if (b.ksplit)                                                                                   \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float, true>), dim3(grid), dim3(64 * NW), 0, s,       \
+                         (const float*)Kp, b);                                                           \
     else                                                                                                 \
-      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float>), dim3(grid), dim3(64 * NW), 0, s,             \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float, false>), dim3(grid), dim3(64 * NW), 0, s,      \
                          (const float*)Kp, b);                                                           \
   } while (0)
-  if (b.chunk_len != 64 && b.chunk_len != 128) return hipErrorInvalidValue;
+  // the segment lengths sym_seg_for sets
   const bool tall = b.chunk_len == 128;
-  if (b.bseg != 8 && !(nb == 1 && ((b.bseg == 16 && tall) || (b.bseg == 2 && !tall)))) return hipErrorInvalidValue;
+  const int lo = nb == 1 ? 2 : 8, hi = nb == 1 ? 8 : 16;  // short chunks: the two smaller lengths
+  if (tall ? b.bseg != 2 * hi : b.bseg != lo && b.bseg != hi) return hipErrorInvalidValue;
+#define KKM_SYM_CASE(NB, LO, HI)                          \
+  do {                                                    \
+    if (tall) KKM_SYM_LAUNCH(NB, 8, 2 * HI);              \
+    else if (b.bseg == LO) KKM_SYM_LAUNCH(NB, 4, LO);     \
+    else KKM_SYM_LAUNCH(NB, 4, HI);                       \
+  } while (0)
   switch (nb) {
-    case 1:
-      if (b.bseg == 16) KKM_SYM_LAUNCH(1, 8, 16);
-      else if (tall) KKM_SYM_LAUNCH(1, 8, 8);
-      else if (b.bseg == 2) KKM_SYM_LAUNCH(1, 4, 2);
-      else KKM_SYM_LAUNCH(1, 4, 8);
-      break;
-    case 2: if (tall) KKM_SYM_LAUNCH(2, 8, 8); else KKM_SYM_LAUNCH(2, 4, 8); break;
-    case 3: if (tall) KKM_SYM_LAUNCH(3, 8, 8); else KKM_SYM_LAUNCH(3, 4, 8); break;
-    case 4: if (tall) KKM_SYM_LAUNCH(4, 8, 8); else KKM_SYM_LAUNCH(4, 4, 8); break;
+    case 1: KKM_SYM_CASE(1, 2, 8); break;
+    case 2: KKM_SYM_CASE(2, 8, 16); break;
+    case 3: KKM_SYM_CASE(3, 8, 16); break;
+    case 4: KKM_SYM_CASE(4, 8, 16); break;
     default: return hipErrorInvalidValue;  // k > kSymMaxK is rejected before launch
   }
+#undef KKM_SYM_CASE
 #undef KKM_SYM_LAUNCH
   return hipGetLastError();
 }

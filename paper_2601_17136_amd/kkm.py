@@ -22,7 +22,8 @@ KKM_STORE_F32, KKM_STORE_F16 = 0, 1
 STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
-KKM_PACKED_FAST_K = 16
+KKM_PACKED_FAST_K = 32
+KKM_ABI_VERSION = 7
 KKM_NOALLOC_SCRATCH_BYTES = 64 << 20
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
           "seed")
@@ -64,7 +65,7 @@ _SIGS = {
     "kkm_last_warning": ([_vp], ctypes.c_char_p),
     "kkm_create": ([ctypes.POINTER(_vp), _vp, _sz], _i32),
     "kkm_destroy": ([_vp], _i32),
-    "kkm_plan": ([_i64, _i32, _i32, _sz, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
+    "kkm_plan": ([_i64, _i32, _i32, _i32, _sz, _i32, _i32, ctypes.POINTER(_i32), ctypes.POINTER(_sz)], _i32),
     "kkm_check_build_args": ([_i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
     "kkm_check_iterate_args": ([_i64, _i32, _i32], _i32),
     "kkm_build_kernel": ([_vp, _vp, _i64, _i32, _i32, ctypes.POINTER(kkm_params)], _i32),
@@ -102,6 +103,9 @@ def lib():
         for name, (args, res) in _SIGS.items():
             f = getattr(L, name)
             f.argtypes, f.restype = args, res
+        if L.kkm_abi_version() != KKM_ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI {L.kkm_abi_version()}, this binding {KKM_ABI_VERSION}: "
+                               "rebuild it with `python __graft_entry__.py build`")
         _lib = L
     return _lib
 
@@ -157,11 +161,12 @@ def kkm_destroy(ctx) -> None:
     _check(lib().kkm_destroy(ctx))
 
 
-def kkm_plan(n: int, d: int, k: int, mem_budget: int, mode: int = KKM_MODE_AUTO, storage: int = KKM_STORE_F32):
+def kkm_plan(n: int, d: int, k: int, kind: int, mem_budget: int, mode: int = KKM_MODE_AUTO,
+             storage: int = KKM_STORE_F32):
     """(resolved mode, device bytes); raises KKMError(KKM_ERR_OOM) if it cannot fit."""
     m, b = _i32(), _sz()
-    _check(lib().kkm_plan(int(n), int(d), int(k), int(mem_budget), int(mode), int(storage), ctypes.byref(m),
-                          ctypes.byref(b)))
+    _check(lib().kkm_plan(int(n), int(d), int(k), int(kind), int(mem_budget), int(mode), int(storage),
+                          ctypes.byref(m), ctypes.byref(b)))
     return m.value, b.value
 
 

@@ -35,9 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == 6
+    assert kkm.kkm_abi_version() == kkm.KKM_ABI_VERSION == 7
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 6" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 7" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
@@ -112,28 +112,48 @@ def test_null_context_is_rejected_without_a_gpu(L):
 
 
 def test_plan_resident_when_it_fits(L):
-    n, d, k = 20000, 784, 64
-    mode, need = kkm.kkm_plan(n, d, k, 288 << 30)
+    n, d, k = 20000, 784, 64    # fp32 polynomial K: past the labels its packed column side pays for
+    mode, need = kkm.kkm_plan(n, d, k, kkm.KKM_POLY, 288 << 30)
     assert mode == kkm.KKM_MODE_RESIDENT
     assert 4 * n * n <= need <= 4 * n * n * 1.1
 
 
 def test_plan_falls_back_to_on_the_fly(L):
-    n, d, k = 200000, 54, 7
-    mode, need = kkm.kkm_plan(n, d, k, 50 << 30)           # K alone is 160 GB, its triangle 80 GB
+    n, d, k, g = 200000, 54, 7, kkm.KKM_GAUSS
+    mode, need = kkm.kkm_plan(n, d, k, g, 50 << 30)           # K alone is 160 GB, its triangle 80 GB
     assert mode == kkm.KKM_MODE_ONTHEFLY and need < (2 << 30)   # staged points and partials only
-    mode, need = kkm.kkm_plan(n, d, 100, 288 << 30)        # too many labels for packed to pay
+    mode, need = kkm.kkm_plan(n, d, 100, g, 288 << 30)        # too many labels for packed storage
     assert mode == kkm.KKM_MODE_RESIDENT and need > 4 * n * n
-    mode, need = kkm.kkm_plan(n, d, 100, 100 << 30)        # and beyond its limit of 64
+    mode, need = kkm.kkm_plan(n, d, 100, g, 100 << 30)        # and beyond its limit of 64
     assert mode == kkm.KKM_MODE_ONTHEFLY
+
+
+# The largest k for which AUTO stores K packed: the column side on the
+# binary16 matrix cores (binary16 K, or the Gaussian's fp32 K in two binary16
+# parts) was measured fastest up to k = 64, on the fp32 ones up to k = 32
+# (k = 64: polynomial packed 2.72 vs resident 2.28 ms per update at
+# n = 60000, d = 780; 27.7 vs 26.0 ms at n = 200000, d = 54).
+@pytest.mark.parametrize("kind,storage,fast", [
+    (kkm.KKM_LINEAR, kkm.KKM_STORE_F32, kkm.KKM_PACKED_FAST_K),
+    (kkm.KKM_POLY, kkm.KKM_STORE_F32, kkm.KKM_PACKED_FAST_K),
+    (kkm.KKM_GAUSS, kkm.KKM_STORE_F32, kkm.KKM_PACKED_MAX_K),
+    (kkm.KKM_LINEAR, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K),
+    (kkm.KKM_POLY, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K),
+    (kkm.KKM_GAUSS, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K)])
+def test_plan_auto_packed_range(L, kind, storage, fast):
+    assert kkm.KKM_PACKED_FAST_K == 32 and kkm.KKM_PACKED_MAX_K == 64
+    n, d = 100000, 128
+    for k in (1, 16, fast, fast + 1, 100):
+        mode, _ = kkm.kkm_plan(n, d, k, kind, 1 << 40, kkm.KKM_MODE_AUTO, storage)
+        assert mode == (kkm.KKM_MODE_PACKED if k <= fast else kkm.KKM_MODE_RESIDENT), (kind, storage, k)
 
 
 # Each workload's storage mode measured fastest on MI355X (whole job, updates/s):
 # 1: packed (n = 2000, k = 8); 2: packed 3593 vs resident 2810; 3: packed 562 vs
-# resident 372; 4 (k = 64): resident 153 vs packed 126; 5: packed 66.0 vs
-# resident 38.8 vs on the fly 36.1.
+# resident 372; 4 (k = 64, Gaussian): packed 210 vs resident 157; 5: packed 66.0
+# vs resident 38.8 vs on the fly 36.1.
 MEASURED_FASTEST = {1: kkm.KKM_MODE_PACKED, 2: kkm.KKM_MODE_PACKED, 3: kkm.KKM_MODE_PACKED,
-                    4: kkm.KKM_MODE_RESIDENT, 5: kkm.KKM_MODE_PACKED}
+                    4: kkm.KKM_MODE_PACKED, 5: kkm.KKM_MODE_PACKED}
 
 
 @pytest.mark.parametrize("cfg", sorted(MEASURED_FASTEST))
@@ -142,7 +162,7 @@ def test_plan_auto_picks_the_measured_fastest(L, cfg):
     MI355X's memory (288 GB less 5%) picks the mode measured fastest."""
     from paper_2601_17136_amd import datagen
     w = datagen.WORKLOADS[cfg]
-    mode, _ = kkm.kkm_plan(w.n, w.d, w.k, int(0.95 * (288 << 30)))
+    mode, _ = kkm.kkm_plan(w.n, w.d, w.k, kkm.KINDS[w.kind], int(0.95 * (288 << 30)))
     assert mode == MEASURED_FASTEST[cfg]
 
 
@@ -163,17 +183,17 @@ def test_plan_packed_holds_half_of_k(L):
     """Packed storage: the upper block triangle (row block I keeps n_pad - 128 I
     columns), i.e. n_pad (n_pad + 128) / 2 floats, and the 200000-point problem
     that needs 160 GB resident fits in 100 GB."""
-    n, d, k = 200000, 54, 7
-    mode, need = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_PACKED)
+    n, d, k, g = 200000, 54, 7, kkm.KKM_GAUSS
+    mode, need = kkm.kkm_plan(n, d, k, g, 100 << 30, kkm.KKM_MODE_PACKED)
     n_pad = -(-n // 128) * 128
     tri = 4 * n_pad * (n_pad + 128) // 2
     assert mode == kkm.KKM_MODE_PACKED and tri <= need <= 1.06 * tri
-    _, need_res = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT)
+    _, need_res = kkm.kkm_plan(n, d, k, g, 1 << 40, kkm.KKM_MODE_RESIDENT)
     assert need < 0.53 * need_res
     with pytest.raises(kkm.KKMError) as e:          # more clusters than the packed SpMM handles
-        kkm.kkm_plan(n, d, kkm.KKM_PACKED_MAX_K + 1, 1 << 40, kkm.KKM_MODE_PACKED)
+        kkm.kkm_plan(n, d, kkm.KKM_PACKED_MAX_K + 1, g, 1 << 40, kkm.KKM_MODE_PACKED)
     assert e.value.code == kkm.KKM_ERR_ARG
-    mode, _ = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_AUTO)   # k <= 16: AUTO picks packed
+    mode, _ = kkm.kkm_plan(n, d, k, g, 100 << 30, kkm.KKM_MODE_AUTO)   # k <= 64, Gaussian: AUTO picks packed
     assert mode == kkm.KKM_MODE_PACKED
 
 
@@ -181,32 +201,32 @@ def test_plan_binary16_storage_halves_k(L):
     """Binary16 storage: 2 bytes per stored entry plus one fp32 row scale per
     point, so the 200000-point problem fits RESIDENT in 100 GB (80 GB of K)
     and PACKED in half of that."""
-    n, d, k = 200000, 54, 7
-    mode, need16 = kkm.kkm_plan(n, d, k, 100 << 30, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
-    _, need32 = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F32)
+    n, d, k, g = 200000, 54, 7, kkm.KKM_POLY
+    mode, need16 = kkm.kkm_plan(n, d, k, g, 100 << 30, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
+    _, need32 = kkm.kkm_plan(n, d, k, g, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F32)
     assert mode == kkm.KKM_MODE_RESIDENT
     assert 2 * n * n <= need16 <= 0.51 * need32
-    mode, needp = kkm.kkm_plan(n, d, 100, 100 << 30, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
-    _, need16_k100 = kkm.kkm_plan(n, d, 100, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
+    mode, needp = kkm.kkm_plan(n, d, 100, g, 100 << 30, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
+    _, need16_k100 = kkm.kkm_plan(n, d, 100, g, 1 << 40, kkm.KKM_MODE_RESIDENT, kkm.KKM_STORE_F16)
     assert mode == kkm.KKM_MODE_RESIDENT and needp == need16_k100
-    mode, needpk = kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
+    mode, needpk = kkm.kkm_plan(n, d, k, g, 1 << 40, kkm.KKM_MODE_AUTO, kkm.KKM_STORE_F16)
     assert mode == kkm.KKM_MODE_PACKED and needpk < 0.53 * need16
     with pytest.raises(kkm.KKMError) as e:
-        kkm.kkm_plan(n, d, k, 1 << 40, kkm.KKM_MODE_RESIDENT, 7)
+        kkm.kkm_plan(n, d, k, g, 1 << 40, kkm.KKM_MODE_RESIDENT, 7)
     assert e.value.code == kkm.KKM_ERR_ARG
 
 
 def test_plan_reports_oom(L):
     with pytest.raises(kkm.KKMError) as e:
-        kkm.kkm_plan(200000, 54, 7, 100 << 30, kkm.KKM_MODE_RESIDENT)
+        kkm.kkm_plan(200000, 54, 7, kkm.KKM_GAUSS, 100 << 30, kkm.KKM_MODE_RESIDENT)
     assert e.value.code == kkm.KKM_ERR_OOM
     with pytest.raises(kkm.KKMError) as e:
-        kkm.kkm_plan(200000, 54, 7, 1 << 20, kkm.KKM_MODE_AUTO)
+        kkm.kkm_plan(200000, 54, 7, kkm.KKM_GAUSS, 1 << 20, kkm.KKM_MODE_AUTO)
     assert e.value.code == kkm.KKM_ERR_OOM
 
 
 def test_plan_rejects_bad_sizes(L):
-    for args in [(0, 5, 1), (10, 0, 1), (10, 5, 11), (10, 5, 0)]:
+    for args in [(0, 5, 1, 2), (10, 0, 1, 2), (10, 5, 11, 2), (10, 5, 0, 2), (10, 5, 1, 3), (10, 5, 1, -1)]:
         with pytest.raises(kkm.KKMError) as e:
             kkm.kkm_plan(*args, 1 << 30)
         assert e.value.code == kkm.KKM_ERR_ARG

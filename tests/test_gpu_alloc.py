@@ -24,7 +24,7 @@ def test_large_k_within_the_planned_budget(oracle):
     X = datagen.make_points(2, n=N, d=D)[0]
     cl = datagen.random_init(N, K, 31)
     gamma = 1.0 / D
-    mode, need = kkm.kkm_plan(N, D, K, 1 << 40, kkm.KKM_MODE_RESIDENT)
+    mode, need = kkm.kkm_plan(N, D, K, kkm.KKM_GAUSS, 1 << 40, kkm.KKM_MODE_RESIDENT)
     assert mode == kkm.KKM_MODE_RESIDENT and need > 8e9
     print(f"[gpu] large K: n={N} d={D}, planned {need} bytes", flush=True)
     kern = oracle.Kernel("gauss", gamma, 0.0, 1)

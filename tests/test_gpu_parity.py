@@ -58,6 +58,10 @@ CASES = {
     "k20-n1500-gauss": (lambda: datagen.make_points(2, n=1500, d=24)[0], 20, "gauss", 1.0 / 24, 0.0, 1, 22),
     "k40-n1800-poly": (lambda: datagen.separated_blobs(1800, 6, 40, seed=6, spread=2.5, sigma=1.0)[0],
                        40, "poly", 0.2, 1.0, 2, 23),
+    # more than 16 labels above 4096 points: the packed SpMM's 16-tile segments
+    # (ragged last segment), binary16 split column side and fp32 column side
+    "k40-n6000-gauss": (lambda: datagen.make_points(4, n=6000, d=16)[0], 40, "gauss", 0.5, 0.0, 1, 30),
+    "k24-n5000-poly": (lambda: datagen.make_points(2, n=5000, d=20)[0], 24, "poly", 0.05, 1.0, 2, 31),
 }
 
 
@@ -333,7 +337,7 @@ def test_gauss_fixup_overflow_path(oracle, mode, d):
     _torch_cuda()
     from paper_2601_17136_amd import kkm
     X = datagen.make_points(4, n=3000, d=d)[0] + np.float32(30.0)
-    _, need = kkm.kkm_plan(3000, X.shape[1], 1, 1 << 40, kkm.MODES[mode])
+    _, need = kkm.kkm_plan(3000, X.shape[1], 1, kkm.KKM_GAUSS, 1 << 40, kkm.MODES[mode])
     with Engine(X, "gauss", 0.5, mode=mode, mem_budget=need + 4096) as eng:
         K = eng.K_rows()
         info = eng.info()
@@ -350,17 +354,22 @@ def test_gauss_fixup_overflow_path(oracle, mode, d):
     assert rowscaled_err(K2, oracle.Kernel("gauss", 0.5).matrix(X)) <= TOL
 
 
-@pytest.mark.parametrize("k_hint,want", [(8, "packed"), (40, "resident"), (0, "resident")])
-def test_auto_mode_follows_the_k_hint(oracle, k_hint, want):
-    """AUTO stores K packed when the announced k is at most 16 and fully
-    otherwise (memory allowing); either way the step matches the oracle."""
+@pytest.mark.parametrize("kind,k_hint,want", [("gauss", 8, "packed"), ("gauss", 40, "packed"),
+                                               ("poly", 32, "packed"), ("poly", 40, "resident"),
+                                               ("gauss", 0, "resident")])
+def test_auto_mode_follows_the_k_hint(oracle, kind, k_hint, want):
+    """AUTO stores K packed when the announced k is at most 64 (Gaussian: the
+    column side on the binary16 matrix cores) or 32 (polynomial: on the fp32
+    ones), and fully otherwise or without a hint (memory allowing); either way
+    the step matches the oracle."""
     _torch_cuda()
     from paper_2601_17136_amd import kkm
     X = datagen.make_points(2, n=700, d=12)[0]
     k = k_hint or 5
     cl = datagen.random_init(700, k, 3)
-    ref = oracle.step_full(oracle.Kernel("gauss", 0.1).matrix(X), cl, k)
-    with Engine(X, "gauss", 0.1, mode="auto", k_hint=k_hint) as eng:
+    g, c, p = (0.1, 0.0, 1) if kind == "gauss" else (0.05, 1.0, 2)
+    ref = oracle.step_full(oracle.Kernel(kind, g, c, p).matrix(X), cl, k)
+    with Engine(X, kind, g, c, p, mode="auto", k_hint=k_hint) as eng:
         assert eng.info()["mode"] == kkm.MODES[want]
         out = eng.step(cl, k)
     assert rowscaled_err(out["E"], ref["E"]) <= TOL and rowscaled_err(out["D"], ref["D"]) <= TOL

@@ -65,6 +65,36 @@ def test_workload_step_full_size(oracle, cfg, mode):
           flush=True)
 
 
+@pytest.mark.parametrize("kind,k", [("poly", 40), ("gauss", 33), ("gauss", 64)])
+def test_many_labels_tall_chunks(oracle, kind, k):
+    """More than 16 labels above 40000 points: the packed SpMM's 128-row
+    chunks and 32-tile segments with three or four 16-label blocks, on the
+    fp32 column side (polynomial) and the split binary16 one (Gaussian);
+    checked on sampled rows as above."""
+    torch = pytest.importorskip("torch")
+    assert torch.cuda.is_available()
+    n, d = 45000, 48
+    X = datagen.make_points(5, n=n, d=d)[0]
+    cl = datagen.random_init(n, k, 40 + k)
+    g, c, p = (1.0 / d, 1.0, 2) if kind == "poly" else (1.0 / d, 0.0, 1)
+    print(f"[gpu] packed, n={n} d={d} k={k} {kind}", flush=True)
+    kern = oracle.Kernel(kind, g, c, p)
+    rows = _rows(n, k)
+    with Engine(X, kind, g, c, p, mode="packed") as eng:
+        out = eng.step(cl, k)
+        again = eng.step(cl, k)
+    assert np.array_equal(out["E"], again["E"]) and out["J"] == again["J"]
+    ref = oracle.step_rows(kern, X, cl, k, rows)
+    np.testing.assert_array_equal(out["counts"], ref["counts"])
+    ez, eJ = rel_err(out["z"], ref["z"]), rel_err(out["J"], ref["J"])
+    eE = rowscaled_err(out["E"][rows], ref["E"])
+    eD = rowscaled_err(out["D"][rows], ref["D"])
+    assert ez <= TOL and eJ <= TOL and eE <= TOL and eD <= TOL, (ez, eJ, eE, eD)
+    D = out["D"]
+    assert np.all(D[np.arange(n), out["cl"]] == D.min(axis=1))
+    print(f"[gpu] k={k} {kind}: E {eE:.2e} D {eD:.2e} z {ez:.2e} J {eJ:.2e}", flush=True)
+
+
 @pytest.mark.parametrize("cfg,mode", [(2, "packed"), (4, "packed"), (2, "resident"), (4, "resident"),
                                       (2, "onthefly")])
 def test_workload_loop_properties(oracle, cfg, mode):
