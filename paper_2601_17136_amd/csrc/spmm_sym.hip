@@ -12,13 +12,17 @@
 // which runs on the matrix cores with 16 labels per block, exact in its
 // products (each is 0 or the entry itself):
 //  - fp32 K in general: v_mfma_f32_16x16x4_f32, 4 columns per instruction;
-//  - binary16 K: v_mfma_f32_16x16x16_f16, 16 columns per instruction;
+//  - binary16 K: v_mfma_f32_16x16x32_f16, 32 columns per instruction;
 //  - fp32 K with every entry in [0, 1] (the Gaussian): each entry as the sum
 //    of two binary16 values, hi = its rounding and lo = the rest rounded, on
-//    v_mfma_f32_16x16x16_f16: 16 columns per two instructions, and hi + lo
+//    v_mfma_f32_16x16x32_f16: 32 columns per two instructions, and hi + lo
 //    within 2^-22 of the entry relative to it (2^-25 absolute below binary16's
 //    normal range; the row's own diagonal entry is 1), sums in fp32.  At
 //    k = 64 this takes the column side from above the HBM time to below it.
+// The k slots of an instruction are summed over, so any order of the
+// columns over them is right as long as the one-hot operand and the entries
+// take the same one: each lane puts the 4 columns of its slot in column
+// group g, then the 4 of group g + 1.
 //
 // Workgroup (chunk q, segment sg): NW wavefronts (4 or 8), one 16-row group
 // each, over the column tiles of segment sg (BSEG tiles) that the chunk's
@@ -50,6 +54,7 @@ namespace kkm {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 
 namespace {
 
@@ -200,24 +205,37 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     // MFMA operand layout.  The next tile's loads are issued as soon as the
     // whole block is staged, so they are in flight while it is multiplied.
     auto mma = [&](int g0, int ng, int cb) {
+      if constexpr (SPLIT) {
+        // entries in [0, 1] as a sum of two binary16 values (hi, and the
+        // rest rounded: within 2^-22 relative).  Column groups g and g + 1
+        // go to one v_mfma_f32_16x16x32_f16 (k slots 0-3 and 4-7 of each
+        // lane; the one-hot operand takes the same order): 32 columns per
+        // instruction and label block, exact 0/1 products, fp32 sums.
 #pragma unroll
-      for (int gg = 0; gg < ng; ++gg) {
-        const int g = g0 + gg;
-        f4 v = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
-        if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (SPLIT) {
-          // entries in [0, 1] as a sum of two binary16 values (hi, and the
-          // rest rounded: within 2^-22 relative); 16 columns per instruction
-          // and label block, exact 0/1 products, fp32 sums
-          const h4 hi = __builtin_convertvector(v, h4);
-          const h4 lo = __builtin_convertvector(v - __builtin_convertvector(hi, f4), h4);
+        for (int gg = 0; gg < ng; gg += 2) {
+          const int g = g0 + gg;
+          f4 v0 = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];      // row li, columns 16g + 4lk .. +3
+          f4 v1 = tw[li * kCh + ((4 * (g + 1 - cb) + lk) ^ li)];  // ... and 16(g+1) + 4lk .. +3
+          if (diag && dz) v0 = v1 = f4{0.f, 0.f, 0.f, 0.f};
+          const h4 h0 = __builtin_convertvector(v0, h4), h1 = __builtin_convertvector(v1, h4);
+          const h4 l0 = __builtin_convertvector(v0 - __builtin_convertvector(h0, f4), h4);
+          const h4 l1 = __builtin_convertvector(v1 - __builtin_convertvector(h1, f4), h4);
+          const h8 hi = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
+          const h8 lo = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
-            const h4 a = onehot[(msk[nb] >> (4 * g)) & 15u];
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, hi, D[nb], 0, 0, 0);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, lo, D[nb], 0, 0, 0);
+            const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
+                                                 onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, hi, D[nb], 0, 0, 0);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, lo, D[nb], 0, 0, 0);
           }
-        } else {
+        }
+      } else {
+#pragma unroll
+        for (int gg = 0; gg < ng; ++gg) {
+          const int g = g0 + gg;
+          f4 v = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
+          if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -232,7 +250,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       // binary16: the raw halves of the whole block are staged (4 KB per
       // wavefront; 8-byte chunk c of row r at c ^ 2r, conflict-free for the
       // row-wise writes and for the operand reads, which LDS serves 32 lanes
-      // at a time) and the column side runs on v_mfma_f32_16x16x16_f16: 16
+      // at a time) and the column side runs on v_mfma_f32_16x16x32_f16: 32
       // columns per instruction and label block, the one-hot operand from a
       // table of the 16 nibbles; the products are exact and the sums fp32,
       // and the row's scale is applied at the end.
@@ -247,13 +265,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
       __builtin_amdgcn_sched_barrier(0);
       if (any) {
 #pragma unroll
-        for (int g = 0; g < 8; ++g) {
-          h4 v = th[li * 32 + ((4 * g + lk) ^ (2 * li))];  // row li, columns 16g + 4lk .. +3
-          if (diag && dz) v = h4{0, 0, 0, 0};
+        for (int g = 0; g < 8; g += 2) {  // column groups g and g + 1 per instruction
+          const h4 v0 = th[li * 32 + ((4 * g + lk) ^ (2 * li))];  // row li, columns 16g + 4lk .. +3
+          const h4 v1 = th[li * 32 + ((4 * g + 4 + lk) ^ (2 * li))];
+          h8 v = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+          if (diag && dz) v = h8{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
-            const h4 a = onehot[(msk[nb] >> (4 * g)) & 15u];
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(a, v, D[nb], 0, 0, 0);
+            const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
+                                                 onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
+            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, v, D[nb], 0, 0, 0);
           }
         }
       }
