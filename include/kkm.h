@@ -67,17 +67,16 @@ typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
  * KKM_PACKED_MAX_K clusters; it is the fastest mode for small k.  ONTHEFLY
  * never stores K: every iteration recomputes its tiles and folds them
  * straight into E, which is the paper's single-GPU sliding-window baseline
- * (Section VI-D) done tile by tile.  AUTO picks by the memory budget, the
- * kernel, the storage and the cluster count the caller announces in
- * kkm_params.k_hint:
- *   k_hint in 1..KKM_PACKED_MAX_K with F16 storage or the Gaussian kernel,
- *   or in 1..KKM_PACKED_FAST_K otherwise: PACKED if it fits, else as below.
- *     PACKED's per-label column side runs on the binary16 matrix cores for a
- *     binary16 K and for the Gaussian's fp32 K (whose entries, all in [0, 1],
- *     it takes as two binary16 parts), on the fp32 ones otherwise; measured
- *     fastest in these ranges at n = 20000 .. 200000;
- *   otherwise: RESIDENT if it fits, else PACKED if it fits (and k_hint is 0
- *     or at most KKM_PACKED_MAX_K), else ONTHEFLY.
+ * (Section VI-D) done tile by tile.  AUTO picks by the memory budget and
+ * the cluster count the caller announces in kkm_params.k_hint:
+ *   k_hint in 1..KKM_PACKED_FAST_K: PACKED if it fits, else RESIDENT if it
+ *     fits, else ONTHEFLY.  PACKED's per-label column side runs on the
+ *     binary16 matrix cores (an fp32 K's entries each as two binary16 parts,
+ *     the rows of the linear and polynomial kernels scaled by powers of two
+ *     first), which keeps it below the HBM time up to 64 labels: measured
+ *     fastest there at n = 20000 .. 200000 for every kernel and storage;
+ *   otherwise: RESIDENT if it fits, else (k_hint 0) PACKED if it fits, else
+ *     ONTHEFLY.
  * A kkm_iterate with more than KKM_PACKED_MAX_K clusters on a K that AUTO
  * stored PACKED (k_hint 0) fails with KKM_ERR_ARG. */
 typedef enum kkm_mode {
@@ -87,7 +86,7 @@ typedef enum kkm_mode {
   KKM_MODE_PACKED = 3
 } kkm_mode;
 #define KKM_PACKED_MAX_K 64 /* largest cluster count kkm_iterate accepts on PACKED storage */
-#define KKM_PACKED_FAST_K 32 /* AUTO stores an fp32 linear or polynomial K PACKED for a k_hint up to this */
+#define KKM_PACKED_FAST_K 64 /* AUTO stores K PACKED for a k_hint up to this */
 #define KKM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20) /* static scratch of kkm_iterate_noalloc, per GPU */
 
 /* Number format of a stored K (RESIDENT or PACKED; ONTHEFLY stores nothing
@@ -186,10 +185,11 @@ const char *kkm_last_warning(const kkm_ctx *ctx);
  * the Gaussian build's fix-up list takes up to a quarter of the room the
  * budget leaves, and the first iteration that needs that room frees it
  * (after one synchronisation to read its counts), so it is not counted
- * here.  kind: kkm_kind of the kernel to be built.  requested_mode:
- * kkm_mode; AUTO resolves by the budget, kind, storage and k as a build
+ * here.  kind: kkm_kind of the kernel to be built (the linear and
+ * polynomial kernels keep a bound per row where K is packed or binary16).
+ * requested_mode: kkm_mode; AUTO resolves by the budget and k as a build
  * with k_hint = k does (see kkm_mode).
- * storage: kkm_storage of K (sizes K and the row scales).
+ * storage: kkm_storage of K (sizes K and the row bounds).
  * Errors: KKM_ERR_ARG (bad sizes, kind or storage, or PACKED with
  * k > KKM_PACKED_MAX_K), KKM_ERR_OOM (even the on-the-fly mode does not fit,
  * or the requested storing mode does not). */
@@ -213,7 +213,12 @@ int kkm_check_iterate_args(int64_t n, int32_t k, int32_t max_iter);
  *   |x|^2 + |y|^2 - 2 x.y may have lost accuracy to cancellation are
  *   recomputed from the coordinate differences.
  * PACKED: as RESIDENT, but only the tiles I <= J of the 128 x 128 tiling
- *   are stored (row i keeps columns 128*floor(i/128) .. ld-1).
+ *   are stored (row i keeps columns 128*floor(i/128) .. ld-1).  The linear
+ *   and polynomial kernels also keep a bound per row (Cauchy-Schwarz) for
+ *   the update's column side, which sums each fp32 entry's two binary16
+ *   parts: an entry v of row i is represented within
+ *   max(2^-22 |v|, 2^-25 p_i), p_i the power of two at or above the bound
+ *   (1 for the Gaussian), and every sum stays fp32.
  * ONTHEFLY: stages X and row norms only.
  * storage F16 (RESIDENT, PACKED): K in binary16 with row scales, see
  *   kkm_storage; diag K stays fp32.

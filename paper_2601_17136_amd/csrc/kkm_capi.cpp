@@ -96,9 +96,13 @@ size_t k_bytes(const Sizes& s, int mode, int storage) {
   if (mode == KKM_MODE_PACKED) return (size_t)packed_floats(s.n, s.ld) * k_elem(storage);
   return mode == KKM_MODE_RESIDENT ? (size_t)s.n * (size_t)s.ld * k_elem(storage) : 0;
 }
-// binary16 storage of the linear and polynomial kernels keeps a scale per row
+// The linear and polynomial kernels keep a bound per row of |K(i, .)| where
+// K is stored in binary16 (the stored values are K / bound) or packed (the
+// packed SpMM's column side scales each row by the power of two at or above
+// its bound).  The Gaussian's entries lie in [0, 1] and need none.
 bool row_scaled(int mode, int storage, int kind) {
-  return storage == KKM_STORE_F16 && (mode == KKM_MODE_RESIDENT || mode == KKM_MODE_PACKED) && kind != KKM_GAUSS;
+  return kind != KKM_GAUSS &&
+         (mode == KKM_MODE_PACKED || (storage == KKM_STORE_F16 && mode == KKM_MODE_RESIDENT));
 }
 int chunk_len_for(const Sizes& s, int mode) { return mode == KKM_MODE_PACKED ? sym_chunk_for(s.n) : kChunk; }
 int64_t qmax_for(const Sizes& s, int k, int mode) {
@@ -349,12 +353,6 @@ void free_build(kkm_ctx* c) {
   c->panel_e = false;
 }
 
-// The packed SpMM's column side may take each fp32 entry as two binary16
-// parts only where every entry lies in [0, 1]: the Gaussian kernel.
-bool split_column_side(const kkm_ctx* c) {
-  return c->mode == KKM_MODE_PACKED && c->storage == KKM_STORE_F32 && c->kind == KKM_GAUSS;
-}
-
 // Lay the per-update scratch for k clusters out over base (ws_bytes of it)
 // and clear what must start at zero.
 int carve_from(kkm_ctx* c, int k, void* base) {
@@ -382,7 +380,6 @@ int carve_from(kkm_ctx* c, int k, void* base) {
   b.ncol = c->pc1 > 0 ? c->pc1 - c->pc0 : s.n;
   b.trK = c->trK;
   b.kf16 = c->storage == KKM_STORE_F16;
-  b.ksplit = split_column_side(c);
   b.kw = c->kw;
   b.Et = (float*)take((size_t)k * s.ld * 4);
   if (c->mode == KKM_MODE_RESIDENT || c->mode == KKM_MODE_PACKED) {
@@ -528,7 +525,6 @@ int ensure_ws(kkm_ctx* c, int k, int iters) {
   b.trK = c->trK;
   b.kw = c->kw;
   b.kf16 = c->storage == KKM_STORE_F16;
-  b.ksplit = split_column_side(c);
   if (c->iter_ws < iters || !c->obj) {
     free_hist(c);
     int cap = std::max(iters, 64);
@@ -622,20 +618,15 @@ int check_ready(kkm_ctx* c, int32_t k, int32_t max_iter) {
 // The mode AUTO resolves to, and the device bytes of a mode.  k_known: k is
 // the cluster count the loop will run with; otherwise (a build without a
 // hint) k only sizes the scratch and the mode is picked without it.
-//   AUTO with k known: PACKED when k is at most packed_fast_k and it fits (it
-//   streams half the bytes per update, and its per-label column side stays
-//   below the HBM time up to that many labels); else RESIDENT when it fits;
-//   else PACKED when k <= KKM_PACKED_MAX_K and it fits; else ONTHEFLY.
+//   AUTO with k known: PACKED when k <= KKM_PACKED_FAST_K and it fits (it
+//   streams half the bytes per update, and its per-label column side, on the
+//   binary16 matrix cores, stays below the HBM time up to that many
+//   labels); else RESIDENT when it fits; else ONTHEFLY.
 //   AUTO with k unknown: RESIDENT, else PACKED, else ONTHEFLY, whichever
 //   fits first.
 // ONTHEFLY is picked only when no stored K fits: at every width measured
-// (d >= 54) a stored K is at least as fast per update.
-int packed_fast_k(int32_t kind, int32_t storage) {
-  // the column side on the binary16 matrix cores (binary16 K, or the fp32
-  // Gaussian split in two binary16 parts) stays fastest up to the packed
-  // storage's limit; on the fp32 ones up to KKM_PACKED_FAST_K labels
-  return storage == KKM_STORE_F16 || kind == KKM_GAUSS ? KKM_PACKED_MAX_K : KKM_PACKED_FAST_K;
-}
+// (d >= 54) a stored K is at least as fast per update.  kind sizes the row
+// bounds the linear and polynomial kernels keep.
 int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, int32_t kind, size_t mem_budget,
               int32_t requested_mode, int32_t storage, int32_t* mode_out, size_t* bytes_out) {
   if (n < 1 || n > 2147483647LL || d < 1 || d > 65536)
@@ -655,9 +646,9 @@ int plan_impl(int64_t n, int32_t d, int32_t k, bool k_known, int32_t kind, size_
   auto fits = [&](int m) { return need_for(m) <= mem_budget; };
   int mode = requested_mode;
   if (mode == KKM_MODE_AUTO) {
-    if (k_known && k <= packed_fast_k(kind, storage) && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
+    if (k_known && k <= KKM_PACKED_FAST_K && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
     else if (fits(KKM_MODE_RESIDENT)) mode = KKM_MODE_RESIDENT;
-    else if ((!k_known || k <= KKM_PACKED_MAX_K) && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
+    else if (!k_known && fits(KKM_MODE_PACKED)) mode = KKM_MODE_PACKED;
     else mode = KKM_MODE_ONTHEFLY;
   }
   const size_t need = need_for(mode);
@@ -908,8 +899,9 @@ int build_impl(kkm_ctx* c, const float* X, int64_t n, int32_t d, int32_t kind, c
            return launch_gemm_kappa_panel(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, pr0, pr1, pc0, pc1, s.ld, kp,
                                           (float*)c->K, c->diagK, c->fix_list, c->fix_count,
                                           c->fix_cap / kFixSegs, c->stream);
+         // the build divides by the row bounds only for binary16 storage
          return launch_gemm_kappa(c->Xp, c->nrm, c->maxnrm, n, s.d_pad, s.ld, mode == KKM_MODE_PACKED, f16,
-                                  c->kw, kp, c->K, c->diagK, c->fix_list, c->fix_count,
+                                  f16 ? c->kw : nullptr, kp, c->K, c->diagK, c->fix_list, c->fix_count,
                                   c->fix_cap / kFixSegs, c->bmax, c->stream);
        })))
     return rc;

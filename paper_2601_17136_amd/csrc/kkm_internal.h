@@ -126,12 +126,11 @@ struct IterBufs {
                         // has label 16nb + li
   int nlb;              // label blocks of 16, ceil(k / 16)
   const float* zero;    // kTile zero floats, read in place of rows not stored in a tile
-  // stored K in binary16: entry (i, j) holds K(i,j) / kw[i] (kw null: 1)
+  // stored K in binary16: entry (i, j) holds K(i,j) / kw[i] (kw null: 1);
+  // packed fp32 K of the linear and polynomial kernels: kw[i] bounds
+  // |K(i, .)| (null for the Gaussian)
   int kf16;
   const float* kw;
-  // fp32 K whose entries lie in [0, 1] (the Gaussian): the packed SpMM's
-  // column side may split each entry into two binary16 parts
-  int ksplit;
 };
 
 // binary16 storage of K

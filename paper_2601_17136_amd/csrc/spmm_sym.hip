@@ -11,14 +11,17 @@
 // of their column: a product with the one-hot matrix of the column labels,
 // which runs on the matrix cores with 16 labels per block, exact in its
 // products (each is 0 or the entry itself):
-//  - fp32 K in general: v_mfma_f32_16x16x4_f32, 4 columns per instruction;
 //  - binary16 K: v_mfma_f32_16x16x32_f16, 32 columns per instruction;
-//  - fp32 K with every entry in [0, 1] (the Gaussian): each entry as the sum
-//    of two binary16 values, hi = its rounding and lo = the rest rounded, on
-//    v_mfma_f32_16x16x32_f16: 32 columns per two instructions, and hi + lo
-//    within 2^-22 of the entry relative to it (2^-25 absolute below binary16's
-//    normal range; the row's own diagonal entry is 1), sums in fp32.  At
-//    k = 64 this takes the column side from above the HBM time to below it.
+//  - fp32 K: each entry v of row r, divided by p_r, a power of two at or
+//    above a bound of |K(r, .)| (1 for the Gaussian, whose entries lie in
+//    [0, 1]; the Cauchy-Schwarz row bound otherwise), as the sum of two
+//    binary16 values, hi = its rounding and lo = the rest rounded, on
+//    v_mfma_f32_16x16x32_f16: 32 columns per two instructions.  hi + lo is
+//    within 2^-22 |v / p_r| of v / p_r, or 2^-25 absolute below binary16's
+//    normal range; the row's sums are multiplied by p_r again (exact) and
+//    stay fp32.  On the fp32 matrix instruction (4 columns each) the column
+//    side outweighed the HBM time above 32 labels; split, it stays below it
+//    up to 64.
 // The k slots of an instruction are summed over, so any order of the
 // columns over them is right as long as the one-hot operand and the entries
 // take the same one: each lane puts the 4 columns of its slot in column
@@ -64,11 +67,18 @@ namespace {
 // KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
 // binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
 // when a tile is consumed, so everything after the loads is the same.
-template <int NB, int NW, int BSEG, typename KT, bool SPLIT>
+// The smallest power of two at or above w, for w up to 2^126 (larger w,
+// infinities and NaN give 2^126; w <= 0 does not occur: the bounds are
+// positive).
+__device__ inline float pow2_at_least(float w) {
+  w = fminf(w, 0x1p126f);
+  return __uint_as_float((__float_as_uint(w) + 0x007fffffu) & 0x7f800000u);
+}
+
+template <int NB, int NW, int BSEG, typename KT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const KT* __restrict__ Kp, IterBufs b) {
   constexpr bool kHalf = sizeof(KT) == 2;
-  static_assert(!(SPLIT && kHalf), "the split column side is for fp32 K");
   using BufT = typename std::conditional<kHalf, h4, f4>::type;
   constexpr int R = 16 * NW, NT = 64 * NW;
   // With one label block the whole 16 x 128 block is staged at once; with
@@ -114,7 +124,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
   __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
-  __shared__ h4 onehot[kHalf || SPLIT ? 16 : 1];  // the 4 bits of a nibble as binary16 0 / 1
+  __shared__ h4 onehot[16];                      // the 4 bits of a nibble as binary16 0 / 1
+  __shared__ float rsc[kHalf ? 1 : R];           // fp32 K: the rows' column-side scales
 
   const int I0 = i0 / kTile;
   const int J_lo = max(Js, I0), J_hi = Je;
@@ -162,7 +173,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   BufT bb[8];
   if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
-  if ((kHalf || SPLIT) && tid < 16)
+  // fp32 K: row u of the chunk is scaled by rsc[u], a power of two, for the
+  // column side (exact both ways; read per tile, so it holds no register)
+  if (!kHalf && tid < R) {
+    const int iv = cr[tid];
+    rsc[tid] = iv >= 0 && b.kw ? 1.f / pow2_at_least(b.kw[iv]) : 1.f;
+  }
+  if (tid < 16)
     onehot[tid] = h4{(_Float16)(tid & 1), (_Float16)((tid >> 1) & 1), (_Float16)((tid >> 2) & 1),
                      (_Float16)((tid >> 3) & 1)};
 #pragma unroll
@@ -204,45 +221,32 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     // writes and the MFMA-layout reads conflict-free) and read back in the
     // MFMA operand layout.  The next tile's loads are issued as soon as the
     // whole block is staged, so they are in flight while it is multiplied.
+    // fp32 K: the row's entries (scaled into [-1, 1]) as a sum of two
+    // binary16 values (hi, and the rest rounded).  Column groups g and g + 1
+    // go to one v_mfma_f32_16x16x32_f16 (k slots 0-3 and 4-7 of each lane;
+    // the one-hot operand takes the same order): 32 columns per instruction
+    // and label block, exact 0/1 products, fp32 sums.
     auto mma = [&](int g0, int ng, int cb) {
-      if constexpr (SPLIT) {
-        // entries in [0, 1] as a sum of two binary16 values (hi, and the
-        // rest rounded: within 2^-22 relative).  Column groups g and g + 1
-        // go to one v_mfma_f32_16x16x32_f16 (k slots 0-3 and 4-7 of each
-        // lane; the one-hot operand takes the same order): 32 columns per
-        // instruction and label block, exact 0/1 products, fp32 sums.
+      const float ips = rsc[um];
 #pragma unroll
-        for (int gg = 0; gg < ng; gg += 2) {
-          const int g = g0 + gg;
-          f4 v0 = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];      // row li, columns 16g + 4lk .. +3
-          f4 v1 = tw[li * kCh + ((4 * (g + 1 - cb) + lk) ^ li)];  // ... and 16(g+1) + 4lk .. +3
-          if (diag && dz) v0 = v1 = f4{0.f, 0.f, 0.f, 0.f};
-          const h4 h0 = __builtin_convertvector(v0, h4), h1 = __builtin_convertvector(v1, h4);
-          const h4 l0 = __builtin_convertvector(v0 - __builtin_convertvector(h0, f4), h4);
-          const h4 l1 = __builtin_convertvector(v1 - __builtin_convertvector(h1, f4), h4);
-          const h8 hi = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
-          const h8 lo = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
+      for (int gg = 0; gg < ng; gg += 2) {
+        const int g = g0 + gg;
+        f4 v0 = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];      // row li, columns 16g + 4lk .. +3
+        f4 v1 = tw[li * kCh + ((4 * (g + 1 - cb) + lk) ^ li)];  // ... and 16(g+1) + 4lk .. +3
+        if (diag && dz) v0 = v1 = f4{0.f, 0.f, 0.f, 0.f};
+        v0 *= ips;
+        v1 *= ips;
+        const h4 h0 = __builtin_convertvector(v0, h4), h1 = __builtin_convertvector(v1, h4);
+        const h4 l0 = __builtin_convertvector(v0 - __builtin_convertvector(h0, f4), h4);
+        const h4 l1 = __builtin_convertvector(v1 - __builtin_convertvector(h1, f4), h4);
+        const h8 hi = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
+        const h8 lo = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
-                                                 onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, hi, D[nb], 0, 0, 0);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, lo, D[nb], 0, 0, 0);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int gg = 0; gg < ng; ++gg) {
-          const int g = g0 + gg;
-          f4 v = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];  // row li, columns 16g + 4lk .. +3
-          if (diag && dz) v = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-              const float a = (float)((msk[nb] >> (4 * g + e)) & 1u);
-              D[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, v[e], D[nb], 0, 0, 0);
-            }
+        for (int nb = 0; nb < NB; ++nb) {
+          const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
+                                               onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
+          D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, hi, D[nb], 0, 0, 0);
+          D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, lo, D[nb], 0, 0, 0);
         }
       }
     };
@@ -327,6 +331,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     const float wm = (im >= 0 && b.kw) ? b.kw[im] : 1.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) D[nb] *= wm;
+  }
+  if constexpr (!kHalf) {
+    const float ps = 1.f / rsc[um];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) D[nb] *= ps;
   }
   const int64_t ecs = (int64_t)b.qmax * R;
   if (im >= 0)
@@ -455,13 +464,10 @@ hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
 #define KKM_SYM_LAUNCH(NB, NW, S)                                                                        \
   do {                                                                                                   \
     if (b.kf16)                                                                                          \
-      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, half_t, false>), dim3(grid), dim3(64 * NW), 0, s,     \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, half_t>), dim3(grid), dim3(64 * NW), 0, s,            \
                          (const half_t*)Kp, b);                                                          \
-    else if (b.ksplit)                                                                                   \
-      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float, true>), dim3(grid), dim3(64 * NW), 0, s,       \
-                         (const float*)Kp, b);                                                           \
     else                                                                                                 \
-      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float, false>), dim3(grid), dim3(64 * NW), 0, s,      \
+      hipLaunchKernelGGL((spmm_sym_kernel<NB, NW, S, float>), dim3(grid), dim3(64 * NW), 0, s,             \
                          (const float*)Kp, b);                                                           \
   } while (0)
   // the segment lengths sym_seg_for sets

@@ -22,7 +22,7 @@ KKM_STORE_F32, KKM_STORE_F16 = 0, 1
 STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
-KKM_PACKED_FAST_K = 32
+KKM_PACKED_FAST_K = 64
 KKM_ABI_VERSION = 7
 KKM_NOALLOC_SCRATCH_BYTES = 64 << 20
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",

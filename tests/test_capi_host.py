@@ -112,7 +112,7 @@ def test_null_context_is_rejected_without_a_gpu(L):
 
 
 def test_plan_resident_when_it_fits(L):
-    n, d, k = 20000, 784, 64    # fp32 polynomial K: past the labels its packed column side pays for
+    n, d, k = 20000, 784, 65    # more labels than packed storage takes
     mode, need = kkm.kkm_plan(n, d, k, kkm.KKM_POLY, 288 << 30)
     assert mode == kkm.KKM_MODE_RESIDENT
     assert 4 * n * n <= need <= 4 * n * n * 1.1
@@ -128,30 +128,29 @@ def test_plan_falls_back_to_on_the_fly(L):
     assert mode == kkm.KKM_MODE_ONTHEFLY
 
 
-# The largest k for which AUTO stores K packed: the column side on the
-# binary16 matrix cores (binary16 K, or the Gaussian's fp32 K in two binary16
-# parts) was measured fastest up to k = 64, on the fp32 ones up to k = 32
-# (k = 64: polynomial packed 2.72 vs resident 2.28 ms per update at
-# n = 60000, d = 780; 27.7 vs 26.0 ms at n = 200000, d = 54).
-@pytest.mark.parametrize("kind,storage,fast", [
-    (kkm.KKM_LINEAR, kkm.KKM_STORE_F32, kkm.KKM_PACKED_FAST_K),
-    (kkm.KKM_POLY, kkm.KKM_STORE_F32, kkm.KKM_PACKED_FAST_K),
-    (kkm.KKM_GAUSS, kkm.KKM_STORE_F32, kkm.KKM_PACKED_MAX_K),
-    (kkm.KKM_LINEAR, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K),
-    (kkm.KKM_POLY, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K),
-    (kkm.KKM_GAUSS, kkm.KKM_STORE_F16, kkm.KKM_PACKED_MAX_K)])
-def test_plan_auto_packed_range(L, kind, storage, fast):
-    assert kkm.KKM_PACKED_FAST_K == 32 and kkm.KKM_PACKED_MAX_K == 64
+# AUTO stores K packed up to k = 64 for every kernel and storage: the packed
+# column side runs on the binary16 matrix cores (binary16 K, or an fp32 K's
+# entries as two binary16 parts), measured fastest there at n = 20000 to
+# 200000 (polynomial, k = 64: packed 1.48 vs resident 2.28 ms per update at
+# n = 60000, d = 780; 14.4 vs 26.0 ms at n = 200000, d = 54).
+@pytest.mark.parametrize("kind", [kkm.KKM_LINEAR, kkm.KKM_POLY, kkm.KKM_GAUSS])
+@pytest.mark.parametrize("storage", [kkm.KKM_STORE_F32, kkm.KKM_STORE_F16])
+def test_plan_auto_packed_range(L, kind, storage):
+    assert kkm.KKM_PACKED_FAST_K == kkm.KKM_PACKED_MAX_K == 64
     n, d = 100000, 128
-    for k in (1, 16, fast, fast + 1, 100):
-        mode, _ = kkm.kkm_plan(n, d, k, kind, 1 << 40, kkm.KKM_MODE_AUTO, storage)
-        assert mode == (kkm.KKM_MODE_PACKED if k <= fast else kkm.KKM_MODE_RESIDENT), (kind, storage, k)
+    for k in (1, 16, 33, 64, 65, 100):
+        mode, need = kkm.kkm_plan(n, d, k, kind, 1 << 40, kkm.KKM_MODE_AUTO, storage)
+        assert mode == (kkm.KKM_MODE_PACKED if k <= 64 else kkm.KKM_MODE_RESIDENT), (kind, storage, k)
+        # the linear and polynomial kernels keep a row bound (n fp32) where K is packed or binary16
+        _, need_g = kkm.kkm_plan(n, d, k, kkm.KKM_GAUSS, 1 << 40, mode, storage)
+        scaled = kind != kkm.KKM_GAUSS and (mode == kkm.KKM_MODE_PACKED or storage == kkm.KKM_STORE_F16)
+        assert need - need_g == (4 * n + 256 if scaled else 0), (kind, storage, k)
 
 
 # Each workload's storage mode measured fastest on MI355X (whole job, updates/s):
 # 1: packed (n = 2000, k = 8); 2: packed 3593 vs resident 2810; 3: packed 562 vs
-# resident 372; 4 (k = 64, Gaussian): packed 210 vs resident 157; 5: packed 66.0
-# vs resident 38.8 vs on the fly 36.1.
+# resident 372; 4 (k = 64, Gaussian): packed 228 vs resident 157; 5: packed 70.8
+# vs resident 39.0 vs on the fly 48.2.
 MEASURED_FASTEST = {1: kkm.KKM_MODE_PACKED, 2: kkm.KKM_MODE_PACKED, 3: kkm.KKM_MODE_PACKED,
                     4: kkm.KKM_MODE_PACKED, 5: kkm.KKM_MODE_PACKED}
 

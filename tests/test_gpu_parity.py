@@ -59,7 +59,8 @@ CASES = {
     "k40-n1800-poly": (lambda: datagen.separated_blobs(1800, 6, 40, seed=6, spread=2.5, sigma=1.0)[0],
                        40, "poly", 0.2, 1.0, 2, 23),
     # more than 16 labels above 4096 points: the packed SpMM's 16-tile segments
-    # (ragged last segment), binary16 split column side and fp32 column side
+    # (ragged last segment); the polynomial's rows scaled by powers of two for
+    # the split column side
     "k40-n6000-gauss": (lambda: datagen.make_points(4, n=6000, d=16)[0], 40, "gauss", 0.5, 0.0, 1, 30),
     "k24-n5000-poly": (lambda: datagen.make_points(2, n=5000, d=20)[0], 24, "poly", 0.05, 1.0, 2, 31),
 }
@@ -355,13 +356,12 @@ def test_gauss_fixup_overflow_path(oracle, mode, d):
 
 
 @pytest.mark.parametrize("kind,k_hint,want", [("gauss", 8, "packed"), ("gauss", 40, "packed"),
-                                               ("poly", 32, "packed"), ("poly", 40, "resident"),
+                                               ("poly", 64, "packed"), ("poly", 65, "resident"),
                                                ("gauss", 0, "resident")])
 def test_auto_mode_follows_the_k_hint(oracle, kind, k_hint, want):
-    """AUTO stores K packed when the announced k is at most 64 (Gaussian: the
-    column side on the binary16 matrix cores) or 32 (polynomial: on the fp32
-    ones), and fully otherwise or without a hint (memory allowing); either way
-    the step matches the oracle."""
+    """AUTO stores K packed when the announced k is at most 64 and fully
+    otherwise or without a hint (memory allowing); either way the step
+    matches the oracle."""
     _torch_cuda()
     from paper_2601_17136_amd import kkm
     X = datagen.make_points(2, n=700, d=12)[0]

@@ -68,9 +68,9 @@ def test_workload_step_full_size(oracle, cfg, mode):
 @pytest.mark.parametrize("kind,k", [("poly", 40), ("gauss", 33), ("gauss", 64)])
 def test_many_labels_tall_chunks(oracle, kind, k):
     """More than 16 labels above 40000 points: the packed SpMM's 128-row
-    chunks and 32-tile segments with three or four 16-label blocks, on the
-    fp32 column side (polynomial) and the split binary16 one (Gaussian);
-    checked on sampled rows as above."""
+    chunks and 32-tile segments with three or four 16-label blocks; the
+    polynomial's rows scaled by powers of two for the split column side, the
+    Gaussian's not; checked on sampled rows as above."""
     torch = pytest.importorskip("torch")
     assert torch.cuda.is_available()
     n, d = 45000, 48
