@@ -16,6 +16,18 @@ from paper_2601_17136_amd import datagen
 pytestmark = pytest.mark.gpu
 
 
+def _norm_spread(X, seed):
+    """The points with row norms spread over four decades (10^-3 .. 10 times
+    their own) and one point at the origin: the packed column side's
+    power-of-two row scales then range widely, one row of K is zero (its
+    bound falls back to 1), and the Cauchy-Schwarz bound of a small row is
+    loose against its entries."""
+    rng = np.random.default_rng(seed)
+    Y = (X * 10.0 ** rng.uniform(-3.0, 1.0, size=(X.shape[0], 1))).astype(np.float32)
+    Y[17] = 0.0
+    return Y
+
+
 def _torch_cuda():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
@@ -63,6 +75,11 @@ CASES = {
     # the split column side
     "k40-n6000-gauss": (lambda: datagen.make_points(4, n=6000, d=16)[0], 40, "gauss", 0.5, 0.0, 1, 30),
     "k24-n5000-poly": (lambda: datagen.make_points(2, n=5000, d=20)[0], 24, "poly", 0.05, 1.0, 2, 31),
+    # the row scales of the split column side over widely spread row norms
+    "k33-n5000-linear-spread": (lambda: _norm_spread(datagen.make_points(2, n=5000, d=12)[0], 32),
+                                33, "linear", 1.0, 0.0, 1, 32),
+    "k20-n3000-poly-spread": (lambda: _norm_spread(datagen.make_points(4, n=3000, d=10)[0], 33),
+                              20, "poly", 0.1, 0.5, 3, 33),
 }
 
 

@@ -65,7 +65,7 @@ def test_workload_step_full_size(oracle, cfg, mode):
           flush=True)
 
 
-@pytest.mark.parametrize("kind,k", [("poly", 40), ("gauss", 33), ("gauss", 64)])
+@pytest.mark.parametrize("kind,k", [("poly", 40), ("linear", 20), ("gauss", 33), ("gauss", 64)])
 def test_many_labels_tall_chunks(oracle, kind, k):
     """More than 16 labels above 40000 points: the packed SpMM's 128-row
     chunks and 32-tile segments with three or four 16-label blocks; the
@@ -76,7 +76,7 @@ def test_many_labels_tall_chunks(oracle, kind, k):
     n, d = 45000, 48
     X = datagen.make_points(5, n=n, d=d)[0]
     cl = datagen.random_init(n, k, 40 + k)
-    g, c, p = (1.0 / d, 1.0, 2) if kind == "poly" else (1.0 / d, 0.0, 1)
+    g, c, p = {"poly": (1.0 / d, 1.0, 2), "linear": (1.0, 0.0, 1), "gauss": (1.0 / d, 0.0, 1)}[kind]
     print(f"[gpu] packed, n={n} d={d} k={k} {kind}", flush=True)
     kern = oracle.Kernel(kind, g, c, p)
     rows = _rows(n, k)
