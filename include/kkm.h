@@ -64,7 +64,7 @@ typedef enum kkm_kind { KKM_LINEAR = 0, KKM_POLY = 1, KKM_GAUSS = 2 } kkm_kind;
  * of the symmetric K (row block I of 128 rows keeps columns 128*I ..
  * ld-1, about half the bytes) and streams that: each stored entry K(i,j)
  * serves both E(j, cl(i)) and E(i, cl(j)).  PACKED handles at most
- * KKM_PACKED_MAX_K clusters; it is the fastest mode for small k.  ONTHEFLY
+ * KKM_PACKED_MAX_K clusters and is the fastest mode up to there.  ONTHEFLY
  * never stores K: every iteration recomputes its tiles and folds them
  * straight into E, which is the paper's single-GPU sliding-window baseline
  * (Section VI-D) done tile by tile.  AUTO picks by the memory budget and

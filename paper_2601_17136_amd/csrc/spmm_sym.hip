@@ -10,7 +10,7 @@
 // SpMM.  The column side needs, for every row, its entries summed per label
 // of their column: a product with the one-hot matrix of the column labels,
 // which runs on the matrix cores with 16 labels per block, exact in its
-// products (each is 0 or the entry itself):
+// products (each is 0 or the operand itself):
 //  - binary16 K: v_mfma_f32_16x16x32_f16, 32 columns per instruction;
 //  - fp32 K: each entry v of row r, divided by p_r, a power of two at or
 //    above a bound of |K(r, .)| (1 for the Gaussian, whose entries lie in
@@ -33,7 +33,8 @@
 // Per tile a wavefront
 //  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
 //    contiguous bytes per instruction, one tile ahead in a single register
-//    buffer (a second buffer costs more occupancy than it gains);
+//    buffer (a second one, with the rows' offsets moved to LDS to make room,
+//    measured no faster on the largest problems and slower on smaller ones);
 //  - adds the rows in registers (row side), combines the wavefronts in LDS
 //    and writes the chunk's partial P[q] for the tile;
 //  - stages the block in LDS and reads it back in the MFMA operand layout
@@ -61,12 +62,6 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 
 namespace {
 
-// 90 VGPRs and ~23 KB (NW = 4) or ~45 KB (NW = 8) of LDS per workgroup:
-// 20 or 16 wavefronts per CU.  Six wavefronts per SIMD (80 VGPRs, spilling)
-// measured slower.
-// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
-// binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
-// when a tile is consumed, so everything after the loads is the same.
 // The smallest power of two at or above w, for w up to 2^126 (larger w,
 // infinities and NaN give 2^126; w <= 0 does not occur: the bounds are
 // positive).
@@ -75,6 +70,12 @@ __device__ inline float pow2_at_least(float w) {
   return __uint_as_float((__float_as_uint(w) + 0x007fffffu) & 0x7f800000u);
 }
 
+// 88-128 VGPRs and 25-39 KB (NW = 4) or 59-78 KB (NW = 8) of LDS per
+// workgroup: 16 wavefronts per CU (20 for some binary16 variants).  Six
+// wavefronts per SIMD (80 VGPRs, spilling) measured slower.
+// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
+// binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
+// when a tile is consumed, so everything after the loads is the same.
 template <int NB, int NW, int BSEG, typename KT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const KT* __restrict__ Kp, IterBufs b) {
