@@ -29,7 +29,8 @@ pytestmark = pytest.mark.gpu
 U16 = 2.0 ** -11
 SUB = 2.0 ** -25
 F16_CASES = ["blobs-n2000-poly", "ragged-poly3", "ragged-gauss", "linear-n300", "rings-n3000-gauss", "n129-d1",
-             "stripes-n2100-k1", "d2500-n300", "n2-k2", "k20-n1500-gauss", "k40-n1800-poly"]
+             "stripes-n2100-k1", "d2500-n300", "n2-k2", "k20-n1500-gauss", "k40-n1800-poly",
+             "k40-n6000-gauss", "k24-n5000-poly", "k33-n5000-linear-spread", "k20-n3000-poly-spread"]
 
 
 def row_scales(X, kind, g, c, p):

@@ -30,10 +30,17 @@ def _both(eng, cl0, k, iters, tol):
     return (Va.cpu().numpy(), ita, ha), (Vb.cpu().numpy(), itb, hb)
 
 
+# two calls in a row, the second smaller; the second pair with more than 16
+# labels (the packed SpMM's 16-tile segments and two label blocks)
+SIZES = [((2600, 24, 10, 6, -1.0, 41), (700, 9, 6, 5, 0.0, 42)),
+         ((5000, 12, 24, 4, -1.0, 43), (4500, 12, 20, 3, -1.0, 44))]
+
+
+@pytest.mark.parametrize("sizes", range(len(SIZES)))
 @pytest.mark.parametrize("mode", ["resident", "packed", "onthefly"])
-def test_noalloc_matches_iterate_twice_smaller_second(mode):
+def test_noalloc_matches_iterate_twice_smaller_second(mode, sizes):
     _torch_cuda()
-    for n, d, k, iters, tol, seed in ((2600, 24, 10, 6, -1.0, 41), (700, 9, 6, 5, 0.0, 42)):
+    for n, d, k, iters, tol, seed in SIZES[sizes]:
         X = datagen.make_points(2, n=n, d=d)[0]
         cl0 = datagen.random_init(n, k, seed)
         print(f"[gpu] noalloc {mode} n={n} d={d} k={k} iters={iters} tol={tol}", flush=True)
