@@ -34,23 +34,28 @@ constexpr int kBlk = 256;
 //                          k <= 16   k > 16
 //   n <= kSymTinyN            2         8
 //   n <= kSymSmallN           8        16
-//   n >  kSymSmallN          16        32
+//   n <= kSymLargeN          16        32
+//   n >  kSymLargeN          16        64
 // Small problems need many workgroups to fill the GPU evenly (2000 points,
 // k = 8: 18.8 us per SpMM at S = 8, 11.4 at S = 2).  Longer segments spread
 // each workgroup's start (row addresses far apart in a K of tens of GB) over
 // more tiles, and each workgroup writes k column-side sums per row of its
 // chunk for its segment, which the next kernel reads back: with more labels
-// these partials and the epilogue weigh more against the tiles streamed
-// (200000 points, k = 64, binary16 column side: 17.0 ms per SpMM at S = 8,
-// 15.6 at 16, 13.6 at 32; 20000 points, k = 64: S = 16 beats 8 and 32).
+// these partials and the epilogue weigh more against the tiles streamed.
+// SpMM per launch, binary16 column side, k = 64: 200000 points 17.0 / 15.6 /
+// 13.6 ms at S = 8 / 16 / 32; 100000 points 3.92 ms at S = 32, 3.79 at 64;
+// 60000 points 1.38 ms at S = 32, 2.01 at 64 (too few workgroups: about
+// (n/128)^2 / 2S chunk segments against 512 at a time); 20000 points S = 16
+// beats 8 and 32.  With one label block S = 16 and 32 measured alike.
 // kSymMaxK bounds the one-hot MFMA label blocks (16 labels each) a wavefront
 // carries.
-constexpr int64_t kSymSmallN = 40000, kSymTinyN = 4096;
+constexpr int64_t kSymSmallN = 40000, kSymTinyN = 4096, kSymLargeN = 90000;
 inline int sym_chunk_for(int64_t n) { return n <= kSymSmallN ? 64 : 128; }
 inline int sym_seg_for(int64_t n, int k) {
   if (n <= kSymTinyN) return k <= 16 ? 2 : 8;
   if (n <= kSymSmallN) return k <= 16 ? 8 : 16;
-  return k <= 16 ? 16 : 32;
+  if (n <= kSymLargeN) return k <= 16 ? 16 : 32;
+  return k <= 16 ? 16 : 64;
 }
 constexpr int kSymMaxK = 64;
 constexpr int kSymRedStripe = 256;  // columns per workgroup of the packed reduction

@@ -38,12 +38,14 @@
 //  - adds the rows in registers (row side), combines the wavefronts in LDS
 //    and writes the chunk's partial P[q] for the tile;
 //  - stages the block in LDS and reads it back in the MFMA operand layout
-//    (lane = row, k slot = column) for the column side.  With one label
-//    block the whole block is staged and the next tile's loads are issued
-//    right after, so they are in flight during the multiply.
+//    (lane = row, k slot = column) for the column side.  The whole block is
+//    staged and the next tile's loads are issued right after, so they are in
+//    flight during the multiply.
 // The scatter writes, once per update, the chunks' members in chunk-major
 // order and each column tile's one-hot bits, so a workgroup's prologue is a
-// single round trip of independent loads.  The column-side sums of a row stay
+// single round trip of independent loads.  With one label block the
+// segment's bits are staged in LDS; with more, each tile's are loaded with
+// its entries (the LDS holds the whole staged block instead).  The column-side sums of a row stay
 // in the accumulators for the whole segment and go to Ecp[sg] at the row's
 // chunk-major position; ecol_sum_kernel adds the segments into Ecol at each
 // row's point index, and spmm_reduce_sym_kernel adds them into E^T.  Fixed
@@ -82,11 +84,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   constexpr bool kHalf = sizeof(KT) == 2;
   using BufT = typename std::conditional<kHalf, h4, f4>::type;
   constexpr int R = 16 * NW, NT = 64 * NW;
-  // With one label block the whole 16 x 128 block is staged at once; with
-  // more, the MFMA work per tile is larger and the block goes in two halves,
-  // which keeps the LDS per workgroup (and so the occupancy) down.
   constexpr bool kFull = NB == 1;
-  constexpr int kCh = kFull ? 32 : 16;                   // 16-byte chunks per staged row
+  // With more than one label block each tile's one-hot bits (NB x 256 bytes)
+  // are read from global memory with its entries instead of a whole
+  // segment's being staged in LDS: the LDS then holds the whole staged block,
+  // so the next tile's loads are issued as soon as it is staged, and
+  // segments can be long.
+  constexpr bool kTileMask = NB > 1;
+  constexpr int kCh = kHalf && !kFull ? 16 : 32;          // 16-byte chunks per staged row (fp32 view)
   constexpr int kMw = BSEG * NB * 64;                    // one-hot words of a segment
   constexpr int kMpt = (kMw + NT - 1) / NT;              // ... per thread
   const int nseg = b.nseg;
@@ -114,7 +119,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   const int64_t mbase = (int64_t)Js * NB * 64, mlast = (int64_t)b.nt * NB * 64 - 1;
   unsigned mv[kMpt];
 #pragma unroll
-  for (int m = 0; m < kMpt; ++m) mv[m] = b.mskg[min(mbase + tid + m * NT, mlast)];
+  for (int m = 0; m < kMpt; ++m) mv[m] = kTileMask ? 0u : b.mskg[min(mbase + tid + m * NT, mlast)];
   // Rows are in increasing index order within a chunk, so the first row has
   // the smallest tile; a segment left of it holds nothing of this chunk.
   if (i0 < 0 || i0 / kTile >= Je) return;
@@ -122,7 +127,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   __shared__ int rtile[kFull ? 1 : R];
   __shared__ int64_t roff[kFull ? 1 : R];
   __shared__ float rwl[kHalf && !kFull ? R : 1];  // row scales (binary16, more label blocks)
-  __shared__ unsigned mskl[BSEG][NB][4][16];     // one-hot bits: [tile][label block][k slot][label]
+  __shared__ unsigned mskl[kTileMask ? 1 : BSEG][NB][4][16];  // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
   __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
   __shared__ h4 onehot[16];                      // the 4 bits of a nibble as binary16 0 / 1
@@ -162,7 +167,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     if (kHalf) rwl[tid] = (iv >= 0 && b.kw) ? b.kw[iv] : 1.f;
   }
   const KT* zp = (const KT*)b.zero + 4 * c32;
-  auto load = [&](BufT(&buf)[8], int J) {
+  auto load = [&](BufT(&buf)[8], unsigned(&mk)[NB], int J) {
+    if constexpr (kTileMask) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) mk[nb] = b.mskg[min(((int64_t)J * NB + nb) * 64 + lk * 16 + li, mlast)];
+    }
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int u = w * 16 + 2 * g + h;
@@ -173,7 +182,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   };
 
   BufT bb[8];
-  if (kFull) load(bb, J_lo);  // in flight while the one-hot bits go to LDS
+  unsigned mk[NB];
+  if (kFull) load(bb, mk, J_lo);  // in flight while the one-hot bits go to LDS
   // fp32 K: row u of the chunk is scaled by rsc[u], a power of two, for the
   // column side (exact both ways; read per tile, so it holds no register)
   if (!kHalf && tid < R) {
@@ -183,18 +193,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   if (tid < 16)
     onehot[tid] = h4{(_Float16)(tid & 1), (_Float16)((tid >> 1) & 1), (_Float16)((tid >> 2) & 1),
                      (_Float16)((tid >> 3) & 1)};
+  if constexpr (!kTileMask) {
 #pragma unroll
-  for (int m = 0; m < kMpt; ++m)
-    if (tid + m * NT < kMw) (&mskl[0][0][0][0])[tid + m * NT] = mv[m];
+    for (int m = 0; m < kMpt; ++m)
+      if (tid + m * NT < kMw) (&mskl[0][0][0][0])[tid + m * NT] = mv[m];
+  }
   __syncthreads();
-  if (!kFull) load(bb, J_lo);
+  if (!kFull) load(bb, mk, J_lo);
 
   f4 D[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
   f4* tw = tile[w];
 
-  auto step = [&](BufT(&raw)[8], int J, int par) {
+  auto step = [&](BufT(&raw)[8], unsigned(&mkr)[NB], int J, int par) {
     f4 buf[8];  // the tile's entries in fp32 (binary16: widened and scaled)
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
@@ -214,7 +226,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     const int bi = J - Js;
     unsigned msk[NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) msk[nb] = mskl[bi][nb][lk][li];
+    for (int nb = 0; nb < NB; ++nb) msk[nb] = kTileMask ? mkr[nb] : mskl[kTileMask ? 0 : bi][nb][lk][li];
     const bool diag = rt_first <= J && J <= rt_last;  // some row of the group sits in tile J
     const bool dz = rt_m >= J;
     const bool any = rt_first < J || diag;
@@ -227,13 +239,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     // go to one v_mfma_f32_16x16x32_f16 (k slots 0-3 and 4-7 of each lane;
     // the one-hot operand takes the same order): 32 columns per instruction
     // and label block, exact 0/1 products, fp32 sums.
-    auto mma = [&](int g0, int ng, int cb) {
+    auto mma = [&]() {
       const float ips = rsc[um];
 #pragma unroll
-      for (int gg = 0; gg < ng; gg += 2) {
-        const int g = g0 + gg;
-        f4 v0 = tw[li * kCh + ((4 * (g - cb) + lk) ^ li)];      // row li, columns 16g + 4lk .. +3
-        f4 v1 = tw[li * kCh + ((4 * (g + 1 - cb) + lk) ^ li)];  // ... and 16(g+1) + 4lk .. +3
+      for (int g = 0; g < 8; g += 2) {
+        f4 v0 = tw[li * 32 + ((4 * g + lk) ^ li)];      // row li, columns 16g + 4lk .. +3
+        f4 v1 = tw[li * 32 + ((4 * g + 4 + lk) ^ li)];  // ... and 16(g+1) + 4lk .. +3
         if (diag && dz) v0 = v1 = f4{0.f, 0.f, 0.f, 0.f};
         v0 *= ips;
         v1 *= ips;
@@ -266,7 +277,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
         th[r * 32 + (c32 ^ (2 * r))] = raw[g];
       }
       __builtin_amdgcn_sched_barrier(0);
-      load(raw, J + 1);
+      load(raw, mkr, J + 1);
       __builtin_amdgcn_sched_barrier(0);
       if (any) {
 #pragma unroll
@@ -283,33 +294,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
           }
         }
       }
-    } else if (kFull) {
+    } else {
 #pragma unroll
       for (int g = 0; g < 8; ++g) {
         const int r = 2 * g + h;
         tw[r * 32 + (c32 ^ r)] = buf[g];
       }
       __builtin_amdgcn_sched_barrier(0);
-      load(raw, J + 1);
+      load(raw, mkr, J + 1);
       __builtin_amdgcn_sched_barrier(0);
-      if (any) mma(0, 8, 0);
-    } else {
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        if ((c32 >> 4) == half) {
-#pragma unroll
-          for (int g = 0; g < 8; ++g) {
-            const int r = 2 * g + h;
-            tw[r * 16 + ((c32 & 15) ^ r)] = buf[g];
-          }
-        }
-        if (half == 1) {
-          __builtin_amdgcn_sched_barrier(0);
-          load(raw, J + 1);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        if (any) mma(4 * half, 4, 4 * half);
-      }
+      if (any) mma();
     }
 
     // row side across the wavefronts -> P[q], columns of tile J
@@ -324,7 +318,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     }
   };
 
-  for (int J = J_lo; J < J_hi; ++J) step(bb, J, (J - J_lo) & 1);
+  for (int J = J_lo; J < J_hi; ++J) step(bb, mk, J, (J - J_lo) & 1);
 
   // D[nb][r]: label 16nb + 4lk + r of row um, at its chunk-major position
   // (binary16 on the matrix path: sums of the stored values, times the row's scale)
@@ -474,15 +468,21 @@ hipError_t launch_spmm_sym(const void* Kp, const IterBufs& b, hipStream_t s) {
   // the segment lengths sym_seg_for sets
   const bool tall = b.chunk_len == 128;
   const int lo = nb == 1 ? 2 : 8, hi = nb == 1 ? 8 : 16;  // short chunks: the two smaller lengths
-  if (tall ? b.bseg != 2 * hi : b.bseg != lo && b.bseg != hi) return hipErrorInvalidValue;
-#define KKM_SYM_CASE(NB, LO, HI)                          \
-  do {                                                    \
-    if (tall) KKM_SYM_LAUNCH(NB, 8, 2 * HI);              \
-    else if (b.bseg == LO) KKM_SYM_LAUNCH(NB, 4, LO);     \
-    else KKM_SYM_LAUNCH(NB, 4, HI);                       \
+  const bool ok = tall ? (nb == 1 ? b.bseg == 16 : b.bseg == 32 || b.bseg == 64) : b.bseg == lo || b.bseg == hi;
+  if (!ok) return hipErrorInvalidValue;
+#define KKM_SYM_CASE(NB, LO, HI)                                         \
+  do {                                                                   \
+    if (tall && b.bseg == 64) KKM_SYM_LAUNCH(NB, 8, 64);                 \
+    else if (tall) KKM_SYM_LAUNCH(NB, 8, 2 * HI);                        \
+    else if (b.bseg == LO) KKM_SYM_LAUNCH(NB, 4, LO);                    \
+    else KKM_SYM_LAUNCH(NB, 4, HI);                                      \
   } while (0)
   switch (nb) {
-    case 1: KKM_SYM_CASE(1, 2, 8); break;
+    case 1:
+      if (tall) KKM_SYM_LAUNCH(1, 8, 16);
+      else if (b.bseg == 2) KKM_SYM_LAUNCH(1, 4, 2);
+      else KKM_SYM_LAUNCH(1, 4, 8);
+      break;
     case 2: KKM_SYM_CASE(2, 8, 16); break;
     case 3: KKM_SYM_CASE(3, 8, 16); break;
     case 4: KKM_SYM_CASE(4, 8, 16); break;
