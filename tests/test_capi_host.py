@@ -149,8 +149,8 @@ def test_plan_auto_packed_range(L, kind, storage):
 
 # Each workload's storage mode measured fastest on MI355X (whole job, updates/s):
 # 1: packed (n = 2000, k = 8); 2: packed 3593 vs resident 2810; 3: packed 562 vs
-# resident 372; 4 (k = 64, Gaussian): packed 228 vs resident 157; 5: packed 70.8
-# vs resident 39.0 vs on the fly 48.2.
+# resident 372; 4 (k = 64, Gaussian): packed 235 vs resident 157; 5: packed 70.8
+# vs resident 39.5 vs on the fly 48.7.
 MEASURED_FASTEST = {1: kkm.KKM_MODE_PACKED, 2: kkm.KKM_MODE_PACKED, 3: kkm.KKM_MODE_PACKED,
                     4: kkm.KKM_MODE_PACKED, 5: kkm.KKM_MODE_PACKED}
 
