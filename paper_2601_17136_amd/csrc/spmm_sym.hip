@@ -91,7 +91,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   // so the next tile's loads are issued as soon as it is staged, and
   // segments can be long.
   constexpr bool kTileMask = NB > 1;
-  constexpr int kCh = kHalf && !kFull ? 16 : 32;          // 16-byte chunks per staged row (fp32 view)
+  constexpr int kCh = kHalf ? 16 : 32;                   // 16-byte chunks per staged row
   constexpr int kMw = BSEG * NB * 64;                    // one-hot words of a segment
   constexpr int kMpt = (kMw + NT - 1) / NT;              // ... per thread
   const int nseg = b.nseg;
@@ -104,9 +104,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   // Everything the workgroup needs is read in one round trip: the chunk's
   // rows by point index from the scatter's chunk-major table (-1 past the
-  // chunk's end and at the start of an unused chunk), and the segment's
-  // one-hot bits (bit 4g+e of [tile][nb][lk][li]: column 16g + 4lk + e of the
-  // tile has label 16nb + li).
+  // chunk's end and at the start of an unused chunk), and with one label
+  // block the segment's one-hot bits (bit 4g+e of [tile][nb][lk][li]: column
+  // 16g + 4lk + e of the tile has label 16nb + li).
   const int* cr = b.crow + (int64_t)q * R;
   const int i0 = cr[0];
   const int um = w * 16 + li;  // this lane's row in the MFMA layout
