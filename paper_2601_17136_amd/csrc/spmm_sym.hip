@@ -30,17 +30,17 @@
 // Workgroup (chunk q, segment sg): NW wavefronts (4 or 8), one 16-row group
 // each, over the column tiles of segment sg (BSEG tiles) that the chunk's
 // rows store.
-// Per tile a wavefront
-//  - streams its 16 rows x 128 columns with 16-byte loads, two rows of 512
-//    contiguous bytes per instruction, one tile ahead in a single register
-//    buffer (a second one, with the rows' offsets moved to LDS to make room,
-//    measured no faster on the largest problems and slower on smaller ones);
+// Per step (one tile of fp32 K, two of binary16) a wavefront
+//  - streams its 16 rows with 16-byte loads, two rows of 512 contiguous
+//    bytes per instruction, one step ahead in a single register buffer (a
+//    second one, with the rows' offsets moved to LDS to make room, measured
+//    no faster on the largest problems and slower on smaller ones);
 //  - adds the rows in registers (row side), combines the wavefronts in LDS
-//    and writes the chunk's partial P[q] for the tile;
-//  - stages the block in LDS and reads it back in the MFMA operand layout
-//    (lane = row, k slot = column) for the column side.  The whole block is
-//    staged and the next tile's loads are issued right after, so they are in
-//    flight during the multiply.
+//    and writes the chunk's partial P[q] for the step's columns;
+//  - stages each block in LDS and reads it back in the MFMA operand layout
+//    (lane = row, k slot = column) for the column side.  The next step's
+//    loads are issued once the step's last block is staged, so they are in
+//    flight during its multiply.
 // The scatter writes, once per update, the chunks' members in chunk-major
 // order and each column tile's one-hot bits, so a workgroup's prologue is a
 // single round trip of independent loads.  With one label block the
@@ -72,19 +72,26 @@ __device__ inline float pow2_at_least(float w) {
   return __uint_as_float((__float_as_uint(w) + 0x007fffffu) & 0x7f800000u);
 }
 
-// 88-128 VGPRs and 25-39 KB (NW = 4) or 59-78 KB (NW = 8) of LDS per
-// workgroup: 16 wavefronts per CU (20 for some binary16 variants).  Six
-// wavefronts per SIMD (80 VGPRs, spilling) measured slower.
-// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1);
-// binary16 rows are read 4 entries (8 bytes) per lane and widened and scaled
-// when a tile is consumed, so everything after the loads is the same.
+// 102-128 VGPRs and 25-39 KB (NW = 4) or 50-78 KB (NW = 8) of LDS per
+// workgroup: 16 wavefronts per CU.  Six wavefronts per SIMD (80 VGPRs,
+// spilling) measured slower.
+// KT: float, or binary16 with row r's entries divided by kw[r] (kw null: 1),
+// widened and scaled in the row side; the column side scales the row's sums
+// once at the end.
 template <int NB, int NW, int BSEG, typename KT>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void spmm_sym_kernel(
     const KT* __restrict__ Kp, IterBufs b) {
   constexpr bool kHalf = sizeof(KT) == 2;
-  using BufT = typename std::conditional<kHalf, h4, f4>::type;
+  using BufT = typename std::conditional<kHalf, h8, f4>::type;  // a lane's 16 bytes of a row
   constexpr int R = 16 * NW, NT = 64 * NW;
-  constexpr bool kFull = NB == 1;
+  // binary16: a step takes two tiles, read 8 entries (16 bytes) per lane
+  // like fp32's 4, so an instruction reads two rows of 512 contiguous bytes;
+  // its rows come from the LDS row table
+  constexpr bool kPair = kHalf;
+  constexpr bool kFull = NB == 1 && !kPair;
+  constexpr int kTps = kPair ? 2 : 1;           // tiles per step
+  constexpr int kStepCols = kTps * kTile;       // columns of P per step
+  constexpr int kLc = 16 / (int)sizeof(KT);     // entries per lane and row
   // With more than one label block each tile's one-hot bits (NB x 256 bytes)
   // are read from global memory with its entries instead of a whole
   // segment's being staged in LDS: the LDS then holds the whole staged block,
@@ -126,10 +133,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 
   __shared__ int rtile[kFull ? 1 : R];
   __shared__ int64_t roff[kFull ? 1 : R];
-  __shared__ float rwl[kHalf && !kFull ? R : 1];  // row scales (binary16, more label blocks)
+  __shared__ float rwl[kHalf ? R : 1];           // row scales (binary16)
   __shared__ unsigned mskl[kTileMask ? 1 : BSEG][NB][4][16];  // one-hot bits: [tile][label block][k slot][label]
   __shared__ f4 tile[NW][16 * kCh];              // per wavefront: 16 rows x kCh chunks of 16 B
-  __shared__ f4 red[2][NW][32];                  // row-side sums of the wavefronts
+  __shared__ f4 red[2][NW][kStepCols / 4];       // row-side sums of the wavefronts
   __shared__ h4 onehot[16];                      // the 4 bits of a nibble as binary16 0 / 1
   __shared__ float rsc[kHalf ? 1 : R];           // fp32 K: the rows' column-side scales
 
@@ -166,23 +173,30 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
     roff[tid] = iv >= 0 ? packed_row(iv, ld) : 0;
     if (kHalf) rwl[tid] = (iv >= 0 && b.kw) ? b.kw[iv] : 1.f;
   }
-  const KT* zp = (const KT*)b.zero + 4 * c32;
-  auto load = [&](BufT(&buf)[8], unsigned(&mk)[NB], int J) {
+  const KT* zp = (const KT*)b.zero + kLc * c32;
+  // the step's rows at lane column kLc * c32 from tile J (binary16: lanes
+  // c32 < 16 in tile J, the others in J + 1), and with more label blocks
+  // the tiles' one-hot bits
+  auto load = [&](BufT(&buf)[8], unsigned(&mk)[kTps][NB], int J) {
     if constexpr (kTileMask) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) mk[nb] = b.mskg[min(((int64_t)J * NB + nb) * 64 + lk * 16 + li, mlast)];
+      for (int t = 0; t < kTps; ++t)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          mk[t][nb] = b.mskg[min(((int64_t)(J + t) * NB + nb) * 64 + lk * 16 + li, mlast)];
     }
+    const int jt = kPair ? J + (c32 >> 4) : J;  // this lane's tile
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       const int u = w * 16 + 2 * g + h;
-      const bool on = (kFull ? rt[g] : rtile[u]) <= J && J < J_hi;
-      const KT* rp = kFull ? rbase[g] + (int64_t)J * kTile : Kp + roff[u] + (int64_t)J * kTile + 4 * c32;
+      const bool on = (kFull ? rt[g] : rtile[u]) <= jt && jt < J_hi;
+      const KT* rp = kFull ? rbase[g] + (int64_t)J * kTile : Kp + roff[u] + (int64_t)J * kTile + kLc * c32;
       buf[g] = __builtin_nontemporal_load((const BufT*)(on ? rp : zp));
     }
   };
 
   BufT bb[8];
-  unsigned mk[NB];
+  unsigned mk[kTps][NB];
   if (kFull) load(bb, mk, J_lo);  // in flight while the one-hot bits go to LDS
   // fp32 K: row u of the chunk is scaled by rsc[u], a power of two, for the
   // column side (exact both ways; read per tile, so it holds no register)
@@ -206,40 +220,85 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
   for (int nb = 0; nb < NB; ++nb) D[nb] = f4{0.f, 0.f, 0.f, 0.f};
   f4* tw = tile[w];
 
-  auto step = [&](BufT(&raw)[8], unsigned(&mkr)[NB], int J, int par) {
-    f4 buf[8];  // the tile's entries in fp32 (binary16: widened and scaled)
+  // row side: this lane's columns over its 8 rows, then the other
+  // half-wave's 8 (binary16: widened and scaled by the row); rs[t] holds
+  // columns kLc * c32 + 4t .. +3 of the step
+  auto rowsum = [&](const BufT(&raw)[8], f4(&rs)[kTps]) {
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
-      if constexpr (kHalf)
-        buf[g] = __builtin_convertvector(raw[g], f4) * (kFull ? rwt[g] : rwl[w * 16 + 2 * g + h]);
-      else
-        buf[g] = raw[g];
+#pragma unroll
+      for (int t = 0; t < kTps; ++t) {
+        f4 v;
+        if constexpr (kHalf) {
+          const h4 x = t == 0 ? __builtin_shufflevector(raw[g], raw[g], 0, 1, 2, 3)
+                              : __builtin_shufflevector(raw[g], raw[g], 4, 5, 6, 7);
+          v = __builtin_convertvector(x, f4) * (kFull ? rwt[g] : rwl[w * 16 + 2 * g + h]);
+        } else {
+          v = raw[g];
+        }
+        rs[t] = g == 0 ? v : rs[t] + v;
+      }
     }
-    // row side: this lane's 4 columns over its 8 rows, then the other half-wave's 8
-    f4 rs = buf[0];
 #pragma unroll
-    for (int g = 1; g < 8; ++g) rs += buf[g];
+    for (int t = 0; t < kTps; ++t)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) rs[e] += __shfl_xor(rs[e], 32, 64);
+      for (int e = 0; e < 4; ++e) rs[t][e] += __shfl_xor(rs[t][e], 32, 64);
+  };
+  // tile J's one-hot bits (J inside the segment)
+  auto bits = [&](unsigned(&msk)[NB], const unsigned(&mkr)[NB], int J) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) msk[nb] = kTileMask ? mkr[nb] : mskl[kTileMask ? 0 : J - Js][nb][lk][li];
+  };
+  // Column side of tile J for the group: entries right of each row's own
+  // diagonal tile.  diag: some row of the group sits in tile J; dz: this
+  // lane's row sits in tile J or right of it (its entries there are row side
+  // only); any: the group has column-side entries in tile J (wavefront-uniform).
+  auto diag_at = [&](int J) { return rt_first <= J && J <= rt_last; };
+  auto any_at = [&](int J) { return rt_first < J || diag_at(J); };
+  // The row side across the wavefronts -> P[q]: each wavefront's sums to
+  // its slot, then the step's columns from tile J (ncols of them are
+  // written; the rest belong to the next segment).
+  auto put_rows = [&](const f4(&rs)[kTps], int par) {
+    if (h == 0)
+#pragma unroll
+      for (int t = 0; t < kTps; ++t) red[par][w][kTps * c32 + t] = rs[t];
+  };
+  auto combine = [&](int J, int par, int ncols) {
+    __syncthreads();
+    if (tid < ncols) {
+      const float* rr = (const float*)red[par];
+      float t = rr[tid];
+#pragma unroll
+      for (int ww = 1; ww < NW; ++ww) t += rr[ww * kStepCols + tid];
+      b.P[(int64_t)q * ld + (int64_t)J * kTile + tid] = t;
+    }
+  };
 
-    // column side: entries right of the row's own diagonal tile
-    const int bi = J - Js;
+  // fp32 K, one tile per step.  The block is staged in LDS (chunk index xor
+  // row keeps both the row-wise writes and the MFMA-layout reads
+  // conflict-free) and read back in the MFMA operand layout.  The next
+  // tile's loads are issued as soon as the whole block is staged, so they
+  // are in flight while it is multiplied.  The row's entries (scaled into
+  // [-1, 1]) go in as a sum of two binary16 values (hi, and the rest
+  // rounded).  Column groups g and g + 1 go to one v_mfma_f32_16x16x32_f16
+  // (k slots 0-3 and 4-7 of each lane; the one-hot operand takes the same
+  // order): 32 columns per instruction and label block, exact 0/1 products,
+  // fp32 sums.
+  auto step = [&](auto& raw, auto& mkr, int J, int par) {  // (generic: instantiated for fp32 only)
+    f4 rs[kTps];
+    rowsum(raw, rs);
     unsigned msk[NB];
+    bits(msk, mkr[0], J);
+    const bool diag = diag_at(J), dz = rt_m >= J;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) msk[nb] = kTileMask ? mkr[nb] : mskl[kTileMask ? 0 : bi][nb][lk][li];
-    const bool diag = rt_first <= J && J <= rt_last;  // some row of the group sits in tile J
-    const bool dz = rt_m >= J;
-    const bool any = rt_first < J || diag;
-    // The block is staged in LDS (chunk index xor row keeps both the row-wise
-    // writes and the MFMA-layout reads conflict-free) and read back in the
-    // MFMA operand layout.  The next tile's loads are issued as soon as the
-    // whole block is staged, so they are in flight while it is multiplied.
-    // fp32 K: the row's entries (scaled into [-1, 1]) as a sum of two
-    // binary16 values (hi, and the rest rounded).  Column groups g and g + 1
-    // go to one v_mfma_f32_16x16x32_f16 (k slots 0-3 and 4-7 of each lane;
-    // the one-hot operand takes the same order): 32 columns per instruction
-    // and label block, exact 0/1 products, fp32 sums.
-    auto mma = [&]() {
+    for (int g = 0; g < 8; ++g) {
+      const int r = 2 * g + h;
+      tw[r * 32 + (c32 ^ r)] = raw[g];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    load(raw, mkr, J + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (any_at(J)) {
       const float ips = rsc[um];
 #pragma unroll
       for (int g = 0; g < 8; g += 2) {
@@ -261,64 +320,76 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
           D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, lo, D[nb], 0, 0, 0);
         }
       }
-    };
-    if constexpr (kHalf) {
-      // binary16: the raw halves of the whole block are staged (4 KB per
-      // wavefront; 8-byte chunk c of row r at c ^ 2r, conflict-free for the
-      // row-wise writes and for the operand reads, which LDS serves 32 lanes
-      // at a time) and the column side runs on v_mfma_f32_16x16x32_f16: 32
-      // columns per instruction and label block, the one-hot operand from a
-      // table of the 16 nibbles; the products are exact and the sums fp32,
-      // and the row's scale is applied at the end.
-      h4* th = (h4*)tw;
-#pragma unroll
-      for (int g = 0; g < 8; ++g) {
-        const int r = 2 * g + h;
-        th[r * 32 + (c32 ^ (2 * r))] = raw[g];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      load(raw, mkr, J + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (any) {
-#pragma unroll
-        for (int g = 0; g < 8; g += 2) {  // column groups g and g + 1 per instruction
-          const h4 v0 = th[li * 32 + ((4 * g + lk) ^ (2 * li))];  // row li, columns 16g + 4lk .. +3
-          const h4 v1 = th[li * 32 + ((4 * g + 4 + lk) ^ (2 * li))];
-          h8 v = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-          if (diag && dz) v = h8{0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
-                                                 onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
-            D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, v, D[nb], 0, 0, 0);
-          }
-        }
-      }
-    } else {
-#pragma unroll
-      for (int g = 0; g < 8; ++g) {
-        const int r = 2 * g + h;
-        tw[r * 32 + (c32 ^ r)] = buf[g];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      load(raw, mkr, J + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (any) mma();
     }
-
-    // row side across the wavefronts -> P[q], columns of tile J
-    if (h == 0) red[par][w][c32] = rs;
-    __syncthreads();
-    if (tid < kTile) {
-      const float* rr = (const float*)red[par];
-      float t = rr[tid];
-#pragma unroll
-      for (int ww = 1; ww < NW; ++ww) t += rr[ww * kTile + tid];
-      b.P[(int64_t)q * ld + (int64_t)J * kTile + tid] = t;
-    }
+    put_rows(rs, par);
+    combine(J, par, kTile);
   };
 
-  for (int J = J_lo; J < J_hi; ++J) step(bb, mk, J, (J - J_lo) & 1);
+  // binary16 K: a step's two blocks go through the wavefront's staging area
+  // in turn (4 KB; 8-byte chunk c of row r at c ^ 2r, conflict-free for the
+  // row-wise writes and for the operand reads, which LDS serves 32 lanes at a
+  // time; a wavefront's LDS accesses are carried out in order, so the second
+  // block's writes follow the first block's reads), and the column side runs
+  // on v_mfma_f32_16x16x32_f16: 32 columns per instruction and label block,
+  // the one-hot operand from a table of the 16 nibbles; the products are
+  // exact and the sums fp32, and the row's scale is applied at the end.  The
+  // next step's loads are issued once the second block is staged, and the
+  // row sums go to LDS as soon as they are formed (the previous step's
+  // barrier ended the reads of their slot), so they hold no registers.
+  auto stage16 = [&](const BufT(&raw)[8], int t) {  // the block of tile J + t
+    if constexpr (kPair) {
+      if ((c32 >> 4) != t) return;
+      h8* th = (h8*)tw;
+      const int cc = c32 & 15;  // chunks 2cc, 2cc + 1 of the block's row
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        const int r = 2 * g + h;
+        th[r * 16 + (cc ^ r)] = raw[g];
+      }
+    }
+  };
+  auto mma16 = [&](int J, const unsigned(&msk)[NB]) {
+    const bool diag = diag_at(J), dz = rt_m >= J;
+    const h4* th = (const h4*)tw;
+#pragma unroll
+    for (int g = 0; g < 8; g += 2) {  // column groups g and g + 1 per instruction
+      const h4 v0 = th[li * 32 + ((4 * g + lk) ^ (2 * li))];  // row li, columns 16g + 4lk .. +3
+      const h4 v1 = th[li * 32 + ((4 * g + 4 + lk) ^ (2 * li))];
+      h8 v = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+      if (diag && dz) v = h8{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const h8 a = __builtin_shufflevector(onehot[(msk[nb] >> (4 * g)) & 15u],
+                                             onehot[(msk[nb] >> (4 * g + 4)) & 15u], 0, 1, 2, 3, 4, 5, 6, 7);
+        D[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, v, D[nb], 0, 0, 0);
+      }
+    }
+  };
+  auto step2 = [&](auto J, int par) {  // (generic: instantiated for binary16 only)
+    const bool two = J + 1 < J_hi;    // tile J + 1 is in the segment
+    {
+      f4 rs[kTps];
+      rowsum(bb, rs);
+      put_rows(rs, par);
+    }
+    unsigned msk[NB];
+    bits(msk, mk[0], J);
+    stage16(bb, 0);
+    if (any_at(J)) mma16(J, msk);
+    bits(msk, mk[kTps - 1], two ? J + 1 : J);
+    stage16(bb, kTps - 1);
+    __builtin_amdgcn_sched_barrier(0);
+    load(bb, mk, J + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    if (two && any_at(J + 1)) mma16(J + 1, msk);
+    combine(J, par, two ? 2 * kTile : kTile);
+  };
+
+  if constexpr (kPair) {
+    for (int J = J_lo; J < J_hi; J += 2) step2(J, ((J - J_lo) >> 1) & 1);
+  } else {
+    for (int J = J_lo; J < J_hi; ++J) step(bb, mk, J, (J - J_lo) & 1);
+  }
 
   // D[nb][r]: label 16nb + 4lk + r of row um, at its chunk-major position
   // (binary16 on the matrix path: sums of the stored values, times the row's scale)
