@@ -118,8 +118,8 @@ struct IterBufs {
   int* status;          // 1: bit 0 = id out of range
   // packed K only
   int nt, nseg, bseg;   // column tiles (ld / kTile); column segments of bseg tiles
-  float* Ecp;           // nseg x k x (qmax * chunk_len): column-side partials per segment,
-                        // at chunk-major positions (member t of chunk q at q * chunk_len + t)
+  float* Ecp;           // nseg x qmax x k x chunk_len: column-side partials per segment and
+                        // chunk, label-major (member t of chunk q, label j at j * chunk_len + t)
   float* Ecol;          // k x n: column-side sums, by point index
   int* chunk_c0;        // qmax: first stored column of each chunk (its first row's tile
                         // start), written by the scatter; null when K is not packed

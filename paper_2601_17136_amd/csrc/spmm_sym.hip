@@ -45,11 +45,12 @@
 // order and each column tile's one-hot bits, so a workgroup's prologue is a
 // single round trip of independent loads.  With one label block the
 // segment's bits are staged in LDS; with more, each tile's are loaded with
-// its entries (the LDS holds the whole staged block instead).  The column-side sums of a row stay
-// in the accumulators for the whole segment and go to Ecp[sg] at the row's
-// chunk-major position; ecol_sum_kernel adds the segments into Ecol at each
-// row's point index, and spmm_reduce_sym_kernel adds them into E^T.  Fixed
-// orders throughout, so the result is bitwise reproducible.
+// its entries (the LDS holds the whole staged block instead).  The
+// column-side sums of a row stay in the accumulators for the whole segment
+// and go to the workgroup's contiguous k x R block of Ecp (label-major, rows
+// at their chunk positions); ecol_sum_kernel adds the segments into Ecol at
+// each row's point index, and spmm_reduce_sym_kernel adds them into E^T.
+// Fixed orders throughout, so the result is bitwise reproducible.
 #include "kkm_internal.h"
 
 #include <algorithm>
@@ -403,14 +404,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) vo
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) D[nb] *= ps;
   }
-  const int64_t ecs = (int64_t)b.qmax * R;
+  // the workgroup's k x R block of Ecp is contiguous
+  float* ep = b.Ecp + ((int64_t)sg * b.qmax + q) * b.k * R + um;
   if (im >= 0)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int lab = 16 * nb + 4 * lk + r;
-        if (lab < b.k) b.Ecp[((int64_t)sg * b.k + lab) * ecs + (int64_t)q * R + um] = D[nb][r];
+        if (lab < b.k) ep[lab * R] = D[nb][r];
       }
 }
 
@@ -427,8 +429,8 @@ __global__ __launch_bounds__(256) void ecol_sum_kernel(IterBufs b) {
   const int i0 = cr[0], row = cr[u];
   if (i0 < 0 || j >= b.k || row < 0) return;
   const int s0 = i0 / kTile / b.bseg, last = b.nseg - 1;
-  const int64_t ecs = (int64_t)b.qmax * cl, seg_stride = (int64_t)b.k * ecs;
-  const float* e = b.Ecp + (int64_t)j * ecs + (int64_t)q * cl + u;
+  const int64_t seg_stride = (int64_t)b.qmax * b.k * cl;
+  const float* e = b.Ecp + ((int64_t)q * b.k + j) * cl + u;  // = chunk q's block + t
   float acc = 0.f;
   for (int sg = s0; sg <= last; sg += 8) {  // eight loads in flight, added in order
     float v[8];
