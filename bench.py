@@ -128,7 +128,8 @@ def parse():
                          "of K (n/Q x n/Q), its build and its updates, without the exchanges")
     ap.add_argument("--peaks", action="store_true",
                     help="measure the achievable peaks instead (16 GiB non-temporal streaming read and "
-                         "write, fp32 MFMA register loop) and print them as one JSON line")
+                         "write, fp32 MFMA register loop, the packed SpMM's load pattern alone over 80 GB) "
+                         "and print them as one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB (a known-size "
                          "reference for memory-traffic counters)")
@@ -407,12 +408,30 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+ROWS_CHUNKS, ROWS_SEGS, ROWS_SEG = 1562, 49, 2048   # 199936 x 100352 fp32 = 80.3 GB
+
+
+def peak_row_orders(nrows, seed=5):
+    """Row tables for the row-pattern read: cluster-sorted (k = 7 random labels,
+    members in index order, cut into 128-row chunks that may straddle two
+    clusters), random, and consecutive."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    lab = rng.integers(0, 7, nrows)
+    return {"cluster_sorted_k7": np.lexsort((np.arange(nrows), lab)).astype(np.int32),
+            "random": rng.permutation(nrows).astype(np.int32),
+            "consecutive": np.arange(nrows, dtype=np.int32)}
+
+
 def peaks_main(kkm, torch):
     """What this GPU sustains, for the roofline fractions against measured peaks:
     a 16 GiB streaming read and write with non-temporal 16-byte accesses, and a
     register loop of v_mfma_f32_32x32x2_f32 (about 18 ms per launch, long enough
-    for the clocks to settle).  One warm-up launch each, then the average of 5."""
+    for the clocks to settle); then the packed SpMM's load pattern alone over an
+    80 GB matrix (workload 5's footprint) in three row orders.  One warm-up
+    launch each, then the average of 5."""
     ctx = kkm.kkm_create(kkm.current_stream_handle())
+    rows_res = {}
     try:
         buf = torch.empty(4 << 30, dtype=torch.float32, device="cuda")   # 16 GiB
         sums = torch.zeros(kkm.PEAK_READ_GROUPS, dtype=torch.float32, device="cuda")
@@ -426,6 +445,19 @@ def peaks_main(kkm, torch):
         out = torch.zeros(4096, dtype=torch.float32, device="cuda")
         kkm.kkm_peak_mfma(ctx, 40000, out, 1)
         m_ms, flops = kkm.kkm_peak_mfma(ctx, 40000, out, 5)
+        A = torch.empty((ROWS_CHUNKS * 128, ROWS_SEGS * ROWS_SEG), dtype=torch.float32, device="cuda")
+        kkm.kkm_peak_write(ctx, A, 1.0, 1)
+        rsums = torch.zeros(ROWS_CHUNKS * ROWS_SEGS, dtype=torch.float32, device="cuda")
+        for name, order in peak_row_orders(A.shape[0]).items():
+            R = torch.from_numpy(order).cuda()
+            kkm.kkm_peak_read_rows(ctx, A, R, ROWS_SEG, rsums, 1)
+            ms = kkm.kkm_peak_read_rows(ctx, A, R, ROWS_SEG, rsums, 5)
+            gbs = A.numel() * 4 / (ms * 1e-3) / 1e9
+            rows_res[name] = {"GBps": round(gbs, 1), "frac_of_8TBps": round(gbs / 8e3, 4), "ms": round(ms, 4),
+                              "sums_exact": bool((rsums == 128.0 * ROWS_SEG).all())}
+            print(f"bench: row-pattern read, {name}: {gbs:.1f} GB/s", file=sys.stderr, flush=True)
+        rows_bytes = A.numel() * 4
+        del A
     finally:
         kkm.kkm_destroy(ctx)
     res = {"metric": "achievable peaks (measurement aids, not the clustering path)",
@@ -435,7 +467,9 @@ def peaks_main(kkm, torch):
            "write_frac_of_8TBps": round(nbytes / (w_ms * 1e-3) / 8e12, 4),
            "mfma_frac_of_157.3TF": round(flops / (m_ms * 1e-3) / 157.3e12, 4),
            "bytes": nbytes, "read_ms": round(r_ms, 4), "write_ms": round(w_ms, 4), "mfma_ms": round(m_ms, 4),
-           "mfma_flop_per_launch": flops, "read_sums_exact": read_ok}
+           "mfma_flop_per_launch": flops, "read_sums_exact": read_ok,
+           "row_pattern_read": {"bytes": rows_bytes, "rows": ROWS_CHUNKS * 128, "ld": ROWS_SEGS * ROWS_SEG,
+                                "segment_floats": ROWS_SEG, "orders": rows_res}}
     print(json.dumps(res), flush=True)
 
 

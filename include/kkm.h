@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KKM_ABI_VERSION 7
+#define KKM_ABI_VERSION 8
 #define KKM_MAX_K 1024 /* largest supported cluster count */
 
 typedef enum kkm_status {
@@ -451,12 +451,26 @@ int kkm_get_info(kkm_ctx *ctx, kkm_info *out);
  *    of the values it read to sums[g] (device, at least 2040 floats), so
  *    the loads cannot be elided and the caller can check them.
  *  - kkm_peak_write: non-temporal 16-byte stores of `value` over buf.
+ *  - kkm_peak_read_rows: the packed SpMM's load pattern without its
+ *    arithmetic, so its rate can be stated against what the pattern itself
+ *    sustains.  buf (device) is an nrows x ld fp32 matrix, row-major (ld a
+ *    multiple of 4, at least 128); rows (device) holds nchunks x 128 row
+ *    indices, clamped into [0, nrows) when read.  Workgroup (c, s), for
+ *    c < nchunks and s < ld / seg (seg a multiple of 128, at most ld), reads
+ *    rows rows[128c .. 128c + 127] over columns [s*seg, (s+1)*seg): eight
+ *    wavefronts of 16 rows, each step 128 columns of its rows with
+ *    non-temporal 16-byte loads (two rows of 512 contiguous bytes per
+ *    instruction), one step in flight per wavefront.  It writes the fp32
+ *    sum of what it read to sums[c * (ld / seg) + s] (device, that many
+ *    floats).  Bytes read per launch: nchunks * 128 * (ld / seg) * seg * 4.
  *  - kkm_peak_mfma: four independent chains of v_mfma_f32_32x32x2_f32 per
  *    wavefront, `iters` instructions each, 1024 workgroups of four
  *    wavefronts; one float per wavefront to out (device, at least 4096
  *    floats); *flops_out (host) = the fp32 matrix flop of one launch. */
 int kkm_peak_read(kkm_ctx *ctx, const void *buf, size_t bytes, float *sums, int32_t reps, float *ms_out);
 int kkm_peak_write(kkm_ctx *ctx, void *buf, size_t bytes, float value, int32_t reps, float *ms_out);
+int kkm_peak_read_rows(kkm_ctx *ctx, const void *buf, int64_t nrows, int64_t ld, const int32_t *rows,
+                       int32_t nchunks, int32_t seg, float *sums, int32_t reps, float *ms_out);
 int kkm_peak_mfma(kkm_ctx *ctx, int32_t iters, float *out, int32_t reps, float *ms_out, double *flops_out);
 
 int kkm_abi_version(void);

@@ -1446,6 +1446,22 @@ int kkm_peak_write(kkm_ctx* c, void* buf, size_t bytes, float value, int32_t rep
                        "peak write");
 }
 
+int kkm_peak_read_rows(kkm_ctx* c, const void* buf, int64_t nrows, int64_t ld, const int32_t* rows, int32_t nchunks,
+                       int32_t seg, float* sums, int32_t reps, float* ms_out) {
+  if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
+  if (!buf || !rows || !sums || !ms_out) return fail(c, KKM_ERR_ARG, "NULL argument");
+  if ((uintptr_t)buf % 16) return fail(c, KKM_ERR_ARG, "buf must be 16-byte aligned");
+  if (nrows < 1 || ld < 128 || ld % 4) return fail(c, KKM_ERR_ARG, "nrows=%lld must be >= 1 and ld=%lld a multiple of 4, >= 128", (long long)nrows, (long long)ld);
+  if (seg < 128 || seg % 128 || seg > ld) return fail(c, KKM_ERR_ARG, "seg=%d must be a positive multiple of 128, at most ld", seg);
+  // the launch's work-items (512 per workgroup) must fit the 32-bit grid
+  if (nchunks < 1 || (int64_t)nchunks * (ld / seg) * 512 > (int64_t)UINT32_MAX)
+    return fail(c, KKM_ERR_ARG, "nchunks=%d x %lld segments is out of range", nchunks, (long long)(ld / seg));
+  if (reps < 1) return fail(c, KKM_ERR_ARG, "reps=%d must be >= 1", reps);
+  return time_launches(c, reps, ms_out, [&] {
+        return launch_peak_rows((const float*)buf, nrows, ld, rows, nchunks, seg, sums, c->stream);
+      }, "peak rows");
+}
+
 int kkm_peak_mfma(kkm_ctx* c, int32_t iters, float* out, int32_t reps, float* ms_out, double* flops_out) {
   if (!c) return fail(nullptr, KKM_ERR_ARG, "ctx is NULL");
   if (!out || !ms_out || !flops_out) return fail(c, KKM_ERR_ARG, "NULL argument");

@@ -274,5 +274,8 @@ constexpr int kPeakMfmaGrid = 1024;
 hipError_t launch_peak_read(const void* buf, int64_t bytes, float* sums, hipStream_t s);
 hipError_t launch_peak_write(void* buf, int64_t bytes, float value, hipStream_t s);
 hipError_t launch_peak_mfma(int iters, float* out, hipStream_t s);
+// nchunks x (ld / seg) workgroups of 512 threads; seg a multiple of 128
+hipError_t launch_peak_rows(const float* buf, int64_t nrows, int64_t ld, const int* rows, int nchunks, int seg,
+                            float* sums, hipStream_t s);
 
 }  // namespace kkm

@@ -1,6 +1,7 @@
 // Achievable-peak microbenchmarks: a streaming read and a streaming write
-// of HBM with non-temporal 16-byte accesses, and a register loop of fp32
-// matrix-core instructions.  They measure what this GPU sustains, so that
+// of HBM with non-temporal 16-byte accesses, a streaming read of rows in the
+// packed SpMM's pattern, and a register loop of fp32 matrix-core
+// instructions.  They measure what this GPU sustains, so that
 // the per-kernel roofline fractions can be stated against measured peaks as
 // well as the datasheet ones.  Nothing on the clustering path calls them.
 #include "kkm_internal.h"
@@ -60,6 +61,52 @@ __global__ __launch_bounds__(256) void peak_write_kernel(peak_f4* __restrict__ p
   for (; i < hi; i += 256) __builtin_nontemporal_store(w, p + i);
 }
 
+// A streaming read of rows in the pattern of the packed SpMM's loads, without
+// its arithmetic.  Workgroup (chunk c, segment s), eight wavefronts, reads
+// rows rows[128c .. 128c + 127] of an nrows x ld fp32 matrix over columns
+// [s * seg, (s + 1) * seg); wavefront w takes rows 16w .. 16w + 15 of the
+// chunk, 128 columns per step: instruction g reads row 2g + h (h = lane / 32)
+// at columns 4 (lane % 32) .. +3, two rows of 512 contiguous bytes, and the
+// next step's loads are issued before the current step is added, so one
+// step is in flight per wavefront.  Row indices are clamped into
+// [0, nrows).  sums[c * nseg + s] = the workgroup's fp32 sum of what it read.
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4))) void peak_rows_kernel(
+    const float* __restrict__ A, int64_t nrows, int64_t ld, const int* __restrict__ rows, int nseg, int seg,
+    float* __restrict__ sums) {
+  const int c = (int)(blockIdx.x / (unsigned)nseg), s = (int)(blockIdx.x % (unsigned)nseg);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, c32 = lane & 31;
+  const float* rp[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    int64_t r = rows[(int64_t)c * 128 + w * 16 + 2 * g + h];
+    r = r < 0 ? 0 : (r >= nrows ? nrows - 1 : r);
+    rp[g] = A + r * ld + (int64_t)s * seg + 4 * c32;
+  }
+  const int steps = seg / 128;
+  peak_f4 buf[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) buf[g] = __builtin_nontemporal_load((const peak_f4*)rp[g]);
+  peak_f4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int t = 1; t <= steps; ++t) {
+    peak_f4 cur[8];
+#pragma unroll
+    for (int g = 0; g < 8; ++g) cur[g] = buf[g];
+    if (t < steps) {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) buf[g] = __builtin_nontemporal_load((const peak_f4*)(rp[g] + (int64_t)t * 128));
+    }
+#pragma unroll
+    for (int g = 0; g < 8; ++g) acc += cur[g];
+  }
+  float v = (acc.x + acc.y) + (acc.z + acc.w);
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __shared__ float part[8];
+  if (lane == 0) part[w] = v;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    sums[blockIdx.x] = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+}
+
 // Four independent accumulation chains of v_mfma_f32_32x32x2_f32 per
 // wavefront (32 x 32 x 2 x 2 = 4096 flop each); one float per wavefront out.
 __global__ __launch_bounds__(256) void peak_mfma_kernel(int iters, float* __restrict__ out) {
@@ -90,6 +137,14 @@ hipError_t launch_peak_read(const void* buf, int64_t bytes, float* sums, hipStre
 
 hipError_t launch_peak_write(void* buf, int64_t bytes, float value, hipStream_t s) {
   hipLaunchKernelGGL(peak_write_kernel, dim3(kPeakGrid), dim3(256), 0, s, (peak_f4*)buf, bytes / 16, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_peak_rows(const float* buf, int64_t nrows, int64_t ld, const int* rows, int nchunks, int seg,
+                            float* sums, hipStream_t s) {
+  const int nseg = (int)(ld / seg);
+  hipLaunchKernelGGL(peak_rows_kernel, dim3((unsigned)((int64_t)nchunks * nseg)), dim3(512), 0, s, buf, nrows, ld,
+                     rows, nseg, seg, sums);
   return hipGetLastError();
 }
 

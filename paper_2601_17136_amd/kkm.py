@@ -23,7 +23,7 @@ STORAGES = {"f32": KKM_STORE_F32, "f16": KKM_STORE_F16}
 KKM_MAX_K = 1024
 KKM_PACKED_MAX_K = 64
 KKM_PACKED_FAST_K = 64
-KKM_ABI_VERSION = 7
+KKM_ABI_VERSION = 8
 KKM_NOALLOC_SCRATCH_BYTES = 64 << 20
 PHASES = ("stage", "gemm", "fixup", "labels", "scatter", "spmm", "assign", "onthefly", "reduce", "other",
           "seed")
@@ -85,6 +85,8 @@ _SIGS = {
     "kkm_copy_diag": ([_vp, _vp], _i32),
     "kkm_set_timing": ([_vp, _i32], _i32),
     "kkm_peak_read": ([_vp, _vp, _sz, _vp, _i32, ctypes.POINTER(ctypes.c_float)], _i32),
+    "kkm_peak_read_rows": ([_vp, _vp, ctypes.c_int64, ctypes.c_int64, _vp, _i32, _i32, _vp, _i32,
+                            ctypes.POINTER(ctypes.c_float)], _i32),
     "kkm_peak_write": ([_vp, _vp, _sz, ctypes.c_float, _i32, ctypes.POINTER(ctypes.c_float)], _i32),
     "kkm_peak_mfma": ([_vp, _i32, _vp, _i32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_f64)], _i32),
     "kkm_get_timing": ([_vp, ctypes.POINTER(kkm_timing)], _i32),
@@ -372,6 +374,27 @@ def kkm_peak_read(ctx, buf, sums, reps: int = 1) -> float:
     ms = ctypes.c_float()
     _check(lib().kkm_peak_read(ctx, _dev_ptr(buf, torch.float32, "buf"), buf.numel() * 4,
                                _dev_ptr(sums, torch.float32, "sums"), int(reps), ctypes.byref(ms)), ctx)
+    return ms.value
+
+
+def kkm_peak_read_rows(ctx, buf, rows, seg: int, sums, reps: int = 1) -> float:
+    """Streaming read of rows in the packed SpMM's load pattern over the 2-D fp32
+    device tensor buf (nrows x ld): workgroup (c, s) reads rows[128c .. 128c + 127]
+    (int32 device tensor, clamped into range) over columns [s*seg, (s+1)*seg) and
+    writes its sum to sums[c * (ld // seg) + s].  Returns ms per launch."""
+    import torch
+    if buf.dim() != 2 or not buf.is_contiguous():
+        raise KKMError(KKM_ERR_ARG, "buf must be a contiguous 2-D tensor")
+    nrows, ld = buf.shape
+    if rows.numel() % 128 or rows.numel() == 0:
+        raise KKMError(KKM_ERR_ARG, "rows must hold a positive multiple of 128 indices")
+    nchunks = rows.numel() // 128
+    if seg > 0 and sums.numel() < nchunks * (ld // seg):
+        raise KKMError(KKM_ERR_ARG, f"sums must hold at least {nchunks * (ld // seg)} floats")
+    ms = ctypes.c_float()
+    _check(lib().kkm_peak_read_rows(ctx, _dev_ptr(buf, torch.float32, "buf"), nrows, ld,
+                                    _dev_ptr(rows, torch.int32, "rows"), nchunks, int(seg),
+                                    _dev_ptr(sums, torch.float32, "sums"), int(reps), ctypes.byref(ms)), ctx)
     return ms.value
 
 

@@ -35,9 +35,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert kkm.kkm_abi_version() == kkm.KKM_ABI_VERSION == 7
+    assert kkm.kkm_abi_version() == kkm.KKM_ABI_VERSION == 8
     hdr = open(HEADER).read()
-    assert "#define KKM_ABI_VERSION 7" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
+    assert "#define KKM_ABI_VERSION 8" in hdr and f"#define KKM_MAX_K {kkm.KKM_MAX_K}" in hdr
     assert f"KKM_NPHASE = {len(kkm.PHASES)}" in hdr
 
 
@@ -109,6 +109,7 @@ def test_null_context_is_rejected_without_a_gpu(L):
     assert L.kkm_peak_read(None, None, 16, None, 1, ctypes.byref(ms)) == kkm.KKM_ERR_ARG
     assert L.kkm_peak_write(None, None, 16, 1.0, 1, ctypes.byref(ms)) == kkm.KKM_ERR_ARG
     assert L.kkm_peak_mfma(None, 1, None, 1, ctypes.byref(ms), ctypes.byref(fl)) == kkm.KKM_ERR_ARG
+    assert L.kkm_peak_read_rows(None, None, 128, 128, None, 1, 128, None, 1, ctypes.byref(ms)) == kkm.KKM_ERR_ARG
 
 
 def test_plan_resident_when_it_fits(L):
