@@ -444,7 +444,10 @@ int kkm_get_info(kkm_ctx *ctx, kkm_info *out);
  * stream and writes the average launch time in ms to *ms_out (host); it
  * returns after the launches have completed.  Errors: KKM_ERR_ARG (NULL
  * pointers, bytes not a positive multiple of 16, a buffer not 16-byte
- * aligned, reps or iters < 1), KKM_ERR_HIP.
+ * aligned, reps or iters < 1; for kkm_peak_read_rows also nrows < 1, ld not
+ * a multiple of 4 or below 128, seg not a positive multiple of 128 or above
+ * ld, nchunks < 1, or more than 2^32 - 1 work-items in the launch),
+ * KKM_ERR_HIP.
  *  - kkm_peak_read: non-temporal 16-byte loads over buf (device, `bytes`
  *    bytes read as fp32), 2040 workgroups, each streaming a contiguous
  *    range 16 KB at a time; workgroup g writes the fp32 sum
