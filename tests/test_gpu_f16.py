@@ -144,17 +144,37 @@ def test_f16_halves_the_stored_bytes():
 @pytest.mark.parametrize("cfg,mode", [(2, "packed"), (2, "resident"), (3, "packed"), (4, "packed"), (5, "packed")])
 def test_f16_workload_step(oracle, cfg, mode):
     w_, X, cl = datagen.workload(cfg)
-    n, k = w_.n, w_.k
     print(f"[gpu] binary16 K full-size step: {w_.describe()} {mode}", flush=True)
-    kern = oracle.Kernel(w_.kind, w_.gamma, w_.coef0, w_.degree)
+    sampled_step(oracle, X, w_.kind, w_.gamma, w_.coef0, w_.degree, cl, w_.k, mode, cfg, f"cfg {cfg} {mode}")
+
+
+@pytest.mark.parametrize("kind,k", [("poly", 40), ("gauss", 64), ("linear", 20)])
+def test_f16_many_labels_tall_chunks(oracle, kind, k):
+    """Binary16 packed K with more than 16 labels above 40000 points: 128-row
+    chunks, 32-tile segments, two to four label blocks, two tiles per step."""
+    n, d = 45000, 48
+    X = datagen.make_points(5, n=n, d=d)[0]
+    cl = datagen.random_init(n, k, 40 + k)
+    g, c, p = {"poly": (1.0 / d, 1.0, 2), "linear": (1.0, 0.0, 1), "gauss": (1.0 / d, 0.0, 1)}[kind]
+    print(f"[gpu] binary16 packed, n={n} d={d} k={k} {kind}", flush=True)
+    sampled_step(oracle, X, kind, g, c, p, cl, k, "packed", k, f"n={n} k={k} {kind}")
+
+
+def sampled_step(oracle, X, kind, g, c, p, cl, k, mode, seed, label):
+    """One binary16 step against the oracle on sampled rows, within the storage
+    bounds; the step repeated on the same context gives the same bits."""
+    n = X.shape[0]
+    kern = oracle.Kernel(kind, g, c, p)
     rows = np.unique(np.concatenate([[0, 1, 127, 128, n // 2, n - 1],
-                                     np.random.default_rng(cfg).choice(n, 42, replace=False)]))
-    with Engine(X, w_.kind, w_.gamma, w_.coef0, w_.degree, mode=mode, storage="f16") as eng:
+                                     np.random.default_rng(seed).choice(n, 42, replace=False)]))
+    with Engine(X, kind, g, c, p, mode=mode, storage="f16") as eng:
         Krows = np.stack([eng.K_rows(int(r), int(r) + 1)[0] for r in rows])
         out = eng.step(cl, k)
+        again = eng.step(cl, k)
+    assert np.array_equal(out["E"], again["E"]) and out["J"] == again["J"]
     ref = oracle.step_rows(kern, X, cl, k, rows)
     diagK = kern.diag(X)
-    w = row_scales(X, w_.kind, w_.gamma, w_.coef0, w_.degree)
+    w = row_scales(X, kind, g, c, p)
     bK = U16 * np.abs(ref["K_rows"]) + SUB * np.maximum(w[rows][:, None], w[None, :])
     eK = check_within(Krows, ref["K_rows"], bK, "K rows")
     bE, bz, bD, bJ = bounds(ref["K_rows"], rows, diagK, w, cl, k)
@@ -164,7 +184,7 @@ def test_f16_workload_step(oracle, cfg, mode):
     eD = check_within(out["D"][rows], ref["D"], bD, "D")
     check_within([out["J"]], [ref["J"]], [bJ], "J")
     flips = check_ids(out["cl"][rows], ref["cl"], ref["D"], bD)
-    print(f"[gpu] cfg {cfg} {mode}: K {eK:.2e} E {eE:.2e} z {ez:.2e} D {eD:.2e}, id flips {flips}", flush=True)
+    print(f"[gpu] {label}: K {eK:.2e} E {eE:.2e} z {ez:.2e} D {eD:.2e}, id flips {flips}", flush=True)
 
 
 @pytest.mark.parametrize("cfg,mode", [(2, "packed"), (4, "resident")])
