@@ -347,15 +347,16 @@ int build_sweep_segments(int64_t n) {
   return nseg < 1 ? 1 : nseg;
 }
 
-template <int KIND, int HP>
+template <int KIND, int HP, bool PACKED>
 __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
     const float* __restrict__ Xp, const float* __restrict__ nrm, const unsigned* __restrict__ maxnrm_bits,
-    int64_t n, int64_t ld, bool packed, int nt, int nseg, KappaParams kp, float* __restrict__ K,
+    int64_t n, int64_t ld, int nt, int nseg, KappaParams kp, float* __restrict__ K,
     float* __restrict__ diagK, int2* __restrict__ fix_list, unsigned long long* __restrict__ fix_count,
     long long seg_cap, const float* __restrict__ bmax) {
   constexpr int d_pad = 2 * HP, ldsA = 2 * HP + 4;
   __shared__ __attribute__((aligned(16))) float As[kTile * ldsA];
-  __shared__ float Tm[4 * 32 * 65];  // per wavefront: a 32 x 64 block transposed (full storage)
+  __shared__ float Tm[PACKED ? 1 : 4 * 32 * 65];  // per wavefront: a 32 x 64 block transposed (full storage)
+  __shared__ __attribute__((aligned(16))) float Ns[kTile];  // Gaussian: the block's squared norms times cg
   // work items (segment s, row block I < sweep_seg_begin(s+1)), segment-major
   int s = 0;
   int64_t first = 0;
@@ -372,29 +373,42 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
                                                          __uint_as_float(*maxnrm_bits), kp);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const float cg = kp.neg_g_log2e;
   for (int f = tid; f < kTile * (HP / 2); f += 256) {  // the block's rows (zero padded past n)
     const int r = f / (HP / 2), c = f % (HP / 2);
     *(float4*)(As + r * ldsA + 4 * c) = *(const float4*)(Xp + (row0 + r) * d_pad + 4 * c);
   }
+  if (KIND == GAUSS && tid < kTile) Ns[tid] = cg * nrm[row0 + tid];  // nrm is zero past n
   __syncthreads();
   const float* const Aw = As + wm * 64 * ldsA;
   float* const Tw = Tm + wave * (32 * 65);
-  const float cg = kp.neg_g_log2e;
-  const float* nrow = nrm + row0 + wm * 64 + 4 * h;
-  const int64_t S = packed ? ld - row0 : ld;  // row stride of the block's stored rows
-  float* const Kr = K + (packed ? packed_row(row0, ld) : row0 * ld);
+  const float* const nrow = Ns + wm * 64 + 4 * h;  // this lane's rows' cg * |x|^2, from LDS
+  const int64_t S = PACKED ? ld - row0 : ld;  // row stride of the block's stored rows
+  float* const Kr = K + (PACKED ? packed_row(row0, ld) : row0 * ld);
   const unsigned lane_b = ((unsigned)(wm * 64 + 4 * h) * (unsigned)S + (unsigned)(wn * 64 + l32)) * 4u;
+
+  // Tile J's column operands and (Gaussian) column norms.  They are loaded
+  // for the next tile before this tile's stores are issued: loads and stores
+  // share one in-order completion counter, so a load issued after the stores
+  // would make the next tile's products wait for the stores to drain.  The
+  // rows' norms come from LDS for the same reason.
+  float b[2][HP];
+  float nj[2] = {0.f, 0.f};  // the columns' squared norms (scaled where used, so nothing waits here)
+  auto fetch = [&](int J, int q) {  // column block q (32 columns) of tile J
+    const int64_t c = (int64_t)J * kTile + wn * 64 + q * 32 + l32;
+    load_operand<HP>(Xp, c, d_pad, h, b[q]);
+    if (KIND == GAUSS) nj[q] = nrm[c];
+  };
+  if (jt0 < jt1) {
+    fetch(jt0, 0);
+    fetch(jt0, 1);
+  }
 
   for (int J = jt0; J < jt1; ++J) {
     const int64_t col0 = (int64_t)J * kTile;
     floatx16 acc[2][2];
-    {
-      float b[2][HP];
-#pragma unroll
-      for (int q = 0; q < 2; ++q) load_operand<HP>(Xp, col0 + wn * 64 + q * 32 + l32, d_pad, h, b[q]);
-      mma_rows_lds<HP>(Aw, b[0], acc[0][0], acc[1][0], l32, h);
-      mma_rows_lds<HP>(Aw, b[1], acc[0][1], acc[1][1], l32, h);
-    }
+    mma_rows_lds<HP>(Aw, b[0], acc[0][0], acc[1][0], l32, h);
+    mma_rows_lds<HP>(Aw, b[1], acc[0][1], acc[1][1], l32, h);
     __builtin_amdgcn_sched_barrier(0);
 
     // kappa, as in gemm_kappa_kernel, with the fix-up estimate kept as one
@@ -402,8 +416,8 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
     // largest squared norms allow an entry of the tile to qualify
     float cnj[2] = {0.f, 0.f};
     if (KIND == GAUSS) {
-      cnj[0] = cg * nrm[col0 + wn * 64 + l32];
-      cnj[1] = cg * nrm[col0 + wn * 64 + 32 + l32];
+      cnj[0] = cg * nj[0];
+      cnj[1] = cg * nj[1];
     }
     const bool tile_fix = KIND == GAUSS && may_fix && gauss_needs_fix(1.f, bmax[I], bmax[J], kp);
     float umin = 0.f;
@@ -415,7 +429,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
         for (int q = 0; q < 4; ++q) {
           float4 n4 = {0.f, 0.f, 0.f, 0.f};
           if (KIND == GAUSS) n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
-          const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
+          const float cn[4] = {n4.x, n4.y, n4.z, n4.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -457,7 +471,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const float4 n4 = *(const float4*)(nrow + bi * 32 + 8 * q);
-          const float cn[4] = {cg * n4.x, cg * n4.y, cg * n4.z, cg * n4.w};
+          const float cn[4] = {n4.x, n4.y, n4.z, n4.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int64_t gi = row0 + wm * 64 + bi * 32 + 8 * q + 4 * h + e;
@@ -496,29 +510,40 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
       }
     }
 
-    // stores of tile (I, J) straight from the MFMA layout (see gemm_kappa_kernel)
-    {
-      char* const Kc = (char*)(Kr + col0);
-      const bool full = row0 + kTile <= n && col0 + kTile <= n;
+    // stores of tile (I, J) straight from the MFMA layout (see gemm_kappa_kernel),
+    // rows 0-31 of each wavefront's block (bi = 0), then rows 32-63
+    char* const Kc = (char*)(Kr + col0);
+    const bool full = row0 + kTile <= n && col0 + kTile <= n;
+    auto store_rows = [&](int bi) {
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int iu = bi * 32 + 8 * (r >> 2) + (r & 3);
-          char* const rowp = Kc + (size_t)iu * (size_t)S * 4u;
-          const float v0 = acc[bi][0][r], v1 = acc[bi][1][r];
-          if (full) {
-            __builtin_nontemporal_store(v0, (float*)(rowp + lane_b));
-            __builtin_nontemporal_store(v1, (float*)(rowp + lane_b + 128u));
-            continue;
-          }
-          if (row0 + wm * 64 + 4 * h + iu >= n) continue;
-          const int64_t j0 = col0 + wn * 64 + l32, j1 = j0 + 32;
-          if (j0 < ld) __builtin_nontemporal_store(j0 < n ? v0 : 0.f, (float*)(rowp + lane_b));
-          if (j1 < ld) __builtin_nontemporal_store(j1 < n ? v1 : 0.f, (float*)(rowp + lane_b + 128u));
+      for (int r = 0; r < 16; ++r) {
+        const int iu = bi * 32 + 8 * (r >> 2) + (r & 3);
+        char* const rowp = Kc + (size_t)iu * (size_t)S * 4u;
+        const float v0 = acc[bi][0][r], v1 = acc[bi][1][r];
+        if (full) {
+          __builtin_nontemporal_store(v0, (float*)(rowp + lane_b));
+          __builtin_nontemporal_store(v1, (float*)(rowp + lane_b + 128u));
+          continue;
         }
-    }
-    if (J != I && !packed) {  // tile (J, I) of full storage: rows j, columns i
+        if (row0 + wm * 64 + 4 * h + iu >= n) continue;
+        const int64_t j0 = col0 + wn * 64 + l32, j1 = j0 + 32;
+        if (j0 < ld) __builtin_nontemporal_store(j0 < n ? v0 : 0.f, (float*)(rowp + lane_b));
+        if (j1 < ld) __builtin_nontemporal_store(j1 < n ? v1 : 0.f, (float*)(rowp + lane_b + 128u));
+      }
+    };
+    // Packed storage: the next tile's first column block is requested between
+    // the two halves of this tile's stores, in registers the products no
+    // longer need, so the next tile's first pass of products overlaps the
+    // second half of the stores.  (Full storage needs the whole tile for its
+    // mirror below, and fetches after it.)
+    store_rows(0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PACKED && J + 1 < jt1) fetch(J + 1, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    store_rows(1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PACKED && J + 1 < jt1) fetch(J + 1, 1);
+    if (!PACKED && J != I) {  // tile (J, I) of full storage: rows j, columns i
 #pragma unroll
       for (int bj = 0; bj < 2; ++bj) {
 #pragma unroll
@@ -544,6 +569,10 @@ __global__ __launch_bounds__(256, 2) void gemm_kappa_sweep_kernel(
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
     }
+    if (!PACKED && J + 1 < jt1) {
+      fetch(J + 1, 0);
+      fetch(J + 1, 1);
+    }
   }
 }
 
@@ -559,9 +588,16 @@ hipError_t launch_gemm_kappa(const float* Xp, const float* nrm, const unsigned* 
     int64_t items = 0;
     for (int q = 0; q < ns; ++q) items += sweep_seg_begin(q + 1, (int)nt, ns);
     const dim3 sgrid((unsigned)items), sblock(256);
-#define KKM_SWEEP(KIND, HP)                                                                             \
-  hipLaunchKernelGGL((gemm_kappa_sweep_kernel<KIND, HP>), sgrid, sblock, 0, s, Xp, nrm, maxnrm_bits, n, ld, \
-                     packed, (int)nt, ns, kp, (float*)K, diagK, fix_list, fix_count, seg_cap, bmax)
+#define KKM_SWEEP(KIND, HP)                                                                                  \
+  do {                                                                                                       \
+    if (packed)                                                                                              \
+      hipLaunchKernelGGL((gemm_kappa_sweep_kernel<KIND, HP, true>), sgrid, sblock, 0, s, Xp, nrm, maxnrm_bits, \
+                         n, ld, (int)nt, ns, kp, (float*)K, diagK, fix_list, fix_count, seg_cap, bmax);        \
+    else                                                                                                     \
+      hipLaunchKernelGGL((gemm_kappa_sweep_kernel<KIND, HP, false>), sgrid, sblock, 0, s, Xp, nrm,             \
+                         maxnrm_bits, n, ld, (int)nt, ns, kp, (float*)K, diagK, fix_list, fix_count, seg_cap,  \
+                         bmax);                                                                              \
+  } while (0)
 #define KKM_SWEEP_HP(KIND)                     \
   switch (d_pad / 2) {                         \
     case 4: KKM_SWEEP(KIND, 4); break;         \
